@@ -1,0 +1,174 @@
+/*
+ * pblock.h — C ABI of the MI355X (gfx950) parallel transformer block library.
+ *
+ * The block is Eq. 2 of MegaScale (Section 3.1):
+ *
+ *     y = x + MLP(LN(x)) + Attention(LN(x))
+ *
+ * with ONE LayerNorm whose output h feeds both branches, a fused in-projection
+ * Z = h W_in^T + b_in whose columns are [Q | K | V | U], causal sliding-window
+ * attention (Section 3.1, "Sliding window attention") on Q, K, V, the GeLU MLP
+ * activation G = gelu(U), and one fused out-projection over C = [O | G]:
+ *
+ *     y = x + C W_out^T + b_out.
+ *
+ * Window rule: query i attends to key j of the same batch row iff
+ * 0 <= i - j < window (window keys, the query's own position included);
+ * window >= seq is ordinary causal attention.  Scores are scaled by
+ * 1/sqrt(head_dim).  LayerNorm uses the biased variance with eps inside the
+ * square root.  GeLU is the tanh form when gelu_tanh != 0, else the erf form.
+ *
+ * Section 3.3 replaces attention with FlashAttention-2 and LN/GeLU with fused
+ * kernels; this library does the same on gfx950 (banded flash-style attention
+ * that skips key tiles outside the window, MFMA GEMMs with fused bias / GeLU /
+ * residual epilogues).  None of that changes the result beyond rounding.
+ *
+ * ---------------------------------------------------------------- layouts
+ * All tensors are dense, row-major, in device memory (HBM), 16-byte aligned.
+ * Let T = batch*seq, H = hidden, A = heads*head_dim, F = ffn,
+ *     N_in = 3A + F, K_out = A + F.
+ *   x, y, dy, dx  [T, H]          activation dtype (bf16 or fp32), token-major
+ *   ln_gamma/beta [H]             activation dtype
+ *   w_in          [N_in, H]       activation dtype; rows Q | K | V | MLP-up;
+ *                                 head h owns rows h*d .. h*d+d-1 of each of
+ *                                 Q, K and V (d = head_dim)
+ *   b_in          [N_in]          activation dtype
+ *   w_out         [H, K_out]      activation dtype; columns attention-out |
+ *                                 MLP-down (the two output projections of
+ *                                 Eq. 2, side by side)
+ *   b_out         [H]             activation dtype: the sum of the attention
+ *                                 and MLP output biases (only their sum enters
+ *                                 Eq. 2)
+ *   dgamma, dbeta [H], dw_in [N_in, H], db_in [N_in], dw_out [H, K_out],
+ *   db_out [H]                    fp32, always
+ *
+ * Saved stash (forward -> backward), regions in this order, each starting at
+ * a 256-byte boundary (see pblock_saved_offsets):
+ *   h     [T, H]      act   LN output
+ *   z     [T, N_in]   act   Q | K | V | U  (U before GeLU)
+ *   c     [T, K_out]  act   O | G          (attention output, GeLU output)
+ *   mean  [T]         fp32  LN row mean
+ *   rstd  [T]         fp32  LN row 1/sqrt(var + eps)
+ *   lse   [batch, heads, seq] fp32  log of each softmax denominator, in the
+ *                     scaled-score domain
+ *
+ * ---------------------------------------------------------------- ownership
+ * The caller allocates every buffer (inputs, outputs, the stash, the
+ * workspace).  The library allocates no device memory and keeps no per-call
+ * state.  Every call is asynchronous on the given HIP stream; buffers must stay
+ * valid until the stream has passed the call.  Calls on disjoint buffers may
+ * run concurrently.  Parameter gradients are overwritten, not accumulated.
+ *
+ * ---------------------------------------------------------------- errors
+ * Functions return a pb_status.  Arguments are checked on the host before any
+ * HIP call is made; on a failed check nothing is launched and
+ * pblock_last_error() describes the problem.  PB_ERR_HIP reports a launch
+ * failure (hipGetLastError after the launches).  Nothing throws, aborts or
+ * exits across this interface.
+ */
+#ifndef PBLOCK_H
+#define PBLOCK_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { PB_BF16 = 0, PB_F32 = 1 } pb_dtype;
+
+typedef enum {
+  PB_OK = 0,
+  PB_ERR_INVALID_ARG = 1, /* null/misaligned pointer, non-positive size ... */
+  PB_ERR_UNSUPPORTED = 2, /* a shape this build has no kernel for          */
+  PB_ERR_WORKSPACE = 3,   /* workspace smaller than pblock_workspace_bytes */
+  PB_ERR_HIP = 4          /* a kernel launch failed                        */
+} pb_status;
+
+typedef struct {
+  int batch;     /* >= 1                                                    */
+  int seq;       /* >= 1                                                    */
+  int hidden;    /* H >= 8, multiple of 8, <= 32768                         */
+  int heads;     /* >= 1                                                    */
+  int head_dim;  /* 64 or 128                                               */
+  int ffn;       /* F >= 8, multiple of 8                                   */
+  int window;    /* >= 1; keys seen per query, itself included              */
+  float ln_eps;  /* > 0, e.g. 1e-5                                          */
+  int gelu_tanh; /* 1: tanh form of GeLU, 0: erf form                      */
+  pb_dtype dtype;/* storage type of activations and parameters              */
+} pb_config;
+
+/* Checks a configuration on the host.  Makes no HIP call. */
+pb_status pblock_validate(const pb_config* cfg);
+
+/* Bytes of the forward -> backward stash described above (0 on a bad cfg). */
+size_t pblock_saved_bytes(const pb_config* cfg);
+
+/* Byte offsets of the stash regions, in the order h, z, c, mean, rstd, lse.
+ * offsets must hold 6 entries.  Host only. */
+pb_status pblock_saved_offsets(const pb_config* cfg, size_t* offsets);
+
+/* Workspace bytes for pblock_forward (backward == 0; needed only when the
+ * forward call gets saved == NULL, which then keeps its stash in the
+ * workspace) or for pblock_backward (backward != 0).  0 on a bad cfg. */
+size_t pblock_workspace_bytes(const pb_config* cfg, int backward);
+
+/* Forward pass of the block (Eq. 2).  Writes y [T, H].  When saved is not
+ * NULL it also fills the stash that pblock_backward reads; when it is NULL
+ * (inference) the stash goes to ws, which must then hold
+ * pblock_workspace_bytes(cfg, 0) bytes.  ws may be NULL when saved is not. */
+pb_status pblock_forward(const pb_config* cfg, const void* x,
+                         const void* ln_gamma, const void* ln_beta,
+                         const void* w_in, const void* b_in,
+                         const void* w_out, const void* b_out,
+                         void* y, void* saved, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+/* Backward pass: the gradients of sum(y * dy) with respect to x and every
+ * parameter, given the stash of the matching forward call.  dx is in the
+ * activation dtype; the six parameter gradients are fp32 and overwritten.
+ * ws must hold pblock_workspace_bytes(cfg, 1) bytes. */
+pb_status pblock_backward(const pb_config* cfg, const void* x,
+                          const void* ln_gamma, const void* ln_beta,
+                          const void* w_in, const void* b_in,
+                          const void* w_out, const void* b_out,
+                          const void* saved, const void* dy, void* dx,
+                          float* dgamma, float* dbeta, float* dw_in,
+                          float* db_in, float* dw_out, float* db_out,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Causal sliding-window attention alone (Section 3.1 SWA; the exact
+ * FlashAttention-2 result of Section 3.3), for all heads of all batch rows.
+ * q, k, v: element (b, s, head, e) at ptr[(b*seq + s)*ld + head*head_dim + e],
+ * ld in elements (>= heads*head_dim, multiple of 8).  o uses ld_o the same
+ * way.  lse [batch, heads, seq] fp32 as in the stash.  Reads cfg->batch, seq,
+ * heads, head_dim, window and dtype only.  No workspace. */
+pb_status pblock_swattn_forward(const pb_config* cfg, const void* q,
+                                const void* k, const void* v, int ld_qkv,
+                                void* o, int ld_o, float* lse,
+                                hipStream_t stream);
+
+/* Gradient of pblock_swattn_forward: given q, k, v, o (ld_o), lse and the
+ * output gradient d_o (ld_do), writes dq, dk, dv (ld_dqkv).  ws must hold
+ * pblock_swattn_workspace_bytes(cfg) bytes (one fp32 softmax row term per
+ * query).  Deterministic: no atomics. */
+size_t pblock_swattn_workspace_bytes(const pb_config* cfg);
+pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
+                                 const void* k, const void* v, int ld_qkv,
+                                 const void* o, int ld_o, const void* d_o,
+                                 int ld_do, const float* lse, void* dq,
+                                 void* dk, void* dv, int ld_dqkv, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
+/* Human-readable name of a status, and a description of the most recent
+ * failed check on the calling thread ("" if none). */
+const char* pblock_status_string(pb_status status);
+const char* pblock_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PBLOCK_H */

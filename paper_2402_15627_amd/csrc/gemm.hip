@@ -1,0 +1,323 @@
+// Projection GEMMs of the parallel block with fused epilogues.
+//
+// bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 256x256 output tile per
+// workgroup of four waves (each wave 128x128), K-tile 64, double-buffered
+// LDS (128 KB).  LDS holds both operands K-contiguous, 128-byte rows with
+// the 16-byte chunk index XOR-swizzled by the row so that fragment reads and
+// tile writes touch distinct banks.  An operand that is M- or N-contiguous in
+// HBM (the token-contracted weight-gradient GEMMs, and the weights of the
+// input-gradient GEMMs) is loaded as 8x8 blocks and transposed in registers
+// on its way into LDS.  The MFMA is issued with the roles of the operands
+// swapped (the N tile as MFMA "A"), so each lane ends up holding four
+// consecutive output columns of one row: 8- or 16-byte epilogue stores.
+//
+// The epilogues carry the block's elementwise work (MegaScale Section 3.3
+// fuses these fine-grained ops): in-projection bias + GeLU writing both U and
+// G, out-projection bias + residual, and the GeLU derivative in the backward
+// pass.
+//
+// fp32 path: a plain LDS-tiled SIMT kernel with the same epilogues.
+#include "common.h"
+#include "kernels.h"
+
+namespace pb {
+namespace {
+
+// ------------------------------------------------------------- epilogues
+template <typename T, Epi EPI>
+PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
+  if constexpr (EPI == Epi::StoreF32) {
+    store4((float*)ep.out + (size_t)m * ep.ld_out + n, v);
+  } else if constexpr (EPI == Epi::BiasGelu) {
+    float b[4], z[4];
+    load4((const T*)ep.bias + n, b);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) z[e] = v[e] + b[e];
+    store4((T*)ep.out + (size_t)m * ep.ld_out + n, z);
+    if (n >= ep.split) {
+      float g[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) g[e] = gelu(z[e], ep.gelu_tanh != 0);
+      store4((T*)ep.out2 + (size_t)m * ep.ld_out2 + (n - ep.split) + ep.col2, g);
+    }
+  } else if constexpr (EPI == Epi::BiasResid) {
+    float b[4], r[4], o[4];
+    load4((const T*)ep.bias + n, b);
+    load4((const T*)ep.resid + (size_t)m * ep.ld_out + n, r);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = v[e] + b[e] + r[e];
+    store4((T*)ep.out + (size_t)m * ep.ld_out + n, o);
+  } else {  // DgeluSplit
+    if (n < ep.split) {
+      store4((T*)ep.out + (size_t)m * ep.ld_out + n, v);
+    } else {
+      const size_t off = (size_t)m * ep.ld_out2 + (n - ep.split) + ep.col2;
+      float u[4], o[4];
+      load4((const T*)ep.aux + off, u);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = v[e] * gelu_grad(u[e], ep.gelu_tanh != 0);
+      store4((T*)ep.out2 + off, o);
+    }
+  }
+}
+
+// --------------------------------------------------------- bf16 MFMA GEMM
+constexpr int kBM = 256, kBN = 256, kBK = 64;
+constexpr int kThreads = 256;
+constexpr int kTileBytes = kBM * kBK * 2;  // one operand tile (32 KB)
+
+// 16-byte chunk c (0..7) of LDS row `row` lives at physical chunk swz(row, c).
+PB_DEV int swz(int row, int c) { return c ^ ((row ^ (row >> 3)) & 7); }
+
+// Tile order: workgroup b runs on XCD b % 8; give each XCD a contiguous run
+// of logical tiles, then walk tiles in groups of 8 tile-rows so that
+// concurrently running workgroups on one XCD share operand strips in its L2.
+PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nt = tiles_m * tiles_n;
+  const int bid = blockIdx.x;
+  const int q = nt / 8, r = nt % 8, x = bid % 8;
+  const int lid = x * q + min(x, r) + bid / 8;
+  constexpr int G = 8;
+  const int per_group = G * tiles_n;
+  const int group = lid / per_group;
+  const int first_m = group * G;
+  const int gsize = min(tiles_m - first_m, G);
+  const int in_group = lid - group * per_group;
+  tm = first_m + in_group % gsize;
+  tn = in_group / gsize;
+}
+
+// Load one 256 x 64 operand tile into registers.  KC: the operand is
+// K-contiguous (row r of the tile at X[(R0 + r) * ld + k]); otherwise it is
+// MN-contiguous (X[k * ld + R0 + r]).  Rows past Rmax are clamped (their
+// results are never stored); k past K reads as zero.
+template <bool KC>
+PB_DEV void load_tile(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k0, int K,
+                      u32x4* r) {
+  const int tid = threadIdx.x;
+  if constexpr (KC) {
+    const int c = tid & 7;
+    const int k = k0 + 8 * c;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      int row = R0 + (tid >> 3) + 32 * i;
+      row = row < Rmax ? row : Rmax - 1;
+      r[i] = k < K ? *reinterpret_cast<const u32x4*>(X + (size_t)row * ld + k) : u32x4{0, 0, 0, 0};
+    }
+  } else {
+    const int col = R0 + 8 * (tid & 31);
+    const int kb = tid >> 5;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = k0 + 8 * kb + j;
+      r[j] = (k < K && col < Rmax) ? *reinterpret_cast<const u32x4*>(X + (size_t)k * ld + col)
+                                   : u32x4{0, 0, 0, 0};
+    }
+  }
+}
+
+template <bool KC>
+PB_DEV void store_tile(u32x4* __restrict__ lds, const u32x4* r) {
+  const int tid = threadIdx.x;
+  if constexpr (KC) {
+    const int c = tid & 7;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int row = (tid >> 3) + 32 * i;
+      lds[row * 8 + swz(row, c)] = r[i];
+    }
+  } else {
+    u32x4 t[8];
+    transpose8x8(r, t);
+    const int mb = tid & 31, kb = tid >> 5;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int row = 8 * mb + i;
+      lds[row * 8 + swz(row, kb)] = t[i];
+    }
+  }
+}
+
+template <bool AK, bool BK, Epi EPI>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __restrict__ A,
+                                                                int lda,
+                                                                const bf16* __restrict__ B,
+                                                                int ldb, int M, int N, int K,
+                                                                EpiArgs ep) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  // stage s: A tile at smem + 2 s * kTileBytes, B tile right after it
+  u32x4* const lds0 = reinterpret_cast<u32x4*>(smem);
+  constexpr int kTileVec = kTileBytes / 16;
+  auto lds_a = [&](int s) { return lds0 + 2 * s * kTileVec; };
+  auto lds_b = [&](int s) { return lds0 + (2 * s + 1) * kTileVec; };
+
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave & 1) * 128, wn = (wave >> 1) * 128;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  u32x4 ra[8], rb[8];
+  const int nk = (K + kBK - 1) / kBK;
+  load_tile<AK>(A, lda, m0, M, 0, K, ra);
+  load_tile<BK>(B, ldb, n0, N, 0, K, rb);
+  store_tile<AK>(lds_a(0), ra);
+  store_tile<BK>(lds_b(0), rb);
+  __syncthreads();
+
+  const int fr = lane & 31, fh = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      load_tile<AK>(A, lda, m0, M, (kt + 1) * kBK, K, ra);
+      load_tile<BK>(B, ldb, n0, N, (kt + 1) * kBK, K, rb);
+    }
+    const u32x4* la = lds_a(cur);
+    const u32x4* lb = lds_b(cur);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int c = 2 * ks + fh;
+      bf16x8 fa[4], fb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = wm + 32 * i + fr;
+        fa[i] = __builtin_bit_cast(bf16x8, la[row * 8 + swz(row, c)]);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = wn + 32 * j + fr;
+        fb[j] = __builtin_bit_cast(bf16x8, lb[row * 8 + swz(row, c)]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) {
+      store_tile<AK>(lds_a(cur ^ 1), ra);
+      store_tile<BK>(lds_b(cur ^ 1), rb);
+    }
+    __syncthreads();
+  }
+
+  // acc[i][j][4*jj + e] is C(m, n) with m = wm + 32 i + (lane & 31) and
+  // n = wn + 32 j + 8 jj + 4 (lane >> 5) + e.
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + wm + 32 * i + fr;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int n = n0 + wn + 32 * j + 8 * jj + 4 * fh;
+        if (n < N) {
+          float v[4] = {acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
+                        acc[i][j][4 * jj + 3]};
+          epi_store4<bf16, EPI>(ep, m, n, v);
+        }
+      }
+  }
+}
+
+// ----------------------------------------------------------- fp32 SIMT GEMM
+constexpr int kSB = 64, kSK = 16;
+
+template <bool AK, bool BK, Epi EPI>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, int lda,
+                                                       const float* __restrict__ B, int ldb,
+                                                       int M, int N, int K, EpiArgs ep) {
+  __shared__ float as[kSK][kSB + 4];
+  __shared__ float bs[kSK][kSB + 4];
+  const int m0 = blockIdx.y * kSB, n0 = blockIdx.x * kSB;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += kSK) {
+    for (int e = threadIdx.x; e < kSB * kSK; e += 256) {
+      const int r = e / kSK, kk = e % kSK;  // r: m or n within the tile
+      const int k = k0 + kk;
+      const int m = m0 + r, n = n0 + r;
+      float av = 0.f, bv = 0.f;
+      if (k < K && m < M) av = AK ? A[(size_t)m * lda + k] : A[(size_t)k * lda + m];
+      if (k < K && n < N) bv = BK ? B[(size_t)n * ldb + k] : B[(size_t)k * ldb + n];
+      as[kk][r] = av;
+      bs[kk][r] = bv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kSK; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = as[kk][ty * 4 + i];
+        b[i] = bs[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i, n = n0 + tx * 4;
+    if (m < M && n < N) epi_store4<float, EPI>(ep, m, n, acc[i]);
+  }
+}
+
+template <bool AK, bool BK, Epi EPI>
+void gemm_dispatch_layout(Dt dt, const void* A, int lda, const void* B, int ldb, int M, int N,
+                          int K, const EpiArgs& ep, hipStream_t s) {
+  if (dt == Dt::BF16) {
+    const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+    const size_t lds = 4 * (size_t)kTileBytes;
+    gemm_bf16_kernel<AK, BK, EPI><<<tiles, kThreads, lds, s>>>(
+        (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
+  } else {
+    dim3 grid((N + kSB - 1) / kSB, (M + kSB - 1) / kSB);
+    gemm_f32_kernel<AK, BK, EPI><<<grid, 256, 0, s>>>((const float*)A, lda, (const float*)B,
+                                                      ldb, M, N, K, ep);
+  }
+}
+
+template <Epi EPI>
+void gemm_dispatch(Dt dt, bool ak, bool bk, const void* A, int lda, const void* B, int ldb,
+                   int M, int N, int K, const EpiArgs& ep, hipStream_t s) {
+  if (ak && bk) gemm_dispatch_layout<true, true, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  else if (ak) gemm_dispatch_layout<true, false, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  else if (bk) gemm_dispatch_layout<false, true, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  else gemm_dispatch_layout<false, false, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
+}
+
+}  // namespace
+
+void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,
+                 const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, hipStream_t s) {
+  switch (epi) {
+    case Epi::StoreF32:
+      gemm_dispatch<Epi::StoreF32>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      break;
+    case Epi::BiasGelu:
+      gemm_dispatch<Epi::BiasGelu>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      break;
+    case Epi::BiasResid:
+      gemm_dispatch<Epi::BiasResid>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      break;
+    case Epi::DgeluSplit:
+      gemm_dispatch<Epi::DgeluSplit>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      break;
+  }
+}
+
+}  // namespace pb

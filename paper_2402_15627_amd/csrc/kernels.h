@@ -1,0 +1,78 @@
+// Host-side launchers of the block's kernels.  Each returns nothing; the
+// caller checks hipGetLastError() after its launch sequence.  Shapes are
+// validated by the C-ABI layer before any launcher runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace pb {
+
+enum class Dt { BF16, F32 };
+
+// ---------------------------------------------------------------- LayerNorm
+// h = gamma * (x - mean) * rstd + beta per row of x [rows, H].
+void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta, void* h,
+                       float* mean, float* rstd, int rows, int H, float eps, hipStream_t s);
+// dx = dy + rstd * (g - mean(g) - xhat * mean(g * xhat)), g = gamma * dh, per
+// row; per-block partial column sums of dh * xhat and dh go to part_dgamma and
+// part_dbeta [ln_backward_blocks(rows), H].
+int ln_backward_blocks(int rows);
+void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
+                        const void* gamma, const float* dh, const void* dy, void* dx,
+                        float* part_dgamma, float* part_dbeta, int rows, int H, hipStream_t s);
+
+// ------------------------------------------------------------ column sums
+// out[c] = sum over r of src[r * ld + c] for a [rows, cols] matrix (cols a
+// multiple of 8).  Deterministic two-stage reduction through part, which holds
+// colsum_partial_floats(rows, cols) floats.
+size_t colsum_partial_floats(int rows, int cols);
+void launch_colsum(Dt dt, const void* src, int ld, int rows, int cols, float* part, float* out,
+                   hipStream_t s);
+void launch_colsum_f32(const float* src, int ld, int rows, int cols, float* part, float* out,
+                       hipStream_t s);
+
+// ------------------------------------------------------------------ GEMMs
+// C[m, n] = sum_k A(m, k) B(k, n), fp32 accumulation.
+// A(m, k) is A[m * lda + k] when a_kcontig, else A[k * lda + m]; B(k, n) is
+// B[n * ldb + k] when b_kcontig, else B[k * ldb + n].
+enum class Epi {
+  StoreF32,    // out_f32[m * ld_out + n] = acc
+  BiasGelu,    // z = acc + bias[n] -> out[m * ld_out + n]; for n >= split also
+               // gelu(z) -> out2[m * ld_out2 + (n - split) + col2]
+  BiasResid,   // out[m * ld_out + n] = acc + bias[n] + resid[m * ld_out + n]
+  DgeluSplit,  // n < split: out[m * ld_out + n] = acc;
+               // n >= split: with c = n - split + col2,
+               //   out2[m * ld_out2 + c] = acc * gelu'(aux[m * ld_out2 + c])
+};
+struct EpiArgs {
+  void* out = nullptr;
+  int ld_out = 0;
+  void* out2 = nullptr;
+  int ld_out2 = 0;
+  const void* bias = nullptr;
+  const void* resid = nullptr;
+  const void* aux = nullptr;
+  int split = 0;
+  int col2 = 0;
+  int gelu_tanh = 1;
+};
+void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,
+                 const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, hipStream_t s);
+
+// -------------------------------------------------------------- attention
+// Causal sliding-window attention over [batch, seq] rows; q/k/v/o/do/dq/dk/dv
+// element (b, t, head, e) at ptr[(b * seq + t) * ld + head * head_dim + e].
+struct AttnShape {
+  int batch, seq, heads, head_dim, window;
+};
+void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
+                         int ld_qkv, void* o, int ld_o, float* lse, hipStream_t s);
+// delta[b, head, t] = sum_e do * o (softmax row term of the backward pass).
+// o uses ld_o, d_o uses ld_do; delta holds batch*heads*seq floats.
+void launch_attn_backward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
+                          int ld_qkv, const void* o, int ld_o, const void* d_o, int ld_do,
+                          const float* lse, float* delta, void* dq, void* dk, void* dv, int ld_d,
+                          hipStream_t s);
+
+}  // namespace pb

@@ -1,0 +1,440 @@
+// C ABI of the parallel transformer block library: argument checks (host
+// only, before any HIP call), stash / workspace layout, and the kernel
+// sequence of the forward and backward passes on the caller's stream.
+#include "pblock.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+pb_status fail(pb_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+struct Dims {
+  long long T, H, A, F, N_in, K_out, heads, d, B, S, W;
+  size_t esz;  // bytes per activation element
+};
+
+Dims dims_of(const pb_config* c) {
+  Dims d;
+  d.B = c->batch;
+  d.S = c->seq;
+  d.T = (long long)c->batch * c->seq;
+  d.H = c->hidden;
+  d.heads = c->heads;
+  d.d = c->head_dim;
+  d.A = (long long)c->heads * c->head_dim;
+  d.F = c->ffn;
+  d.N_in = 3 * d.A + d.F;
+  d.K_out = d.A + d.F;
+  d.W = c->window;
+  d.esz = c->dtype == PB_BF16 ? 2 : 4;
+  return d;
+}
+
+constexpr long long kMaxInt = 2147483647LL;
+
+pb_status check_config(const pb_config* c) {
+  if (!c) return fail(PB_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->dtype != PB_BF16 && c->dtype != PB_F32)
+    return fail(PB_ERR_INVALID_ARG, "dtype %d is neither PB_BF16 nor PB_F32", (int)c->dtype);
+  if (c->batch < 1 || c->seq < 1 || c->heads < 1 || c->window < 1)
+    return fail(PB_ERR_INVALID_ARG, "batch, seq, heads and window must be >= 1");
+  if (c->hidden < 8 || c->hidden % 8)
+    return fail(PB_ERR_INVALID_ARG, "hidden=%d must be a positive multiple of 8", c->hidden);
+  if (c->hidden > 32768)
+    return fail(PB_ERR_UNSUPPORTED, "hidden=%d > 32768 (LayerNorm keeps a row in registers)",
+                c->hidden);
+  if (c->ffn < 8 || c->ffn % 8)
+    return fail(PB_ERR_INVALID_ARG, "ffn=%d must be a positive multiple of 8", c->ffn);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(PB_ERR_UNSUPPORTED, "head_dim=%d: kernels exist for 64 and 128", c->head_dim);
+  if (!(c->ln_eps > 0.f) || !isfinite(c->ln_eps))
+    return fail(PB_ERR_INVALID_ARG, "ln_eps must be finite and > 0");
+  if (c->gelu_tanh != 0 && c->gelu_tanh != 1)
+    return fail(PB_ERR_INVALID_ARG, "gelu_tanh must be 0 or 1");
+  if (c->heads > 65535 || c->batch > 65535)
+    return fail(PB_ERR_UNSUPPORTED, "heads and batch must be <= 65535 (grid limits)");
+  const Dims d = dims_of(c);
+  if (d.T * d.heads > kMaxInt || d.N_in > kMaxInt / 4 || d.T > kMaxInt / 4)
+    return fail(PB_ERR_UNSUPPORTED, "problem too large for 32-bit row/column indices");
+  return PB_OK;
+}
+
+struct SavedLayout {
+  size_t off[6];  // h, z, c, mean, rstd, lse
+  size_t total;
+};
+SavedLayout saved_layout(const Dims& d) {
+  SavedLayout L;
+  size_t o = 0;
+  const size_t sizes[6] = {(size_t)(d.T * d.H) * d.esz, (size_t)(d.T * d.N_in) * d.esz,
+                           (size_t)(d.T * d.K_out) * d.esz, (size_t)d.T * 4, (size_t)d.T * 4,
+                           (size_t)(d.B * d.heads * d.S) * 4};
+  for (int i = 0; i < 6; ++i) {
+    L.off[i] = o;
+    o = align256(o + sizes[i]);
+  }
+  L.total = o;
+  return L;
+}
+
+struct BwdLayout {
+  size_t d_o, dz, dh, delta, pdg, pdb, part, total;
+};
+BwdLayout bwd_layout(const Dims& d) {
+  BwdLayout L;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align256(o + bytes);
+    return at;
+  };
+  const int nblk = pb::ln_backward_blocks((int)d.T);
+  L.d_o = take((size_t)(d.T * d.A) * d.esz);
+  L.dz = take((size_t)(d.T * d.N_in) * d.esz);
+  L.dh = take((size_t)(d.T * d.H) * 4);
+  L.delta = take((size_t)(d.B * d.heads * d.S) * 4);
+  L.pdg = take((size_t)nblk * d.H * 4);
+  L.pdb = take((size_t)nblk * d.H * 4);
+  size_t part = pb::colsum_partial_floats((int)d.T, (int)d.H);
+  size_t p2 = pb::colsum_partial_floats((int)d.T, (int)d.N_in);
+  size_t p3 = pb::colsum_partial_floats(nblk, (int)d.H);
+  if (p2 > part) part = p2;
+  if (p3 > part) part = p3;
+  L.part = take(part * 4);
+  L.total = o;
+  return L;
+}
+
+pb_status check_ptr(const void* p, const char* name) {
+  if (!p) return fail(PB_ERR_INVALID_ARG, "%s is NULL", name);
+  if ((uintptr_t)p % 16) return fail(PB_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return PB_OK;
+}
+
+#define PB_CHECK(expr)             \
+  do {                             \
+    pb_status _st = (expr);        \
+    if (_st != PB_OK) return _st;  \
+  } while (0)
+
+pb_status finish_launches() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(PB_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  g_err[0] = '\0';
+  return PB_OK;
+}
+
+pb::Dt dt_of(const pb_config* c) { return c->dtype == PB_BF16 ? pb::Dt::BF16 : pb::Dt::F32; }
+
+// Element offset helper for activation buffers.
+const void* at(const void* base, long long elems, size_t esz) {
+  return (const char*)base + (size_t)elems * esz;
+}
+void* at(void* base, long long elems, size_t esz) { return (char*)base + (size_t)elems * esz; }
+
+pb::AttnShape attn_shape(const Dims& d) {
+  pb::AttnShape a;
+  a.batch = (int)d.B;
+  a.seq = (int)d.S;
+  a.heads = (int)d.heads;
+  a.head_dim = (int)d.d;
+  // a window of at least seq keys is full causal attention; clamping keeps
+  // the kernels' index arithmetic within int range
+  a.window = (int)(d.W < d.S ? d.W : d.S);
+  return a;
+}
+
+pb_status check_attn_config(const pb_config* c) {
+  if (!c) return fail(PB_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->dtype != PB_BF16 && c->dtype != PB_F32)
+    return fail(PB_ERR_INVALID_ARG, "dtype %d is neither PB_BF16 nor PB_F32", (int)c->dtype);
+  if (c->batch < 1 || c->seq < 1 || c->heads < 1 || c->window < 1)
+    return fail(PB_ERR_INVALID_ARG, "batch, seq, heads and window must be >= 1");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(PB_ERR_UNSUPPORTED, "head_dim=%d: kernels exist for 64 and 128", c->head_dim);
+  if (c->heads > 65535 || c->batch > 65535)
+    return fail(PB_ERR_UNSUPPORTED, "heads and batch must be <= 65535 (grid limits)");
+  if ((long long)c->batch * c->seq * c->heads > kMaxInt)
+    return fail(PB_ERR_UNSUPPORTED, "batch*seq*heads exceeds 32-bit indexing");
+  return PB_OK;
+}
+
+pb_status check_ld(int ld, const pb_config* c, const char* name) {
+  if (ld < (long long)c->heads * c->head_dim || ld % 8)
+    return fail(PB_ERR_INVALID_ARG, "%s=%d must be >= heads*head_dim and a multiple of 8", name,
+                ld);
+  return PB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pb_status pblock_validate(const pb_config* cfg) {
+  pb_status st = check_config(cfg);
+  if (st == PB_OK) g_err[0] = '\0';
+  return st;
+}
+
+size_t pblock_saved_bytes(const pb_config* cfg) {
+  if (check_config(cfg) != PB_OK) return 0;
+  return saved_layout(dims_of(cfg)).total;
+}
+
+pb_status pblock_saved_offsets(const pb_config* cfg, size_t* offsets) {
+  PB_CHECK(check_config(cfg));
+  if (!offsets) return fail(PB_ERR_INVALID_ARG, "offsets is NULL");
+  const SavedLayout L = saved_layout(dims_of(cfg));
+  for (int i = 0; i < 6; ++i) offsets[i] = L.off[i];
+  return PB_OK;
+}
+
+size_t pblock_workspace_bytes(const pb_config* cfg, int backward) {
+  if (check_config(cfg) != PB_OK) return 0;
+  const Dims d = dims_of(cfg);
+  return backward ? bwd_layout(d).total : saved_layout(d).total;
+}
+
+pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gamma,
+                         const void* ln_beta, const void* w_in, const void* b_in,
+                         const void* w_out, const void* b_out, void* y, void* saved, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  PB_CHECK(check_config(cfg));
+  PB_CHECK(check_ptr(x, "x"));
+  PB_CHECK(check_ptr(ln_gamma, "ln_gamma"));
+  PB_CHECK(check_ptr(ln_beta, "ln_beta"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(b_in, "b_in"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(b_out, "b_out"));
+  PB_CHECK(check_ptr(y, "y"));
+  const Dims d = dims_of(cfg);
+  const SavedLayout L = saved_layout(d);
+  void* stash = saved;
+  if (stash) {
+    PB_CHECK(check_ptr(stash, "saved"));
+  } else {
+    PB_CHECK(check_ptr(ws, "ws (needed when saved is NULL)"));
+    if (ws_bytes < L.total)
+      return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed to hold the stash", ws_bytes,
+                  L.total);
+    stash = ws;
+  }
+  const pb::Dt dt = dt_of(cfg);
+  const size_t e = d.esz;
+  char* sb = (char*)stash;
+  void* h = sb + L.off[0];
+  void* z = sb + L.off[1];
+  void* c = sb + L.off[2];
+  float* mean = (float*)(sb + L.off[3]);
+  float* rstd = (float*)(sb + L.off[4]);
+  float* lse = (float*)(sb + L.off[5]);
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
+
+  // F1: shared LayerNorm
+  pb::launch_ln_forward(dt, x, ln_gamma, ln_beta, h, mean, rstd, T, H, cfg->ln_eps, stream);
+  // F2: Z = h W_in^T + b_in (Q | K | V | U); G = gelu(U) -> C[:, A:]
+  pb::EpiArgs e1;
+  e1.out = z;
+  e1.ld_out = N_in;
+  e1.out2 = c;
+  e1.ld_out2 = K_out;
+  e1.bias = b_in;
+  e1.split = 3 * A;
+  e1.col2 = A;
+  e1.gelu_tanh = cfg->gelu_tanh;
+  pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h, H, w_in, H, T, N_in, H, e1, stream);
+  // F3: sliding-window attention, O -> C[:, :A]
+  pb::launch_attn_forward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
+                          lse, stream);
+  // F5: y = x + C W_out^T + b_out (both branches and the residual of Eq. 2)
+  pb::EpiArgs e2;
+  e2.out = y;
+  e2.ld_out = H;
+  e2.bias = b_out;
+  e2.resid = x;
+  pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, c, K_out, w_out, K_out, T, H, K_out, e2,
+                  stream);
+  return finish_launches();
+}
+
+pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_gamma,
+                          const void* ln_beta, const void* w_in, const void* b_in,
+                          const void* w_out, const void* b_out, const void* saved,
+                          const void* dy, void* dx, float* dgamma, float* dbeta, float* dw_in,
+                          float* db_in, float* dw_out, float* db_out, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+  PB_CHECK(check_config(cfg));
+  PB_CHECK(check_ptr(x, "x"));
+  PB_CHECK(check_ptr(ln_gamma, "ln_gamma"));
+  PB_CHECK(check_ptr(ln_beta, "ln_beta"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(b_in, "b_in"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(b_out, "b_out"));
+  PB_CHECK(check_ptr(saved, "saved"));
+  PB_CHECK(check_ptr(dy, "dy"));
+  PB_CHECK(check_ptr(dx, "dx"));
+  PB_CHECK(check_ptr(dgamma, "dgamma"));
+  PB_CHECK(check_ptr(dbeta, "dbeta"));
+  PB_CHECK(check_ptr(dw_in, "dw_in"));
+  PB_CHECK(check_ptr(db_in, "db_in"));
+  PB_CHECK(check_ptr(dw_out, "dw_out"));
+  PB_CHECK(check_ptr(db_out, "db_out"));
+  PB_CHECK(check_ptr(ws, "ws"));
+  const Dims d = dims_of(cfg);
+  const BwdLayout W = bwd_layout(d);
+  if (ws_bytes < W.total)
+    return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, W.total);
+  const SavedLayout L = saved_layout(d);
+  const pb::Dt dt = dt_of(cfg);
+  const size_t e = d.esz;
+  const char* sb = (const char*)saved;
+  const void* h = sb + L.off[0];
+  const void* z = sb + L.off[1];
+  const void* c = sb + L.off[2];
+  const float* mean = (const float*)(sb + L.off[3]);
+  const float* rstd = (const float*)(sb + L.off[4]);
+  const float* lse = (const float*)(sb + L.off[5]);
+  char* wb = (char*)ws;
+  void* d_o = wb + W.d_o;
+  void* dz = wb + W.dz;
+  float* dh = (float*)(wb + W.dh);
+  float* delta = (float*)(wb + W.delta);
+  float* pdg = (float*)(wb + W.pdg);
+  float* pdb = (float*)(wb + W.pdb);
+  float* part = (float*)(wb + W.part);
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  (void)ln_beta;
+  (void)b_in;
+  (void)b_out;
+
+  // B1: dC = dy W_out; dO = dC[:, :A]; dU = dC[:, A:] * gelu'(U) -> dZ[:, 3A:]
+  pb::EpiArgs e1;
+  e1.out = d_o;
+  e1.ld_out = A;
+  e1.out2 = dz;
+  e1.ld_out2 = N_in;
+  e1.aux = z;
+  e1.split = A;
+  e1.col2 = 3 * A;
+  e1.gelu_tanh = cfg->gelu_tanh;
+  pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
+                  stream);
+  // B2: dW_out = dy^T C (contraction over tokens); db_out = sum_t dy
+  pb::EpiArgs e2;
+  e2.out = dw_out;
+  e2.ld_out = K_out;
+  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2, stream);
+  pb::launch_colsum(dt, dy, H, T, H, part, db_out, stream);
+  // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
+  pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
+                           d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in, stream);
+  // B4: dh = dZ W_in (fp32)
+  pb::EpiArgs e4;
+  e4.out = dh;
+  e4.ld_out = H;
+  pb::launch_gemm(dt, pb::Epi::StoreF32, true, false, dz, N_in, w_in, H, T, H, N_in, e4, stream);
+  // B5: dW_in = dZ^T h; db_in = sum_t dZ
+  pb::EpiArgs e5;
+  e5.out = dw_in;
+  e5.ld_out = H;
+  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5, stream);
+  pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+  // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
+  pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, dy, dx, pdg, pdb, T, H, stream);
+  const int nblk = pb::ln_backward_blocks(T);
+  pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
+  pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
+  return finish_launches();
+}
+
+pb_status pblock_swattn_forward(const pb_config* cfg, const void* q, const void* k,
+                                const void* v, int ld_qkv, void* o, int ld_o, float* lse,
+                                hipStream_t stream) {
+  PB_CHECK(check_attn_config(cfg));
+  PB_CHECK(check_ptr(q, "q"));
+  PB_CHECK(check_ptr(k, "k"));
+  PB_CHECK(check_ptr(v, "v"));
+  PB_CHECK(check_ptr(o, "o"));
+  PB_CHECK(check_ptr(lse, "lse"));
+  PB_CHECK(check_ld(ld_qkv, cfg, "ld_qkv"));
+  PB_CHECK(check_ld(ld_o, cfg, "ld_o"));
+  pb::AttnShape a;
+  a.batch = cfg->batch;
+  a.seq = cfg->seq;
+  a.heads = cfg->heads;
+  a.head_dim = cfg->head_dim;
+  a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
+  pb::launch_attn_forward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, lse, stream);
+  return finish_launches();
+}
+
+size_t pblock_swattn_workspace_bytes(const pb_config* cfg) {
+  if (check_attn_config(cfg) != PB_OK) return 0;
+  return align256((size_t)cfg->batch * cfg->heads * cfg->seq * 4);
+}
+
+pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void* k,
+                                 const void* v, int ld_qkv, const void* o, int ld_o,
+                                 const void* d_o, int ld_do, const float* lse, void* dq, void* dk,
+                                 void* dv, int ld_dqkv, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  PB_CHECK(check_attn_config(cfg));
+  PB_CHECK(check_ptr(q, "q"));
+  PB_CHECK(check_ptr(k, "k"));
+  PB_CHECK(check_ptr(v, "v"));
+  PB_CHECK(check_ptr(o, "o"));
+  PB_CHECK(check_ptr(d_o, "d_o"));
+  PB_CHECK(check_ptr(lse, "lse"));
+  PB_CHECK(check_ptr(dq, "dq"));
+  PB_CHECK(check_ptr(dk, "dk"));
+  PB_CHECK(check_ptr(dv, "dv"));
+  PB_CHECK(check_ptr(ws, "ws"));
+  PB_CHECK(check_ld(ld_qkv, cfg, "ld_qkv"));
+  PB_CHECK(check_ld(ld_o, cfg, "ld_o"));
+  PB_CHECK(check_ld(ld_do, cfg, "ld_do"));
+  PB_CHECK(check_ld(ld_dqkv, cfg, "ld_dqkv"));
+  const size_t need = pblock_swattn_workspace_bytes(cfg);
+  if (ws_bytes < need) return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, need);
+  pb::AttnShape a;
+  a.batch = cfg->batch;
+  a.seq = cfg->seq;
+  a.heads = cfg->heads;
+  a.head_dim = cfg->head_dim;
+  a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
+  pb::launch_attn_backward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, (float*)ws,
+                           dq, dk, dv, ld_dqkv, stream);
+  return finish_launches();
+}
+
+const char* pblock_status_string(pb_status status) {
+  switch (status) {
+    case PB_OK: return "PB_OK";
+    case PB_ERR_INVALID_ARG: return "PB_ERR_INVALID_ARG";
+    case PB_ERR_UNSUPPORTED: return "PB_ERR_UNSUPPORTED";
+    case PB_ERR_WORKSPACE: return "PB_ERR_WORKSPACE";
+    case PB_ERR_HIP: return "PB_ERR_HIP";
+  }
+  return "PB_ERR_UNKNOWN";
+}
+
+const char* pblock_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,248 @@
+"""Python binding of the C ABI in include/pblock.h (ctypes; argument
+marshalling only).
+
+Every entry point has the name of its C function and forwards to it: torch
+tensors (or raw integer device addresses) become pointers, the stream defaults
+to torch's current stream.  All arithmetic runs in the HIP library; there is no
+fallback.  If libpblock.so is missing or cannot be loaded, loading raises
+ImportError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_float, c_int, c_size_t, c_void_p
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpblock.so")
+
+PB_BF16, PB_F32 = 0, 1
+STATUS = {0: "PB_OK", 1: "PB_ERR_INVALID_ARG", 2: "PB_ERR_UNSUPPORTED", 3: "PB_ERR_WORKSPACE",
+          4: "PB_ERR_HIP"}
+SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
+
+# Every function the header declares (checked by the CPU tests).
+EXPORTS = (
+    "pblock_validate", "pblock_saved_bytes", "pblock_saved_offsets", "pblock_workspace_bytes",
+    "pblock_forward", "pblock_backward", "pblock_swattn_forward",
+    "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_status_string",
+    "pblock_last_error",
+)
+
+
+class PbConfig(ctypes.Structure):
+    _fields_ = [("batch", c_int), ("seq", c_int), ("hidden", c_int), ("heads", c_int),
+                ("head_dim", c_int), ("ffn", c_int), ("window", c_int), ("ln_eps", c_float),
+                ("gelu_tanh", c_int), ("dtype", c_int)]
+
+
+class PblockError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libpblock.so once and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run __graft_entry__.build() "
+                          f"(or python -m paper_2402_15627_amd.build)")
+    lib = ctypes.CDLL(path)
+    P = c_void_p
+    cfgp = POINTER(PbConfig)
+    sig = {
+        "pblock_validate": (c_int, [cfgp]),
+        "pblock_saved_bytes": (c_size_t, [cfgp]),
+        "pblock_saved_offsets": (c_int, [cfgp, POINTER(c_size_t)]),
+        "pblock_workspace_bytes": (c_size_t, [cfgp, c_int]),
+        "pblock_forward": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, c_size_t, P]),
+        "pblock_backward": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P,
+                                    c_size_t, P]),
+        "pblock_swattn_forward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, P]),
+        "pblock_swattn_workspace_bytes": (c_size_t, [cfgp]),
+        "pblock_swattn_backward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, c_int, P, P, P, P,
+                                           c_int, P, c_size_t, P]),
+        "pblock_status_string": (ctypes.c_char_p, [c_int]),
+        "pblock_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------- marshalling
+def _ptr(t):
+    """Device address of a tensor, an int address, or None -> NULL."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def _check(status: int):
+    if status != 0:
+        raise PblockError(status, pblock_last_error())
+
+
+def make_config(batch, seq, hidden, heads, head_dim, ffn, window, dtype="bf16", ln_eps=1e-5,
+                gelu_tanh=True) -> PbConfig:
+    return PbConfig(batch, seq, hidden, heads, head_dim, ffn, window, ln_eps, int(bool(gelu_tanh)),
+                    PB_BF16 if dtype == "bf16" else PB_F32)
+
+
+def config_from_shape(s) -> PbConfig:
+    """PbConfig from any object with the block's shape fields (e.g. inputs.BlockShape)."""
+    return make_config(s.batch, s.seq, s.hidden, s.heads, s.head_dim, s.ffn, s.window, s.dtype,
+                       s.ln_eps, s.gelu_tanh)
+
+
+# ------------------------------------------------------------ entry points
+def pblock_validate(cfg: PbConfig) -> int:
+    return load_library().pblock_validate(ctypes.byref(cfg))
+
+
+def pblock_saved_bytes(cfg: PbConfig) -> int:
+    return load_library().pblock_saved_bytes(ctypes.byref(cfg))
+
+
+def pblock_saved_offsets(cfg: PbConfig) -> dict:
+    arr = (c_size_t * 6)()
+    _check(load_library().pblock_saved_offsets(ctypes.byref(cfg), arr))
+    return dict(zip(SAVED_REGIONS, list(arr)))
+
+
+def pblock_workspace_bytes(cfg: PbConfig, backward: bool) -> int:
+    return load_library().pblock_workspace_bytes(ctypes.byref(cfg), int(bool(backward)))
+
+
+def pblock_forward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, y, saved=None, ws=None,
+                   stream=None):
+    _check(load_library().pblock_forward(
+        ctypes.byref(cfg), _ptr(x), _ptr(ln_gamma), _ptr(ln_beta), _ptr(w_in), _ptr(b_in),
+        _ptr(w_out), _ptr(b_out), _ptr(y), _ptr(saved), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def pblock_backward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, saved, dy, dx, dgamma,
+                    dbeta, dw_in, db_in, dw_out, db_out, ws, stream=None):
+    _check(load_library().pblock_backward(
+        ctypes.byref(cfg), _ptr(x), _ptr(ln_gamma), _ptr(ln_beta), _ptr(w_in), _ptr(b_in),
+        _ptr(w_out), _ptr(b_out), _ptr(saved), _ptr(dy), _ptr(dx), _ptr(dgamma), _ptr(dbeta),
+        _ptr(dw_in), _ptr(db_in), _ptr(dw_out), _ptr(db_out), _ptr(ws), _nbytes(ws),
+        _stream(stream)))
+
+
+def pblock_swattn_forward(cfg, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
+    _check(load_library().pblock_swattn_forward(
+        ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(lse),
+        _stream(stream)))
+
+
+def pblock_swattn_workspace_bytes(cfg) -> int:
+    return load_library().pblock_swattn_workspace_bytes(ctypes.byref(cfg))
+
+
+def pblock_swattn_backward(cfg, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, dq, dk, dv, ld_dqkv,
+                           ws, stream=None):
+    _check(load_library().pblock_swattn_backward(
+        ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(d_o), ld_do,
+        _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), ld_dqkv, _ptr(ws), _nbytes(ws),
+        _stream(stream)))
+
+
+def pblock_status_string(status: int) -> str:
+    return load_library().pblock_status_string(status).decode()
+
+
+def pblock_last_error() -> str:
+    return load_library().pblock_last_error().decode()
+
+
+# ------------------------------------------------------- device-side block
+class ParallelBlock:
+    """One block's device buffers (torch owns the memory) around the C calls.
+
+    ``tensors`` maps x, gamma, beta, w_in, b_in, w_out, b_out, dy to device
+    tensors of the activation dtype.  The stash, the workspace and every
+    output are allocated once here, so repeated forward()/backward() calls
+    allocate nothing.
+    """
+
+    def __init__(self, cfg: PbConfig, tensors: dict, device="cuda"):
+        import torch
+        self.cfg = cfg
+        self.t = tensors
+        T = cfg.batch * cfg.seq
+        H = cfg.hidden
+        A = cfg.heads * cfg.head_dim
+        n_in, k_out = 3 * A + cfg.ffn, A + cfg.ffn
+        act = torch.bfloat16 if cfg.dtype == PB_BF16 else torch.float32
+        f32 = torch.float32
+        u8 = torch.uint8
+        self.y = torch.empty((cfg.batch, cfg.seq, H), dtype=act, device=device)
+        self.saved = torch.empty(pblock_saved_bytes(cfg), dtype=u8, device=device)
+        self.ws = torch.empty(pblock_workspace_bytes(cfg, True), dtype=u8, device=device)
+        self.grads = dict(
+            dx=torch.empty((cfg.batch, cfg.seq, H), dtype=act, device=device),
+            dgamma=torch.empty(H, dtype=f32, device=device),
+            dbeta=torch.empty(H, dtype=f32, device=device),
+            dw_in=torch.empty((n_in, H), dtype=f32, device=device),
+            db_in=torch.empty(n_in, dtype=f32, device=device),
+            dw_out=torch.empty((H, k_out), dtype=f32, device=device),
+            db_out=torch.empty(H, dtype=f32, device=device),
+        )
+        self.T = T
+
+    def forward(self, stream=None):
+        t = self.t
+        pblock_forward(self.cfg, t["x"], t["gamma"], t["beta"], t["w_in"], t["b_in"], t["w_out"],
+                       t["b_out"], self.y, self.saved, None, stream)
+        return self.y
+
+    def backward(self, dy=None, stream=None):
+        t, g = self.t, self.grads
+        pblock_backward(self.cfg, t["x"], t["gamma"], t["beta"], t["w_in"], t["b_in"], t["w_out"],
+                        t["b_out"], self.saved, t["dy"] if dy is None else dy, g["dx"],
+                        g["dgamma"], g["dbeta"], g["dw_in"], g["db_in"], g["dw_out"],
+                        g["db_out"], self.ws, stream)
+        return g
+
+    def saved_view(self, name: str):
+        """A typed view of one stash region (h, z, c, mean, rstd, lse)."""
+        import torch
+        cfg = self.cfg
+        off = pblock_saved_offsets(cfg)[name]
+        T, H, A = self.T, cfg.hidden, cfg.heads * cfg.head_dim
+        act = torch.bfloat16 if cfg.dtype == PB_BF16 else torch.float32
+        shapes = {"h": ((T, H), act), "z": ((T, 3 * A + cfg.ffn), act),
+                  "c": ((T, A + cfg.ffn), act), "mean": ((T,), torch.float32),
+                  "rstd": ((T,), torch.float32),
+                  "lse": ((cfg.batch, cfg.heads, cfg.seq), torch.float32)}
+        shape, dt = shapes[name]
+        n = 1
+        for s_ in shape:
+            n *= s_
+        nbytes = n * torch.empty((), dtype=dt).element_size()
+        return self.saved[off:off + nbytes].view(dt).view(shape)

@@ -1,0 +1,145 @@
+"""The C ABI on a machine without a GPU: the library loads, exports every
+function include/pblock.h declares, and rejects bad arguments on the host
+before any HIP call (so these run on the CPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2402_15627_amd import pblock as pb
+from paper_2402_15627_amd.inputs import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pblock.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(pb.LIB_PATH), reason="libpblock.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pblock_\w+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(pb.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(pb.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def good_cfg(**kw):
+    s = WORKLOADS["13b_shape"]
+    c = pb.config_from_shape(s)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("hidden", 12, 1), ("hidden", 0, 1), ("ffn", 20, 1), ("batch", 0, 1),
+    ("seq", 0, 1), ("heads", 0, 1), ("window", 0, 1), ("head_dim", 96, 2), ("head_dim", 32, 2),
+    ("hidden", 40960, 2), ("gelu_tanh", 2, 1), ("dtype", 7, 1), ("ln_eps", 0.0, 1),
+    ("ln_eps", float("nan"), 1),
+])
+def test_validate_rejects(field, value, status):
+    c = good_cfg(**{field: value})
+    assert pb.pblock_validate(c) == status
+    assert pb.pblock_last_error() != ""
+    assert pb.pblock_saved_bytes(c) == 0
+    assert pb.pblock_workspace_bytes(c, True) == 0
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_validate_accepts_every_workload(name):
+    assert pb.pblock_validate(pb.config_from_shape(WORKLOADS[name])) == 0
+
+
+def align(v):
+    return (v + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_saved_layout(name):
+    s = WORKLOADS[name]
+    c = pb.config_from_shape(s)
+    e = 2 if s.dtype == "bf16" else 4
+    T = s.tokens
+    sizes = [T * s.hidden * e, T * s.n_in * e, T * s.k_out * e, 4 * T, 4 * T,
+             4 * s.batch * s.heads * s.seq]
+    off, o = [], 0
+    for z in sizes:
+        off.append(o)
+        o = align(o + z)
+    assert pb.pblock_saved_offsets(c) == dict(zip(pb.SAVED_REGIONS, off))
+    assert pb.pblock_saved_bytes(c) == o
+    assert pb.pblock_workspace_bytes(c, False) == o
+    # backward workspace holds at least dO, dZ and dh
+    assert pb.pblock_workspace_bytes(c, True) >= T * s.attn_width * e + T * s.n_in * e + 4 * T * s.hidden
+
+
+FAKE = 1 << 40  # a 16-byte aligned address; never dereferenced: every call below fails its checks
+
+
+def fwd_args(**over):
+    a = dict(x=FAKE, ln_gamma=FAKE, ln_beta=FAKE, w_in=FAKE, b_in=FAKE, w_out=FAKE, b_out=FAKE,
+             y=FAKE, saved=FAKE)
+    a.update(over)
+    return a
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(x=None), 1), (dict(w_in=None), 1), (dict(y=FAKE + 8), 1), (dict(b_out=FAKE + 2), 1),
+    (dict(saved=None), 1),  # no stash and no workspace
+])
+def test_forward_rejects_bad_pointers_before_launching(over, status):
+    lib = pb.load_library()
+    a = fwd_args(**over)
+    c = good_cfg()
+    st = lib.pblock_forward(ctypes.byref(c), a["x"], a["ln_gamma"], a["ln_beta"], a["w_in"],
+                            a["b_in"], a["w_out"], a["b_out"], a["y"], a["saved"], None, 0, None)
+    assert st == status, pb.pblock_last_error()
+
+
+def test_forward_rejects_small_workspace():
+    lib = pb.load_library()
+    a = fwd_args(saved=None)
+    c = good_cfg()
+    need = pb.pblock_workspace_bytes(c, False)
+    st = lib.pblock_forward(ctypes.byref(c), a["x"], a["ln_gamma"], a["ln_beta"], a["w_in"],
+                            a["b_in"], a["w_out"], a["b_out"], a["y"], None, FAKE, need - 1, None)
+    assert st == 3
+    assert "ws_bytes" in pb.pblock_last_error()
+
+
+def test_backward_rejects_small_workspace_and_nulls():
+    lib = pb.load_library()
+    c = good_cfg()
+    need = pb.pblock_workspace_bytes(c, True)
+    args = [FAKE] * 16
+    st = lib.pblock_backward(ctypes.byref(c), *args, FAKE, need - 1, None)
+    assert st == 3
+    args[9] = None  # dx
+    st = lib.pblock_backward(ctypes.byref(c), *args, FAKE, need, None)
+    assert st == 1 and "dx" in pb.pblock_last_error()
+
+
+def test_swattn_rejects_bad_leading_dimension():
+    lib = pb.load_library()
+    c = good_cfg()
+    A = c.heads * c.head_dim
+    st = lib.pblock_swattn_forward(ctypes.byref(c), FAKE, FAKE, FAKE, A - 8, FAKE, A, FAKE, None)
+    assert st == 1 and "ld_qkv" in pb.pblock_last_error()
+    st = lib.pblock_swattn_forward(ctypes.byref(c), FAKE, FAKE, FAKE, A + 4, FAKE, A, FAKE, None)
+    assert st == 1
+    st = lib.pblock_swattn_backward(ctypes.byref(c), FAKE, FAKE, FAKE, A, FAKE, A, FAKE, A, FAKE,
+                                    FAKE, FAKE, FAKE, A, FAKE, 0, None)
+    assert st == 3
+
+
+def test_status_strings():
+    assert [pb.pblock_status_string(i) for i in range(5)] == [pb.STATUS[i] for i in range(5)]
