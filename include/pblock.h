@@ -162,6 +162,31 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
                                  void* dk, void* dv, int ld_dqkv, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* Steps of the forward and backward passes, for pblock_set_step_events. */
+typedef enum {
+  PB_STEP_LN_FWD = 0, /* LayerNorm of x                                     */
+  PB_STEP_IN_PROJ,    /* Z = h W_in^T + b_in, G = gelu(U)                   */
+  PB_STEP_ATTN_FWD,   /* sliding-window attention, O and lse                */
+  PB_STEP_OUT_PROJ,   /* y = x + C W_out^T + b_out                          */
+  PB_STEP_DC,         /* dC = dy W_out; dU = dC_mlp * gelu'(U)              */
+  PB_STEP_DW_OUT,     /* dW_out = dy^T C                                    */
+  PB_STEP_DB_OUT,     /* db_out = sum over tokens of dy                     */
+  PB_STEP_ATTN_BWD,   /* dQ, dK, dV                                         */
+  PB_STEP_DH,         /* dh = dZ W_in                                       */
+  PB_STEP_DW_IN,      /* dW_in = dZ^T h                                     */
+  PB_STEP_DB_IN,      /* db_in = sum over tokens of dZ                      */
+  PB_STEP_LN_BWD,     /* dx = dy + LN backward; dgamma, dbeta               */
+  PB_STEP_COUNT
+} pb_step;
+
+/* Benchmark hook.  With begin and end not NULL, later pblock_forward and
+ * pblock_backward calls record begin[i] on their stream just before the
+ * launches of step i and end[i] just after them (NULL entries are skipped).
+ * Both arrays hold PB_STEP_COUNT events and are copied; the events belong to
+ * the caller.  pblock_set_step_events(NULL, NULL) turns recording off.  The
+ * setting is process-wide and not thread-safe.  Host only. */
+pb_status pblock_set_step_events(const hipEvent_t* begin, const hipEvent_t* end);
+
 /* Human-readable name of a status, and a description of the most recent
  * failed check on the calling thread ("" if none). */
 const char* pblock_status_string(pb_status status);

@@ -22,6 +22,22 @@ pb_status fail(pb_status st, const char* fmt, ...) {
   return st;
 }
 
+// Step events of the benchmark hook (pblock_set_step_events).
+bool g_ev_on = false;
+hipEvent_t g_ev_begin[PB_STEP_COUNT];
+hipEvent_t g_ev_end[PB_STEP_COUNT];
+
+struct StepScope {
+  int step;
+  hipStream_t s;
+  StepScope(pb_step st, hipStream_t stream) : step(st), s(stream) {
+    if (g_ev_on && g_ev_begin[step]) hipEventRecord(g_ev_begin[step], s);
+  }
+  ~StepScope() {
+    if (g_ev_on && g_ev_end[step]) hipEventRecord(g_ev_end[step], s);
+  }
+};
+
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 struct Dims {
@@ -248,7 +264,10 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
 
   // F1: shared LayerNorm
-  pb::launch_ln_forward(dt, x, ln_gamma, ln_beta, h, mean, rstd, T, H, cfg->ln_eps, stream);
+  {
+    StepScope sc(PB_STEP_LN_FWD, stream);
+    pb::launch_ln_forward(dt, x, ln_gamma, ln_beta, h, mean, rstd, T, H, cfg->ln_eps, stream);
+  }
   // F2: Z = h W_in^T + b_in (Q | K | V | U); G = gelu(U) -> C[:, A:]
   pb::EpiArgs e1;
   e1.out = z;
@@ -259,18 +278,27 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   e1.split = 3 * A;
   e1.col2 = A;
   e1.gelu_tanh = cfg->gelu_tanh;
-  pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h, H, w_in, H, T, N_in, H, e1, stream);
+  {
+    StepScope sc(PB_STEP_IN_PROJ, stream);
+    pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h, H, w_in, H, T, N_in, H, e1, stream);
+  }
   // F3: sliding-window attention, O -> C[:, :A]
-  pb::launch_attn_forward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
-                          lse, stream);
+  {
+    StepScope sc(PB_STEP_ATTN_FWD, stream);
+    pb::launch_attn_forward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
+                            lse, stream);
+  }
   // F5: y = x + C W_out^T + b_out (both branches and the residual of Eq. 2)
   pb::EpiArgs e2;
   e2.out = y;
   e2.ld_out = H;
   e2.bias = b_out;
   e2.resid = x;
-  pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, c, K_out, w_out, K_out, T, H, K_out, e2,
-                  stream);
+  {
+    StepScope sc(PB_STEP_OUT_PROJ, stream);
+    pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, c, K_out, w_out, K_out, T, H, K_out, e2,
+                    stream);
+  }
   return finish_launches();
 }
 
@@ -335,33 +363,61 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   e1.split = A;
   e1.col2 = 3 * A;
   e1.gelu_tanh = cfg->gelu_tanh;
-  pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
-                  stream);
+  {
+    StepScope sc(PB_STEP_DC, stream);
+    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
+                    stream);
+  }
   // B2: dW_out = dy^T C (contraction over tokens); db_out = sum_t dy
   pb::EpiArgs e2;
   e2.out = dw_out;
   e2.ld_out = K_out;
-  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2, stream);
-  pb::launch_colsum(dt, dy, H, T, H, part, db_out, stream);
+  {
+    StepScope sc(PB_STEP_DW_OUT, stream);
+    pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
+                    stream);
+  }
+  {
+    StepScope sc(PB_STEP_DB_OUT, stream);
+    pb::launch_colsum(dt, dy, H, T, H, part, db_out, stream);
+  }
   // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
-  pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
-                           d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in, stream);
+  {
+    StepScope sc(PB_STEP_ATTN_BWD, stream);
+    pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
+                             K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
+                             N_in, stream);
+  }
   // B4: dh = dZ W_in (fp32)
   pb::EpiArgs e4;
   e4.out = dh;
   e4.ld_out = H;
-  pb::launch_gemm(dt, pb::Epi::StoreF32, true, false, dz, N_in, w_in, H, T, H, N_in, e4, stream);
+  {
+    StepScope sc(PB_STEP_DH, stream);
+    pb::launch_gemm(dt, pb::Epi::StoreF32, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
+                    stream);
+  }
   // B5: dW_in = dZ^T h; db_in = sum_t dZ
   pb::EpiArgs e5;
   e5.out = dw_in;
   e5.ld_out = H;
-  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5, stream);
-  pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+  {
+    StepScope sc(PB_STEP_DW_IN, stream);
+    pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5,
+                    stream);
+  }
+  {
+    StepScope sc(PB_STEP_DB_IN, stream);
+    pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+  }
   // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
-  pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, dy, dx, pdg, pdb, T, H, stream);
-  const int nblk = pb::ln_backward_blocks(T);
-  pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
-  pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
+  {
+    StepScope sc(PB_STEP_LN_BWD, stream);
+    pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, dy, dx, pdg, pdb, T, H, stream);
+    const int nblk = pb::ln_backward_blocks(T);
+    pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
+    pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
+  }
   return finish_launches();
 }
 
@@ -422,6 +478,19 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void
   pb::launch_attn_backward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, (float*)ws,
                            dq, dk, dv, ld_dqkv, stream);
   return finish_launches();
+}
+
+pb_status pblock_set_step_events(const hipEvent_t* begin, const hipEvent_t* end) {
+  if (!begin || !end) {
+    g_ev_on = false;
+    return PB_OK;
+  }
+  for (int i = 0; i < PB_STEP_COUNT; ++i) {
+    g_ev_begin[i] = begin[i];
+    g_ev_end[i] = end[i];
+  }
+  g_ev_on = true;
+  return PB_OK;
 }
 
 const char* pblock_status_string(pb_status status) {

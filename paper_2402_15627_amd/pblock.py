@@ -25,9 +25,13 @@ SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
 EXPORTS = (
     "pblock_validate", "pblock_saved_bytes", "pblock_saved_offsets", "pblock_workspace_bytes",
     "pblock_forward", "pblock_backward", "pblock_swattn_forward",
-    "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_status_string",
-    "pblock_last_error",
+    "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_set_step_events",
+    "pblock_status_string", "pblock_last_error",
 )
+
+# pb_step order of include/pblock.h
+STEPS = ("ln_fwd", "in_proj", "attn_fwd", "out_proj", "dc", "dw_out", "db_out", "attn_bwd", "dh",
+         "dw_in", "db_in", "ln_bwd")
 
 
 class PbConfig(ctypes.Structure):
@@ -68,6 +72,7 @@ def load_library(path: str = LIB_PATH):
         "pblock_swattn_workspace_bytes": (c_size_t, [cfgp]),
         "pblock_swattn_backward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, c_int, P, P, P, P,
                                            c_int, P, c_size_t, P]),
+        "pblock_set_step_events": (c_int, [P, P]),
         "pblock_status_string": (ctypes.c_char_p, [c_int]),
         "pblock_last_error": (ctypes.c_char_p, []),
     }
@@ -170,6 +175,20 @@ def pblock_swattn_backward(cfg, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, dq, d
         ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(d_o), ld_do,
         _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), ld_dqkv, _ptr(ws), _nbytes(ws),
         _stream(stream)))
+
+
+def pblock_set_step_events(begin, end):
+    """begin/end: sequences of len(STEPS) raw hipEvent_t handles (ints, 0 to
+    skip a step), or None to turn recording off."""
+    lib = load_library()
+    if begin is None or end is None:
+        _check(lib.pblock_set_step_events(None, None))
+        return
+    n = len(STEPS)
+    assert len(begin) == n and len(end) == n
+    b = (c_void_p * n)(*[h or None for h in begin])
+    e = (c_void_p * n)(*[h or None for h in end])
+    _check(lib.pblock_set_step_events(b, e))
 
 
 def pblock_status_string(status: int) -> str:
