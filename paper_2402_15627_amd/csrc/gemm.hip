@@ -1,7 +1,7 @@
 // Projection GEMMs of the parallel block with fused epilogues.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 256x256 output tile per
-// workgroup of four waves (each wave 128x128), K-tile 64, double-buffered
+// workgroup of eight waves (each wave 64x128), K-tile 64, double-buffered
 // LDS (128 KB).  LDS holds both operands K-contiguous, 128-byte rows with
 // the 16-byte chunk index XOR-swizzled by the row so that fragment reads and
 // tile writes touch distinct banks.  An operand that is M- or N-contiguous in
@@ -24,7 +24,8 @@ namespace pb {
 namespace {
 
 // ------------------------------------------------------------- epilogues
-template <typename T, Epi EPI>
+// Four consecutive output columns n..n+3 of row m.  GT: tanh form of GeLU.
+template <typename T, Epi EPI, bool GT>
 PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
   if constexpr (EPI == Epi::StoreF32) {
     store4((float*)ep.out + (size_t)m * ep.ld_out + n, v);
@@ -37,7 +38,7 @@ PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
     if (n >= ep.split) {
       float g[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) g[e] = gelu(z[e], ep.gelu_tanh != 0);
+      for (int e = 0; e < 4; ++e) g[e] = gelu<GT>(z[e]);
       store4((T*)ep.out2 + (size_t)m * ep.ld_out2 + (n - ep.split) + ep.col2, g);
     }
   } else if constexpr (EPI == Epi::BiasResid) {
@@ -55,15 +56,21 @@ PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
       float u[4], o[4];
       load4((const T*)ep.aux + off, u);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = v[e] * gelu_grad(u[e], ep.gelu_tanh != 0);
+      for (int e = 0; e < 4; ++e) o[e] = v[e] * gelu_grad<GT>(u[e]);
       store4((T*)ep.out2 + off, o);
     }
   }
 }
 
 // --------------------------------------------------------- bf16 MFMA GEMM
+// 256 x 256 output tile, K-tile 64, eight waves in a 4 (m) x 2 (n) grid, each
+// wave 64 x 128 (2 x 4 MFMA blocks of 32 x 32); two waves per SIMD hide each
+// other's LDS and global latency.
 constexpr int kBM = 256, kBN = 256, kBK = 64;
-constexpr int kThreads = 256;
+constexpr int kWavesM = 4, kWavesN = 2;
+constexpr int kThreads = 64 * kWavesM * kWavesN;
+constexpr int kWTM = kBM / kWavesM, kWTN = kBN / kWavesN;
+constexpr int kTM = kWTM / 32, kTN = kWTN / 32;
 constexpr int kTileBytes = kBM * kBK * 2;  // one operand tile (32 KB)
 
 // 16-byte chunk c (0..7) of LDS row `row` lives at physical chunk swz(row, c).
@@ -87,58 +94,75 @@ PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
   tn = in_group / gsize;
 }
 
-// Load one 256 x 64 operand tile into registers.  KC: the operand is
-// K-contiguous (row r of the tile at X[(R0 + r) * ld + k]); otherwise it is
-// MN-contiguous (X[k * ld + R0 + r]).  Rows past Rmax are clamped (their
-// results are never stored); k past K reads as zero.
+// One 256 x 64 operand tile, global -> registers -> LDS.
+// KC: K-contiguous operand, row r of the tile at X[(R0 + r) * ld + k]: each
+//     thread moves four 16-byte chunks (rows past Rmax are clamped: their
+//     results are never stored).
+// else MN-contiguous, X[k * ld + R0 + r]: each thread moves a 4 (k) x 8 (mn)
+//     piece and transposes it into eight 8-byte LDS writes.
+// k past K reads as zero.  Loads are unconditional (address clamped, value
+// selected) so the loop body stays branch-free.
 template <bool KC>
-PB_DEV void load_tile(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k0, int K,
-                      u32x4* r) {
-  const int tid = threadIdx.x;
-  if constexpr (KC) {
-    const int c = tid & 7;
-    const int k = k0 + 8 * c;
+struct TileLoader {
+  u32x4 r[4];
+
+  PB_DEV void load(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k0, int K) {
+    const int tid = threadIdx.x;
+    if constexpr (KC) {
+      const int c = tid & 7;
+      const int k = k0 + 8 * c;
+      const bool kok = k < K;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      int row = R0 + (tid >> 3) + 32 * i;
-      row = row < Rmax ? row : Rmax - 1;
-      r[i] = k < K ? *reinterpret_cast<const u32x4*>(X + (size_t)row * ld + k) : u32x4{0, 0, 0, 0};
-    }
-  } else {
-    const int col = R0 + 8 * (tid & 31);
-    const int kb = tid >> 5;
+      for (int i = 0; i < 4; ++i) {
+        int row = R0 + (tid >> 3) + 64 * i;
+        row = row < Rmax ? row : Rmax - 1;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(X + (size_t)row * ld + (kok ? k : 0));
+        r[i] = kok ? v : u32x4{0, 0, 0, 0};
+      }
+    } else {
+      const int col = R0 + 8 * (tid & 31);
+      const int kq = tid >> 5;  // 0..15
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = k0 + 8 * kb + j;
-      r[j] = (k < K && col < Rmax) ? *reinterpret_cast<const u32x4*>(X + (size_t)k * ld + col)
-                                   : u32x4{0, 0, 0, 0};
+      for (int j = 0; j < 4; ++j) {
+        const int k = k0 + 4 * kq + j;
+        const bool ok = k < K && col < Rmax;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(X + (ok ? (size_t)k * ld + col : 0));
+        r[j] = ok ? v : u32x4{0, 0, 0, 0};
+      }
     }
   }
-}
 
-template <bool KC>
-PB_DEV void store_tile(u32x4* __restrict__ lds, const u32x4* r) {
-  const int tid = threadIdx.x;
-  if constexpr (KC) {
-    const int c = tid & 7;
+  PB_DEV void store(unsigned char* __restrict__ lds) const {
+    const int tid = threadIdx.x;
+    if constexpr (KC) {
+      const int c = tid & 7;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = (tid >> 3) + 32 * i;
-      lds[row * 8 + swz(row, c)] = r[i];
-    }
-  } else {
-    u32x4 t[8];
-    transpose8x8(r, t);
-    const int mb = tid & 31, kb = tid >> 5;
+      for (int i = 0; i < 4; ++i) {
+        const int row = (tid >> 3) + 64 * i;
+        *reinterpret_cast<u32x4*>(lds + row * 128 + swz(row, c) * 16) = r[i];
+      }
+    } else {
+      const int mb = tid & 31, kq = tid >> 5;
+      const int c = kq >> 1, half = kq & 1;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = 8 * mb + i;
-      lds[row * 8 + swz(row, kb)] = t[i];
+      for (int i = 0; i < 8; ++i) {
+        const int q = i >> 1;
+        uint32_t w0, w1;
+        if (i & 1) {
+          w0 = (r[0][q] >> 16) | (r[1][q] & 0xffff0000u);
+          w1 = (r[2][q] >> 16) | (r[3][q] & 0xffff0000u);
+        } else {
+          w0 = (r[0][q] & 0xffffu) | (r[1][q] << 16);
+          w1 = (r[2][q] & 0xffffu) | (r[3][q] << 16);
+        }
+        const int row = 8 * mb + i;
+        *reinterpret_cast<u32x2*>(lds + row * 128 + swz(row, c) * 16 + half * 8) = u32x2{w0, w1};
+      }
     }
   }
-}
+};
 
-template <bool AK, bool BK, Epi EPI>
+template <bool AK, bool BK, Epi EPI, bool GT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __restrict__ A,
                                                                 int lda,
                                                                 const bf16* __restrict__ B,
@@ -146,66 +170,71 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
                                                                 EpiArgs ep) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   // stage s: A tile at smem + 2 s * kTileBytes, B tile right after it
-  u32x4* const lds0 = reinterpret_cast<u32x4*>(smem);
-  constexpr int kTileVec = kTileBytes / 16;
-  auto lds_a = [&](int s) { return lds0 + 2 * s * kTileVec; };
-  auto lds_b = [&](int s) { return lds0 + (2 * s + 1) * kTileVec; };
+  auto lds_a = [&](int s) { return smem + (2 * s) * kTileBytes; };
+  auto lds_b = [&](int s) { return smem + (2 * s + 1) * kTileBytes; };
 
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
   int tm, tn;
   tile_coords(tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave & 1) * 128, wn = (wave >> 1) * 128;
+  const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
 
-  f32x16 acc[4][4];
+  f32x16 acc[kTM][kTN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kTM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < kTN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  u32x4 ra[8], rb[8];
+  TileLoader<AK> la;
+  TileLoader<BK> lb;
   const int nk = (K + kBK - 1) / kBK;
-  load_tile<AK>(A, lda, m0, M, 0, K, ra);
-  load_tile<BK>(B, ldb, n0, N, 0, K, rb);
-  store_tile<AK>(lds_a(0), ra);
-  store_tile<BK>(lds_b(0), rb);
+  la.load(A, lda, m0, M, 0, K);
+  lb.load(B, ldb, n0, N, 0, K);
+  la.store(lds_a(0));
+  lb.store(lds_b(0));
   __syncthreads();
 
   const int fr = lane & 31, fh = lane >> 5;
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     if (kt + 1 < nk) {
-      load_tile<AK>(A, lda, m0, M, (kt + 1) * kBK, K, ra);
-      load_tile<BK>(B, ldb, n0, N, (kt + 1) * kBK, K, rb);
+      la.load(A, lda, m0, M, (kt + 1) * kBK, K);
+      lb.load(B, ldb, n0, N, (kt + 1) * kBK, K);
     }
-    const u32x4* la = lds_a(cur);
-    const u32x4* lb = lds_b(cur);
+    const u32x4* pa = reinterpret_cast<const u32x4*>(lds_a(cur));
+    const u32x4* pb = reinterpret_cast<const u32x4*>(lds_b(cur));
+    // fragments of k-step ks + 1 are read while the MFMAs of ks run
+    bf16x8 fa[2][kTM], fb[2][kTN];
+    auto read_frags = [&](int ks, int buf) {
+      const int c = 2 * ks + fh;
+#pragma unroll
+      for (int i = 0; i < kTM; ++i) {
+        const int row = wm + 32 * i + fr;
+        fa[buf][i] = __builtin_bit_cast(bf16x8, pa[row * 8 + swz(row, c)]);
+      }
+#pragma unroll
+      for (int j = 0; j < kTN; ++j) {
+        const int row = wn + 32 * j + fr;
+        fb[buf][j] = __builtin_bit_cast(bf16x8, pb[row * 8 + swz(row, c)]);
+      }
+    };
+    read_frags(0, 0);
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      const int c = 2 * ks + fh;
-      bf16x8 fa[4], fb[4];
+      const int b = ks & 1;
+      if (ks + 1 < kBK / 16) read_frags(ks + 1, b ^ 1);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm + 32 * i + fr;
-        fa[i] = __builtin_bit_cast(bf16x8, la[row * 8 + swz(row, c)]);
-      }
+      for (int i = 0; i < kTM; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = wn + 32 * j + fr;
-        fb[j] = __builtin_bit_cast(bf16x8, lb[row * 8 + swz(row, c)]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < kTN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[b][j], fa[b][i], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) {
-      store_tile<AK>(lds_a(cur ^ 1), ra);
-      store_tile<BK>(lds_b(cur ^ 1), rb);
+      la.store(lds_a(cur ^ 1));
+      lb.store(lds_b(cur ^ 1));
     }
     __syncthreads();
   }
@@ -213,18 +242,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
   // acc[i][j][4*jj + e] is C(m, n) with m = wm + 32 i + (lane & 31) and
   // n = wn + 32 j + 8 jj + 4 (lane >> 5) + e.
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < kTM; ++i) {
     const int m = m0 + wm + 32 * i + fr;
     if (m >= M) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < kTN; ++j)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         const int n = n0 + wn + 32 * j + 8 * jj + 4 * fh;
         if (n < N) {
           float v[4] = {acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
                         acc[i][j][4 * jj + 3]};
-          epi_store4<bf16, EPI>(ep, m, n, v);
+          epi_store4<bf16, EPI, GT>(ep, m, n, v);
         }
       }
   }
@@ -233,7 +262,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
 // ----------------------------------------------------------- fp32 SIMT GEMM
 constexpr int kSB = 64, kSK = 16;
 
-template <bool AK, bool BK, Epi EPI>
+template <bool AK, bool BK, Epi EPI, bool GT>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, int lda,
                                                        const float* __restrict__ B, int ldb,
                                                        int M, int N, int K, EpiArgs ep) {
@@ -272,50 +301,53 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i, n = n0 + tx * 4;
-    if (m < M && n < N) epi_store4<float, EPI>(ep, m, n, acc[i]);
+    if (m < M && n < N) epi_store4<float, EPI, GT>(ep, m, n, acc[i]);
   }
 }
 
-template <bool AK, bool BK, Epi EPI>
+template <bool AK, bool BK, Epi EPI, bool GT>
 void gemm_dispatch_layout(Dt dt, const void* A, int lda, const void* B, int ldb, int M, int N,
                           int K, const EpiArgs& ep, hipStream_t s) {
   if (dt == Dt::BF16) {
     const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
     const size_t lds = 4 * (size_t)kTileBytes;
-    gemm_bf16_kernel<AK, BK, EPI><<<tiles, kThreads, lds, s>>>(
+    gemm_bf16_kernel<AK, BK, EPI, GT><<<tiles, kThreads, lds, s>>>(
         (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
   } else {
     dim3 grid((N + kSB - 1) / kSB, (M + kSB - 1) / kSB);
-    gemm_f32_kernel<AK, BK, EPI><<<grid, 256, 0, s>>>((const float*)A, lda, (const float*)B,
-                                                      ldb, M, N, K, ep);
+    gemm_f32_kernel<AK, BK, EPI, GT><<<grid, 256, 0, s>>>((const float*)A, lda, (const float*)B,
+                                                          ldb, M, N, K, ep);
   }
 }
 
-template <Epi EPI>
+template <Epi EPI, bool GT>
 void gemm_dispatch(Dt dt, bool ak, bool bk, const void* A, int lda, const void* B, int ldb,
                    int M, int N, int K, const EpiArgs& ep, hipStream_t s) {
-  if (ak && bk) gemm_dispatch_layout<true, true, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
-  else if (ak) gemm_dispatch_layout<true, false, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
-  else if (bk) gemm_dispatch_layout<false, true, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
-  else gemm_dispatch_layout<false, false, EPI>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  if (ak && bk) gemm_dispatch_layout<true, true, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  else if (ak) gemm_dispatch_layout<true, false, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  else if (bk) gemm_dispatch_layout<false, true, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
+  else gemm_dispatch_layout<false, false, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
 }
 
 }  // namespace
 
 void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,
                  const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, hipStream_t s) {
+  const bool gt = ep.gelu_tanh != 0;
   switch (epi) {
     case Epi::StoreF32:
-      gemm_dispatch<Epi::StoreF32>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      gemm_dispatch<Epi::StoreF32, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
       break;
     case Epi::BiasGelu:
-      gemm_dispatch<Epi::BiasGelu>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      if (gt) gemm_dispatch<Epi::BiasGelu, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      else gemm_dispatch<Epi::BiasGelu, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
       break;
     case Epi::BiasResid:
-      gemm_dispatch<Epi::BiasResid>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      gemm_dispatch<Epi::BiasResid, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
       break;
     case Epi::DgeluSplit:
-      gemm_dispatch<Epi::DgeluSplit>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      if (gt) gemm_dispatch<Epi::DgeluSplit, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      else gemm_dispatch<Epi::DgeluSplit, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
       break;
   }
 }
