@@ -105,9 +105,14 @@ PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
 template <bool KC>
 struct TileLoader {
   u32x4 r[4];
+  uint32_t ok;  // bit i: r[i] is in range (else it is stored as zero)
 
+  // The zero-fill select is applied in store(), not here: consuming the
+  // loaded registers right away would make the compiler wait for the loads
+  // before the MFMAs of the current tile instead of overlapping them.
   PB_DEV void load(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k0, int K) {
     const int tid = threadIdx.x;
+    ok = 0;
     if constexpr (KC) {
       const int c = tid & 7;
       const int k = k0 + 8 * c;
@@ -116,8 +121,8 @@ struct TileLoader {
       for (int i = 0; i < 4; ++i) {
         int row = R0 + (tid >> 3) + 64 * i;
         row = row < Rmax ? row : Rmax - 1;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(X + (size_t)row * ld + (kok ? k : 0));
-        r[i] = kok ? v : u32x4{0, 0, 0, 0};
+        r[i] = *reinterpret_cast<const u32x4*>(X + (size_t)row * ld + (kok ? k : 0));
+        ok |= (uint32_t)kok << i;
       }
     } else {
       const int col = R0 + 8 * (tid & 31);
@@ -125,21 +130,24 @@ struct TileLoader {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int k = k0 + 4 * kq + j;
-        const bool ok = k < K && col < Rmax;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(X + (ok ? (size_t)k * ld + col : 0));
-        r[j] = ok ? v : u32x4{0, 0, 0, 0};
+        const bool in = k < K && col < Rmax;
+        r[j] = *reinterpret_cast<const u32x4*>(X + (in ? (size_t)k * ld + col : 0));
+        ok |= (uint32_t)in << j;
       }
     }
   }
 
   PB_DEV void store(unsigned char* __restrict__ lds) const {
     const int tid = threadIdx.x;
+    u32x4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = ((ok >> i) & 1) ? r[i] : u32x4{0, 0, 0, 0};
     if constexpr (KC) {
       const int c = tid & 7;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = (tid >> 3) + 64 * i;
-        *reinterpret_cast<u32x4*>(lds + row * 128 + swz(row, c) * 16) = r[i];
+        *reinterpret_cast<u32x4*>(lds + row * 128 + swz(row, c) * 16) = v[i];
       }
     } else {
       const int mb = tid & 31, kq = tid >> 5;
@@ -149,11 +157,11 @@ struct TileLoader {
         const int q = i >> 1;
         uint32_t w0, w1;
         if (i & 1) {
-          w0 = (r[0][q] >> 16) | (r[1][q] & 0xffff0000u);
-          w1 = (r[2][q] >> 16) | (r[3][q] & 0xffff0000u);
+          w0 = (v[0][q] >> 16) | (v[1][q] & 0xffff0000u);
+          w1 = (v[2][q] >> 16) | (v[3][q] & 0xffff0000u);
         } else {
-          w0 = (r[0][q] & 0xffffu) | (r[1][q] << 16);
-          w1 = (r[2][q] & 0xffffu) | (r[3][q] << 16);
+          w0 = (v[0][q] & 0xffffu) | (v[1][q] << 16);
+          w1 = (v[2][q] & 0xffffu) | (v[3][q] << 16);
         }
         const int row = 8 * mb + i;
         *reinterpret_cast<u32x2*>(lds + row * 128 + swz(row, c) * 16 + half * 8) = u32x2{w0, w1};
