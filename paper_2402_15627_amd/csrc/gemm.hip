@@ -267,6 +267,155 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
   }
 }
 
+// ------------------------------------------- bf16 MFMA GEMM, LDS-DMA path
+// Used when K is a multiple of 64.  The operand tiles go from global memory
+// straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
+// LDS base + 16 * lane), so there is no register staging and no LDS write
+// instruction.  A K-contiguous operand is stored K-major (as above); an
+// MN-contiguous operand is stored MN-major, 64 k-rows of 512 bytes with the
+// 16-byte chunk index XOR-ed by 4 (k mod 4), and its MFMA fragments are read
+// with ds_read_b64_tr_b16, which transposes 4 (k) x 16 (mn) blocks across a
+// 16-lane group.  The DMA instructions are issued from inline assembly and
+// waited for explicitly, so the compiler adds no conservative waits between
+// them and the LDS reads of the other stage.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+#define PB_LDS __attribute__((address_space(3)))
+
+PB_DEV int swz_mn(int krow, int c) { return c ^ (4 * (krow & 3)); }
+
+PB_DEV void dma16(const void* g, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_byte_addr)
+               : "memory", "m0");
+}
+PB_DEV void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// This wave's 4 KB share of one 256 x 64 operand tile (four 1 KB DMA pieces).
+template <bool KC>
+PB_DEV void dma_tile(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k0,
+                     uint32_t lds_tile, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int base = wave * 4096 + i * 1024;
+    const int p = base + 16 * lane;
+    const bf16* g;
+    if constexpr (KC) {
+      const int row = p >> 7, c = swz(row, (p >> 4) & 7);
+      int r = R0 + row;
+      r = r < Rmax ? r : Rmax - 1;  // clamped rows: results never stored
+      g = X + (size_t)r * ld + k0 + 8 * c;
+    } else {
+      const int krow = p >> 9, c = swz_mn(krow, (p >> 4) & 31);
+      int col = R0 + 8 * c;
+      col = col < Rmax ? col : Rmax - 8;
+      g = X + (size_t)(k0 + krow) * ld + col;
+    }
+    dma16(g, __builtin_amdgcn_readfirstlane(lds_tile + base));
+  }
+}
+
+// MFMA fragment (8 bf16 along k) of tile row `row`, k-step ks, lane half h.
+template <bool KC>
+PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, int lane) {
+  if constexpr (KC) {
+    return *reinterpret_cast<const bf16x8*>(lds_tile + row * 128 + swz(row, 2 * ks + h) * 16);
+  } else {
+    // lane 4 j + q of a 16-lane group reads k-row kb + j, mn (row & ~15) + 4 q;
+    // the transposing read hands lane i the four k values of mn (row & ~15) + i
+    const int i = lane & 15;
+    const int j = i >> 2, q = i & 3;
+    const int mn = (row & ~15) + 4 * q;
+    const int kb = 16 * ks + 8 * h;
+    const int c = mn >> 3, off = (mn & 7) * 2;
+    const int k1 = kb + j, k2 = kb + 4 + j;
+    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (PB_LDS s16x4*)(lds_tile + k1 * 512 + swz_mn(k1, c) * 16 + off));
+    const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (PB_LDS s16x4*)(lds_tile + k2 * 512 + swz_mn(k2, c) * 16 + off));
+    const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
+    return bf16x8{a4[0], a4[1], a4[2], a4[3], b4[0], b4[1], b4[2], b4[3]};
+  }
+}
+
+template <bool AK, bool BK, Epi EPI, bool GT>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* __restrict__ A,
+                                                                    int lda,
+                                                                    const bf16* __restrict__ B,
+                                                                    int ldb, int M, int N, int K,
+                                                                    EpiArgs ep) {
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
+  auto a_off = [&](int s) { return (2 * s) * kTileBytes; };
+  auto b_off = [&](int s) { return (2 * s + 1) * kTileBytes; };
+
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
+
+  f32x16 acc[kTM][kTN];
+#pragma unroll
+  for (int i = 0; i < kTM; ++i)
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nk = K / kBK;
+  dma_tile<AK>(A, lda, m0, M, 0, lds0 + a_off(0), wave, lane);
+  dma_tile<BK>(B, ldb, n0, N, 0, lds0 + b_off(0), wave, lane);
+
+  const int fr = lane & 31, fh = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    wait_dma_all();   // this wave's pieces of stage cur have landed
+    block_barrier();  // everyone's have; everyone is done reading stage cur ^ 1
+    if (kt + 1 < nk) {
+      dma_tile<AK>(A, lda, m0, M, (kt + 1) * kBK, lds0 + a_off(cur ^ 1), wave, lane);
+      dma_tile<BK>(B, ldb, n0, N, (kt + 1) * kBK, lds0 + b_off(cur ^ 1), wave, lane);
+    }
+    const unsigned char* pa = smem + a_off(cur);
+    const unsigned char* pb = smem + b_off(cur);
+    bf16x8 fa[2][kTM], fb[2][kTN];
+    auto read_frags = [&](int ks, int buf) {
+#pragma unroll
+      for (int i = 0; i < kTM; ++i) fa[buf][i] = dma_frag<AK>(pa, wm + 32 * i + fr, ks, fh, lane);
+#pragma unroll
+      for (int j = 0; j < kTN; ++j) fb[buf][j] = dma_frag<BK>(pb, wn + 32 * j + fr, ks, fh, lane);
+    };
+    read_frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int b = ks & 1;
+      if (ks + 1 < kBK / 16) read_frags(ks + 1, b ^ 1);
+#pragma unroll
+      for (int i = 0; i < kTM; ++i)
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[b][j], fa[b][i], acc[i][j], 0, 0, 0);
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < kTM; ++i) {
+    const int m = m0 + wm + 32 * i + fr;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int n = n0 + wn + 32 * j + 8 * jj + 4 * fh;
+        if (n < N) {
+          float v[4] = {acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
+                        acc[i][j][4 * jj + 3]};
+          epi_store4<bf16, EPI, GT>(ep, m, n, v);
+        }
+      }
+  }
+}
+
 // ----------------------------------------------------------- fp32 SIMT GEMM
 constexpr int kSB = 64, kSK = 16;
 
@@ -319,8 +468,12 @@ void gemm_dispatch_layout(Dt dt, const void* A, int lda, const void* B, int ldb,
   if (dt == Dt::BF16) {
     const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
     const size_t lds = 4 * (size_t)kTileBytes;
-    gemm_bf16_kernel<AK, BK, EPI, GT><<<tiles, kThreads, lds, s>>>(
-        (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
+    if (K % kBK == 0)
+      gemm_bf16_dma_kernel<AK, BK, EPI, GT><<<tiles, kThreads, lds, s>>>(
+          (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
+    else
+      gemm_bf16_kernel<AK, BK, EPI, GT><<<tiles, kThreads, lds, s>>>(
+          (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
   } else {
     dim3 grid((N + kSB - 1) / kSB, (M + kSB - 1) / kSB);
     gemm_f32_kernel<AK, BK, EPI, GT><<<grid, 256, 0, s>>>((const float*)A, lda, (const float*)B,
