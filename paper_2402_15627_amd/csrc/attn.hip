@@ -27,75 +27,91 @@
 namespace pb {
 namespace {
 
-constexpr int kAttnThreads = 256;  // four waves
-constexpr int kTile = 64;          // keys (forward, dQ) or queries (dK/dV) per LDS tile
 constexpr float kNegInf = -__builtin_huge_valf();
 
+// Waves per workgroup and tile length (tokens per LDS tile):
+//   forward and dQ: 32 NW queries per workgroup, key tiles of kTL
+//   dK/dV         : 32 NW keys per workgroup, query tiles of kTLdkv
+constexpr int NW = 2;
+constexpr int kThreads = 64 * NW;
+constexpr int kTL = 64;      // forward and dQ key tiles
+constexpr int kTLdkv = 32;   // dK/dV query tiles (keeps its registers and LDS in budget)
+
+PB_DEV float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+#define PB_LDS __attribute__((address_space(3)))
+
 // ------------------------------------------------------------ LDS tiles
-// Natural tile: 64 token rows x D, row r chunk c (8 elements) at
-// r * (D/8) + (c ^ (r & 7)).
+// Every tile is natural: kTL token rows x D features, 2 D bytes per row, the
+// 16-byte chunk c of row r stored at chunk c ^ f(r).  For D = 128 (16 chunks
+// per row, one 256-byte bank period) f is a 4-bit rotation of r that makes
+// both access patterns conflict-free: a 16-byte read by 16 consecutive rows
+// at one chunk, and a transposing read of 8 consecutive rows x 4 aligned
+// chunks.  D = 64 uses an injective 3-bit variant.
 template <int D>
-PB_DEV void load_nat(const bf16* __restrict__ base, int ld, int row0, int rows_valid, int tid,
-                     u32x4* r) {
-  constexpr int CPR = D / 8;
-#pragma unroll
-  for (int u = 0; u < CPR / 4; ++u) {
-    const int ci = tid + kAttnThreads * u;
-    const int row = ci / CPR, c = ci % CPR;
-    const int t = row0 + row;
-    r[u] = t < rows_valid ? *reinterpret_cast<const u32x4*>(base + (size_t)t * ld + 8 * c)
-                          : u32x4{0, 0, 0, 0};
-  }
+PB_DEV int rowswz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return ((r & 1) << 2) | ((r >> 1) & 3);
 }
 template <int D>
-PB_DEV void store_nat(u32x4* __restrict__ lds, int tid, const u32x4* r) {
-  constexpr int CPR = D / 8;
-#pragma unroll
-  for (int u = 0; u < CPR / 4; ++u) {
-    const int ci = tid + kAttnThreads * u;
-    const int row = ci / CPR, c = ci % CPR;
-    lds[row * CPR + (c ^ (row & 7))] = r[u];
-  }
+PB_DEV int chunk_at(int r, int c) { return c ^ rowswz<D>(r); }
+
+PB_DEV void dma16(const void* g, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_byte_addr)
+               : "memory", "m0");
 }
-template <int D>
-PB_DEV bf16x8 frag_nat(const u32x4* lds, int row, int c) {
-  return __builtin_bit_cast(bf16x8, lds[row * (D / 8) + (c ^ (row & 7))]);
+PB_DEV void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// This wave's share of a natural tile, rows row0 .. row0 + kTL - 1 of a
+// [rows_valid, ld] token-major matrix, by LDS-DMA (each lane's 16 bytes land
+// at the piece's LDS base + 16 * lane).  Rows past rows_valid are read from
+// the last valid row: finite values that the window mask always zeroes.
+template <int D, int TL>
+PB_DEV void dma_tile(const bf16* __restrict__ base, int ld, int row0, int rows_valid,
+                     uint32_t lds_tile, int wave, int lane) {
+  constexpr int RB = 2 * D;
+  constexpr int BYTES = TL * RB;
+  constexpr int PER_WAVE = BYTES / NW;
+#pragma unroll
+  for (int i = 0; i < PER_WAVE / 1024; ++i) {
+    const int piece = wave * PER_WAVE + i * 1024;
+    const int p = piece + 16 * lane;
+    const int row = p / RB, slot = (p / 16) % (RB / 16);
+    const int c = chunk_at<D>(row, slot);
+    const int t = min(row0 + row, rows_valid - 1);
+    dma16(base + (size_t)t * ld + 8 * c, __builtin_amdgcn_readfirstlane(lds_tile + piece));
+  }
 }
 
-// Transposed tile: D rows (one per feature e) x 64 tokens.  Chunk c of row e
-// holds tokens 16(c/2) + 4(c%2) + {0,1,2,3} then 16(c/2) + 8 + 4(c%2) +
-// {0,1,2,3}: the k order in which an MFMA consumes probabilities straight
-// from its accumulator registers.  Stored at e * 8 + (c ^ (e & 7)).
-// Block bi (0 <= bi < D) = chunk bi & 7 of rows 8 (bi >> 3) .. +7.
-PB_DEV int perm_token(int c, int e) { return 16 * (c >> 1) + 4 * (c & 1) + (e & 3) + 8 * (e >> 2); }
-
+// MFMA operand with 8 consecutive features of token row `row` (k-step ks of
+// the feature contraction, lane half h).
 template <int D>
-PB_DEV void load_t(const bf16* __restrict__ base, int ld, int row0, int rows_valid, int bi,
-                   u32x4* r) {
-  const int c = bi & 7, dg = bi >> 3;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int t = row0 + perm_token(c, e);
-    r[e] = t < rows_valid ? *reinterpret_cast<const u32x4*>(base + (size_t)t * ld + 8 * dg)
-                          : u32x4{0, 0, 0, 0};
-  }
+PB_DEV bf16x8 frag_row(const unsigned char* tile, int row, int ks, int h) {
+  return *reinterpret_cast<const bf16x8*>(tile + row * (2 * D) + chunk_at<D>(row, 2 * ks + h) * 16);
 }
+// MFMA operand with 8 tokens of feature row `e` of the transposed tile, in
+// the order the probabilities sit in a 32 x 32 accumulator: tokens
+// 16 s + 4 h + {0..3} then 16 s + 8 + 4 h + {0..3}.  Two transposing reads:
+// lane 4 j + q of a 16-lane group addresses token kb + j, features
+// (e & ~15) + 4 q .. +3; lane i receives tokens kb .. kb + 3 of feature
+// (e & ~15) + i.
 template <int D>
-PB_DEV void store_t(u32x4* __restrict__ lds, int bi, const u32x4* r) {
-  const int c = bi & 7, dg = bi >> 3;
-  u32x4 t[8];
-  transpose8x8(r, t);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int e = 8 * dg + i;
-    lds[e * 8 + (c ^ (e & 7))] = t[i];
-  }
-}
-PB_DEV bf16x8 frag_t(const u32x4* lds, int e, int c) {
-  return __builtin_bit_cast(bf16x8, lds[e * 8 + (c ^ (e & 7))]);
+PB_DEV bf16x8 frag_tr(const unsigned char* tile, int e, int s, int h, int lane) {
+  const int i = lane & 15, j = i >> 2, q = i & 3;
+  const int d0 = (e & ~15) + 4 * q;
+  const int c = d0 >> 3, off = (d0 & 7) * 2;
+  const int t1 = 16 * s + 4 * h + j, t2 = t1 + 8;
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (PB_LDS s16x4*)(tile + t1 * (2 * D) + chunk_at<D>(t1, c) * 16 + off));
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (PB_LDS s16x4*)(tile + t2 * (2 * D) + chunk_at<D>(t2, c) * 16 + off));
+  const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
+  return bf16x8{a4[0], a4[1], a4[2], a4[3], b4[0], b4[1], b4[2], b4[3]};
 }
 
-// Probabilities for MFMA k-step s (16 tokens) from two 32-token accumulators.
+// Probabilities for MFMA k-step s (16 tokens) from 32-token accumulators.
 PB_DEV bf16x8 probs_frag(const f32x16* p, int s) {
   const f32x16& a = p[s >> 1];
   const int o = 8 * (s & 1);
@@ -112,18 +128,27 @@ PB_DEV f32x16 zero16() {
   return z;
 }
 
+// 8 consecutive features of one token row from global memory (zero if !ok).
+PB_DEV bf16x8 load_row_frag(const bf16* p, bool ok) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+  return ok ? __builtin_bit_cast(bf16x8, v) : bf16x8{};
+}
+
 // ============================================================== forward
+// Workgroup: 32 NW queries of one (batch row, head); wave w owns queries
+// q0 + 32 w .. +31, lane l query q0 + 32 w + (l & 31).  Per key tile:
+// S^T = K Q^T (keys x queries), online softmax per lane, O^T += V^T P^T.
 template <int D>
-__global__ __launch_bounds__(kAttnThreads, 1) void attn_fwd_bf16(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     bf16* __restrict__ O, int ld_o, float* __restrict__ lse, int S, int H, int W, float scale) {
-  constexpr int NB = 32 * 4;                 // queries per workgroup
-  constexpr int NAT = kTile * D / 8;         // u32x4 per natural tile
-  constexpr int TT = D * 8;                  // u32x4 per transposed tile
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  u32x4* const lds0 = (u32x4*)smem;
-  auto kn = [&](int s) { return lds0 + s * (NAT + TT); };
-  auto vt = [&](int s) { return lds0 + s * (NAT + TT) + NAT; };
+  constexpr int TL = kTL;
+  constexpr int NB = 32 * NW;
+  constexpr int TB = TL * 2 * D;  // bytes per tile
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
+  auto k_off = [&](int s) { return (2 * s) * TB; };
+  auto v_off = [&](int s) { return (2 * s + 1) * TB; };
 
   const int nqb = (S + NB - 1) / NB;
   const int q0 = (nqb - 1 - (int)blockIdx.x) * NB;  // longest rows first
@@ -140,9 +165,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_fwd_bf16(
   bf16x8 qf[D / 16];
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks)
-    qf[ks] = q < S ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                    qb + (size_t)q * ld + 16 * ks + 8 * fh))
-                   : bf16x8{};
+    qf[ks] = load_row_frag(qb + (size_t)min(q, S - 1) * ld + 16 * ks + 8 * fh, q < S);
 
   const float c2 = scale * kLog2e;
   float m_run = kNegInf, l_run = 0.f;
@@ -151,40 +174,39 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_fwd_bf16(
   for (int i = 0; i < D / 32; ++i) o[i] = zero16();
 
   const int q_last = min(q0 + NB - 1, S - 1);
-  const int kv_begin = (max(0, q0 - W + 1) / kTile) * kTile;
-  const int ntiles = (q_last - kv_begin) / kTile + 1;
-  // wave's own key range
+  const int kv_begin = (max(0, q0 - W + 1) / TL) * TL;
+  const int ntiles = (q_last - kv_begin) / TL + 1;
   const int w_lo = qw0 - W + 1, w_hi = min(qw0 + 31, S - 1);
 
-  u32x4 rk[D / 32], rv[8];
-  load_nat<D>(kb, ld, kv_begin, S, tid, rk);
-  if (tid < D) load_t<D>(vb, ld, kv_begin, S, tid, rv);
-  store_nat<D>(kn(0), tid, rk);
-  if (tid < D) store_t<D>(vt(0), tid, rv);
-  __syncthreads();
+  dma_tile<D, TL>(kb, ld, kv_begin, S, lds0 + k_off(0), wave, lane);
+  dma_tile<D, TL>(vb, ld, kv_begin, S, lds0 + v_off(0), wave, lane);
 
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1;
-    const int kv0 = kv_begin + t * kTile;
+    const int kv0 = kv_begin + t * TL;
+    wait_dma_all();
+    block_barrier();
     if (t + 1 < ntiles) {
-      load_nat<D>(kb, ld, kv0 + kTile, S, tid, rk);
-      if (tid < D) load_t<D>(vb, ld, kv0 + kTile, S, tid, rv);
+      dma_tile<D, TL>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
+      dma_tile<D, TL>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
     }
-    if (qw0 < S && kv0 <= w_hi && kv0 + kTile - 1 >= w_lo) {
-      f32x16 s[2];
+    if (qw0 < S && kv0 <= w_hi && kv0 + TL - 1 >= w_lo) {
+      const unsigned char* kt = smem + k_off(cur);
+      const unsigned char* vt = smem + v_off(cur);
+      f32x16 s[TL / 32];
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
+      for (int h2 = 0; h2 < TL / 32; ++h2) {
         s[h2] = zero16();
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks)
-          s[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_nat<D>(kn(cur), 32 * h2 + fr, 2 * ks + fh), qf[ks], s[h2], 0, 0, 0);
+          s[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(kt, 32 * h2 + fr, ks, fh),
+                                                          qf[ks], s[h2], 0, 0, 0);
       }
-      const bool full = (kv0 + kTile - 1 <= qw0) && (qw0 + 31 - kv0 < W) &&
-                        (kv0 + kTile <= S) && (qw0 + 32 <= S);
+      const bool full = (kv0 + TL - 1 <= qw0) && (qw0 + 31 - kv0 < W) && (kv0 + TL <= S) &&
+                        (qw0 + 32 <= S);
       float mx = kNegInf;
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+      for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           float x = s[h2][r] * c2;
@@ -199,14 +221,14 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_fwd_bf16(
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float m_new = fmaxf(m_run, mx);
       const float m_use = m_new == kNegInf ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_use);
+      const float alpha = exp2_hw(m_run - m_use);
       m_run = m_new;
       float ls = 0.f;
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+      for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = exp2f(s[h2][r] - m_use);
+          const float p = exp2_hw(s[h2][r] - m_use);
           s[h2][r] = p;
           ls += p;
         }
@@ -216,16 +238,11 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_fwd_bf16(
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2)
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(vt(cur), 32 * db + fr, 2 * s2 + fh),
-                                                          probs_frag(s, s2), o[db], 0, 0, 0);
+        for (int s2 = 0; s2 < TL / 16; ++s2)
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              frag_tr<D>(vt, 32 * db + fr, s2, fh, lane), probs_frag(s, s2), o[db], 0, 0, 0);
       }
     }
-    if (t + 1 < ntiles) {
-      store_nat<D>(kn(cur ^ 1), tid, rk);
-      if (tid < D) store_t<D>(vt(cur ^ 1), tid, rv);
-    }
-    __syncthreads();
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -271,25 +288,27 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(const T* __restrict__ O
 }
 
 // ====================================================== backward: dK, dV
+// Workgroup: 32 NW keys; wave w owns keys k0 + 32 w .. +31 (lane: one key).
+// Per query tile: S = Q K^T and dP = dO V^T (queries x keys), P and
+// dS = P (dP - delta), then dV^T += dO^T P and dK^T += Q^T dS, the
+// transposed operands read from the natural Q and dO tiles.
 template <int D>
-__global__ __launch_bounds__(kAttnThreads, 1) void attn_dkdv_bf16(
+__global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV, int ld_d,
     int S, int H, int W, float scale) {
-  constexpr int NB = 32 * 4;  // keys per workgroup
-  constexpr int NAT = kTile * D / 8, TT = D * 8;
-  constexpr int STAGE = 2 * NAT + 2 * TT + 2 * kTile / 4;  // in u32x4
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  auto qn = [&](int s) { return (u32x4*)smem + s * STAGE; };
-  auto don = [&](int s) { return (u32x4*)smem + s * STAGE + NAT; };
-  auto qt = [&](int s) { return (u32x4*)smem + s * STAGE + 2 * NAT; };
-  auto dot_ = [&](int s) { return (u32x4*)smem + s * STAGE + 2 * NAT + TT; };
-  auto lsd = [&](int s) { return (float*)((u32x4*)smem + s * STAGE + 2 * NAT + 2 * TT); };
+  constexpr int TL = kTLdkv;
+  constexpr int NB = 32 * NW;
+  constexpr int TB = TL * 2 * D;
+  constexpr int STAGE = 2 * TB + 2 * TL * 4;  // Q, dO, then lse*log2e and delta
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
+  auto q_off = [&](int s) { return s * STAGE; };
+  auto g_off = [&](int s) { return s * STAGE + TB; };
+  auto l_off = [&](int s) { return s * STAGE + 2 * TB; };
 
-  const int nkb = (S + NB - 1) / NB;
   const int k0 = (int)blockIdx.x * NB;
-  (void)nkb;
   const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
@@ -306,9 +325,9 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dkdv_bf16(
   bf16x8 kf[D / 16], vf[D / 16];
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
-    const size_t off = (size_t)key * ld + 16 * ks + 8 * fh;
-    kf[ks] = key < S ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kb + off)) : bf16x8{};
-    vf[ks] = key < S ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vb + off)) : bf16x8{};
+    const size_t off = (size_t)min(key, S - 1) * ld + 16 * ks + 8 * fh;
+    kf[ks] = load_row_frag(kb + off, key < S);
+    vf[ks] = load_row_frag(vb + off, key < S);
   }
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -317,63 +336,59 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dkdv_bf16(
   const float c2 = scale * kLog2e;
   const int k_last = min(k0 + NB - 1, S - 1);
   const int q_end = min(S - 1, k_last + W - 1);
-  const int ntiles = (q_end - k0) / kTile + 1;
+  const int ntiles = (q_end - k0) / TL + 1;
   const int w_lo = kw0, w_hi = min(S - 1, kw0 + 31 + W - 1);  // queries this wave needs
 
-  u32x4 rq[D / 32], rg[D / 32], rt[8];
   float rl = 0.f;
-  auto load_stage = [&](int qs) {
-    load_nat<D>(qb, ld, qs, S, tid, rq);
-    load_nat<D>(gb, ld_o, qs, S, tid, rg);
-    if (tid < D) load_t<D>(qb, ld, qs, S, tid, rt);
-    else if (tid >= 128 && tid < 128 + D) load_t<D>(gb, ld_o, qs, S, tid - 128, rt);
-    if (tid < kTile) rl = qs + tid < S ? lseb[qs + tid] * kLog2e : __builtin_huge_valf();
-    else if (tid < 2 * kTile) rl = qs + tid - kTile < S ? delb[qs + tid - kTile] : 0.f;
+  auto issue_stage = [&](int qs, int s) {
+    dma_tile<D, TL>(qb, ld, qs, S, lds0 + q_off(s), wave, lane);
+    dma_tile<D, TL>(gb, ld_o, qs, S, lds0 + g_off(s), wave, lane);
+    if (tid < TL) rl = qs + tid < S ? lseb[qs + tid] * kLog2e : __builtin_huge_valf();
+    else if (tid < 2 * TL) rl = qs + tid - TL < S ? delb[qs + tid - TL] : 0.f;
   };
-  auto store_stage = [&](int s) {
-    store_nat<D>(qn(s), tid, rq);
-    store_nat<D>(don(s), tid, rg);
-    if (tid < D) store_t<D>(qt(s), tid, rt);
-    else if (tid >= 128 && tid < 128 + D) store_t<D>(dot_(s), tid - 128, rt);
-    if (tid < 2 * kTile) lsd(s)[tid] = rl;
+  auto finish_stage = [&](int s) {
+    if (tid < 2 * TL) ((float*)(smem + l_off(s)))[tid] = rl;
   };
-  load_stage(k0);
-  store_stage(0);
-  __syncthreads();
+  issue_stage(k0, 0);
+  finish_stage(0);
 
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1;
-    const int qs = k0 + t * kTile;
-    if (t + 1 < ntiles) load_stage(qs + kTile);
-    if (kw0 < S && qs <= w_hi && qs + kTile - 1 >= w_lo) {
-      f32x16 p[2], ds[2];
+    const int qs = k0 + t * TL;
+    wait_dma_all();
+    block_barrier();
+    if (t + 1 < ntiles) issue_stage(qs + TL, cur ^ 1);
+    if (kw0 < S && qs <= w_hi && qs + TL - 1 >= w_lo) {
+      const unsigned char* qt = smem + q_off(cur);
+      const unsigned char* gt = smem + g_off(cur);
+      const float* ls = (const float*)(smem + l_off(cur));
+      f32x16 p[TL / 32], ds[TL / 32];
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
+      for (int h2 = 0; h2 < TL / 32; ++h2) {
         p[h2] = zero16();
         ds[h2] = zero16();
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          p[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_nat<D>(qn(cur), 32 * h2 + fr, 2 * ks + fh), kf[ks], p[h2], 0, 0, 0);
-          ds[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_nat<D>(don(cur), 32 * h2 + fr, 2 * ks + fh), vf[ks], ds[h2], 0, 0, 0);
+          p[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(qt, 32 * h2 + fr, ks, fh),
+                                                          kf[ks], p[h2], 0, 0, 0);
+          ds[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(gt, 32 * h2 + fr, ks, fh),
+                                                           vf[ks], ds[h2], 0, 0, 0);
         }
       }
       // lane holds key `key` and queries qs + 32 h2 + 8 j + 4 fh + i (r = 4 j + i)
-      const bool full = (qs >= kw0 + 31) && (qs + kTile - 1 - kw0 < W) && (qs + kTile <= S) &&
+      const bool full = (qs >= kw0 + 31) && (qs + TL - 1 - kw0 < W) && (qs + TL <= S) &&
                         (kw0 + 32 <= S);
-      const float* ls = lsd(cur);
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+      for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int ql = 32 * h2 + 8 * j + 4 * fh;
           const f32x4 L4 = *reinterpret_cast<const f32x4*>(ls + ql);
-          const f32x4 D4 = *reinterpret_cast<const f32x4*>(ls + kTile + ql);
+          const f32x4 D4 = *reinterpret_cast<const f32x4*>(ls + TL + ql);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int r = 4 * j + i;
-            float pv = exp2f(p[h2][r] * c2 - L4[i]);
+            float pv = exp2_hw(p[h2][r] * c2 - L4[i]);
             if (!full) {
               const int dist = qs + ql + i - key;
               if (dist < 0 || dist >= W || qs + ql + i >= S) pv = 0.f;
@@ -385,15 +400,14 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dkdv_bf16(
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2) {
-          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(dot_(cur), 32 * db + fr, 2 * s2 + fh),
-                                                           probs_frag(p, s2), dv[db], 0, 0, 0);
-          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(qt(cur), 32 * db + fr, 2 * s2 + fh),
-                                                           probs_frag(ds, s2), dk[db], 0, 0, 0);
+        for (int s2 = 0; s2 < TL / 16; ++s2) {
+          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              frag_tr<D>(gt, 32 * db + fr, s2, fh, lane), probs_frag(p, s2), dv[db], 0, 0, 0);
+          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              frag_tr<D>(qt, 32 * db + fr, s2, fh, lane), probs_frag(ds, s2), dk[db], 0, 0, 0);
         }
     }
-    if (t + 1 < ntiles) store_stage(cur ^ 1);
-    __syncthreads();
+    if (t + 1 < ntiles) finish_stage(cur ^ 1);
   }
 
   if (key < S) {
@@ -416,19 +430,22 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dkdv_bf16(
 }
 
 // ============================================================ backward: dQ
+// Workgroup: 32 NW queries; per key tile: S^T = K Q^T and dP^T = V dO^T,
+// dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T (K^T read from the natural K
+// tile).
 template <int D>
-__global__ __launch_bounds__(kAttnThreads, 1) void attn_dq_bf16(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_dq_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dQ, int ld_d, int S, int H, int W,
     float scale) {
-  constexpr int NB = 32 * 4;
-  constexpr int NAT = kTile * D / 8, TT = D * 8;
-  constexpr int STAGE = 2 * NAT + TT;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  auto kn = [&](int s) { return (u32x4*)smem + s * STAGE; };
-  auto vn = [&](int s) { return (u32x4*)smem + s * STAGE + NAT; };
-  auto kt = [&](int s) { return (u32x4*)smem + s * STAGE + 2 * NAT; };
+  constexpr int TL = kTL;
+  constexpr int NB = 32 * NW;
+  constexpr int TB = TL * 2 * D;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
+  auto k_off = [&](int s) { return (2 * s) * TB; };
+  auto v_off = [&](int s) { return (2 * s + 1) * TB; };
 
   const int nqb = (S + NB - 1) / NB;
   const int q0 = (nqb - 1 - (int)blockIdx.x) * NB;
@@ -443,15 +460,12 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dq_bf16(
 
   const int qw0 = q0 + 32 * wave;
   const int q = qw0 + fr;
+  const int qc = min(q, S - 1);
   bf16x8 qf[D / 16], gf[D / 16];
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
-    qf[ks] = q < S ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                    qb + (size_t)q * ld + 16 * ks + 8 * fh))
-                   : bf16x8{};
-    gf[ks] = q < S ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                    gb + (size_t)q * ld_o + 16 * ks + 8 * fh))
-                   : bf16x8{};
+    qf[ks] = load_row_frag(qb + (size_t)qc * ld + 16 * ks + 8 * fh, q < S);
+    gf[ks] = load_row_frag(gb + (size_t)qc * ld_o + 16 * ks + 8 * fh, q < S);
   }
   const size_t row_off = ((size_t)b * H + head) * S;
   const float L2 = q < S ? lse[row_off + q] * kLog2e : 0.f;
@@ -463,50 +477,45 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dq_bf16(
   for (int i = 0; i < D / 32; ++i) dq[i] = zero16();
 
   const int q_last = min(q0 + NB - 1, S - 1);
-  const int kv_begin = (max(0, q0 - W + 1) / kTile) * kTile;
-  const int ntiles = (q_last - kv_begin) / kTile + 1;
+  const int kv_begin = (max(0, q0 - W + 1) / TL) * TL;
+  const int ntiles = (q_last - kv_begin) / TL + 1;
   const int w_lo = qw0 - W + 1, w_hi = min(qw0 + 31, S - 1);
 
-  u32x4 rk[D / 32], rv[D / 32], rt[8];
-  auto load_stage = [&](int ks0) {
-    load_nat<D>(kb, ld, ks0, S, tid, rk);
-    load_nat<D>(vb, ld, ks0, S, tid, rv);
-    if (tid < D) load_t<D>(kb, ld, ks0, S, tid, rt);
-  };
-  auto store_stage = [&](int s) {
-    store_nat<D>(kn(s), tid, rk);
-    store_nat<D>(vn(s), tid, rv);
-    if (tid < D) store_t<D>(kt(s), tid, rt);
-  };
-  load_stage(kv_begin);
-  store_stage(0);
-  __syncthreads();
+  dma_tile<D, TL>(kb, ld, kv_begin, S, lds0 + k_off(0), wave, lane);
+  dma_tile<D, TL>(vb, ld, kv_begin, S, lds0 + v_off(0), wave, lane);
 
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1;
-    const int kv0 = kv_begin + t * kTile;
-    if (t + 1 < ntiles) load_stage(kv0 + kTile);
-    if (qw0 < S && kv0 <= w_hi && kv0 + kTile - 1 >= w_lo) {
-      f32x16 p[2], ds[2];
+    const int kv0 = kv_begin + t * TL;
+    wait_dma_all();
+    block_barrier();
+    if (t + 1 < ntiles) {
+      dma_tile<D, TL>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
+      dma_tile<D, TL>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
+    }
+    if (qw0 < S && kv0 <= w_hi && kv0 + TL - 1 >= w_lo) {
+      const unsigned char* kt = smem + k_off(cur);
+      const unsigned char* vt = smem + v_off(cur);
+      f32x16 p[TL / 32], ds[TL / 32];
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
+      for (int h2 = 0; h2 < TL / 32; ++h2) {
         p[h2] = zero16();
         ds[h2] = zero16();
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          p[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_nat<D>(kn(cur), 32 * h2 + fr, 2 * ks + fh), qf[ks], p[h2], 0, 0, 0);
-          ds[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_nat<D>(vn(cur), 32 * h2 + fr, 2 * ks + fh), gf[ks], ds[h2], 0, 0, 0);
+          p[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(kt, 32 * h2 + fr, ks, fh),
+                                                          qf[ks], p[h2], 0, 0, 0);
+          ds[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(vt, 32 * h2 + fr, ks, fh),
+                                                           gf[ks], ds[h2], 0, 0, 0);
         }
       }
-      const bool full = (kv0 + kTile - 1 <= qw0) && (qw0 + 31 - kv0 < W) &&
-                        (kv0 + kTile <= S) && (qw0 + 32 <= S);
+      const bool full = (kv0 + TL - 1 <= qw0) && (qw0 + 31 - kv0 < W) && (kv0 + TL <= S) &&
+                        (qw0 + 32 <= S);
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
+      for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float pv = exp2f(p[h2][r] * c2 - L2);
+          float pv = exp2_hw(p[h2][r] * c2 - L2);
           if (!full) {
             const int k = kv0 + 32 * h2 + 8 * (r >> 2) + 4 * fh + (r & 3);
             const int dist = q - k;
@@ -517,12 +526,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_dq_bf16(
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2)
-          dq[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(kt(cur), 32 * db + fr, 2 * s2 + fh),
-                                                           probs_frag(ds, s2), dq[db], 0, 0, 0);
+        for (int s2 = 0; s2 < TL / 16; ++s2)
+          dq[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              frag_tr<D>(kt, 32 * db + fr, s2, fh, lane), probs_frag(ds, s2), dq[db], 0, 0, 0);
     }
-    if (t + 1 < ntiles) store_stage(cur ^ 1);
-    __syncthreads();
   }
 
   if (q < S) {
@@ -646,19 +653,19 @@ __global__ __launch_bounds__(64) void attn_dkdv_f32(const float* __restrict__ Q,
 }
 
 template <int D>
-size_t fwd_lds() { return 2 * ((size_t)kTile * D / 8 + (size_t)D * 8) * 16; }
+size_t fwd_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 template <int D>
-size_t dkdv_lds() { return 2 * (2 * (size_t)kTile * D / 8 + 2 * (size_t)D * 8 + 2 * kTile / 4) * 16; }
+size_t dkdv_lds() { return 2 * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4); }
 template <int D>
-size_t dq_lds() { return 2 * (2 * (size_t)kTile * D / 8 + (size_t)D * 8) * 16; }
+size_t dq_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 
 template <int D>
 void fwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v, int ld,
            void* o, int ld_o, float* lse, hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)D);
   if (dt == Dt::BF16) {
-    dim3 g((a.seq + 127) / 128, a.heads, a.batch);
-    attn_fwd_bf16<D><<<g, kAttnThreads, fwd_lds<D>(), s>>>(
+    dim3 g((a.seq + 32 * NW - 1) / (32 * NW), a.heads, a.batch);
+    attn_fwd_bf16<D><<<g, kThreads, fwd_lds<D>(), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (bf16*)o, ld_o, lse, a.seq, a.heads,
         a.window, scale);
   } else {
@@ -677,11 +684,11 @@ void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
   if (dt == Dt::BF16) {
     attn_delta_kernel<bf16><<<(nrows + 255) / 256, 256, 0, s>>>(
         (const bf16*)o, ld_o, (const bf16*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
-    dim3 g((a.seq + 127) / 128, a.heads, a.batch);
-    attn_dkdv_bf16<D><<<g, kAttnThreads, dkdv_lds<D>(), s>>>(
+    dim3 g((a.seq + 32 * NW - 1) / (32 * NW), a.heads, a.batch);
+    attn_dkdv_bf16<D><<<g, kThreads, dkdv_lds<D>(), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (const bf16*)d_o, ld_do, lse, delta,
         (bf16*)dk, (bf16*)dv, ld_d, a.seq, a.heads, a.window, scale);
-    attn_dq_bf16<D><<<g, kAttnThreads, dq_lds<D>(), s>>>(
+    attn_dq_bf16<D><<<g, kThreads, dq_lds<D>(), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (const bf16*)d_o, ld_do, lse, delta,
         (bf16*)dq, ld_d, a.seq, a.heads, a.window, scale);
   } else {
