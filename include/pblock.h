@@ -110,15 +110,26 @@ size_t pblock_saved_bytes(const pb_config* cfg);
  * offsets must hold 6 entries.  Host only. */
 pb_status pblock_saved_offsets(const pb_config* cfg, size_t* offsets);
 
-/* Workspace bytes for pblock_forward (backward == 0; needed only when the
- * forward call gets saved == NULL, which then keeps its stash in the
- * workspace) or for pblock_backward (backward != 0).  0 on a bad cfg. */
-size_t pblock_workspace_bytes(const pb_config* cfg, int backward);
+/* Workspace sizes.  mode:
+ *   PB_WS_FORWARD             pblock_forward with a caller stash (saved != NULL)
+ *   PB_WS_FORWARD_WITH_STASH  pblock_forward with saved == NULL: the stash is
+ *                             kept at the start of ws
+ *   PB_WS_BACKWARD            pblock_backward
+ * The sizes include a region for tail-split GEMM partial tiles (the last,
+ * partial wave of output tiles is split along K so the chip stays full).
+ * That region is optional: a smaller ws (down to 0 bytes for PB_WS_FORWARD,
+ * the stash for PB_WS_FORWARD_WITH_STASH, and the size without the region
+ * for PB_WS_BACKWARD) also works, unsplit (results then differ only in
+ * rounding order).  0 on a bad cfg. */
+enum { PB_WS_FORWARD_WITH_STASH = 0, PB_WS_BACKWARD = 1, PB_WS_FORWARD = 2 };
+size_t pblock_workspace_bytes(const pb_config* cfg, int mode);
 
 /* Forward pass of the block (Eq. 2).  Writes y [T, H].  When saved is not
- * NULL it also fills the stash that pblock_backward reads; when it is NULL
- * (inference) the stash goes to ws, which must then hold
- * pblock_workspace_bytes(cfg, 0) bytes.  ws may be NULL when saved is not. */
+ * NULL it also fills the stash that pblock_backward reads, and ws (NULL or
+ * up to pblock_workspace_bytes(cfg, PB_WS_FORWARD) bytes) only holds GEMM
+ * partial tiles.  When saved is NULL (inference) the stash goes to the start
+ * of ws, which must then hold at least the stash
+ * (pblock_workspace_bytes(cfg, PB_WS_FORWARD_WITH_STASH) for full speed). */
 pb_status pblock_forward(const pb_config* cfg, const void* x,
                          const void* ln_gamma, const void* ln_beta,
                          const void* w_in, const void* b_in,
@@ -129,7 +140,8 @@ pb_status pblock_forward(const pb_config* cfg, const void* x,
 /* Backward pass: the gradients of sum(y * dy) with respect to x and every
  * parameter, given the stash of the matching forward call.  dx is in the
  * activation dtype; the six parameter gradients are fp32 and overwritten.
- * ws must hold pblock_workspace_bytes(cfg, 1) bytes. */
+ * ws should hold pblock_workspace_bytes(cfg, PB_WS_BACKWARD) bytes (fewer,
+ * down to the size without the GEMM partial-tile region, also works). */
 pb_status pblock_backward(const pb_config* cfg, const void* x,
                           const void* ln_gamma, const void* ln_beta,
                           const void* w_in, const void* b_in,

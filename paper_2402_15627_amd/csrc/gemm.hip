@@ -17,6 +17,8 @@
 // pass.
 //
 // fp32 path: a plain LDS-tiled SIMT kernel with the same epilogues.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -76,14 +78,15 @@ constexpr int kTileBytes = kBM * kBK * 2;  // one operand tile (32 KB)
 // 16-byte chunk c (0..7) of LDS row `row` lives at physical chunk swz(row, c).
 PB_DEV int swz(int row, int c) { return c ^ ((row ^ (row >> 3)) & 7); }
 
-// Tile order: workgroup b runs on XCD b % 8; give each XCD a contiguous run
-// of logical tiles, then walk tiles in groups of 8 tile-rows so that
-// concurrently running workgroups on one XCD share operand strips in its L2.
-PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int nt = tiles_m * tiles_n;
-  const int bid = blockIdx.x;
-  const int q = nt / 8, r = nt % 8, x = bid % 8;
-  const int lid = x * q + min(x, r) + bid / 8;
+// Tile order.  Workgroup b runs on XCD b % 8; xcd_remap gives each XCD a
+// contiguous run of logical ids, and tile_of walks logical ids in groups of 8
+// tile-rows, so concurrently running workgroups on one XCD share operand
+// strips in its L2.
+PB_DEV int xcd_remap(int bid, int n) {
+  const int q = n / 8, r = n % 8, x = bid % 8;
+  return x * q + min(x, r) + bid / 8;
+}
+PB_DEV void tile_of(int lid, int tiles_m, int tiles_n, int& tm, int& tn) {
   constexpr int G = 8;
   const int per_group = G * tiles_n;
   const int group = lid / per_group;
@@ -92,6 +95,9 @@ PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
   const int in_group = lid - group * per_group;
   tm = first_m + in_group % gsize;
   tn = in_group / gsize;
+}
+PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+  tile_of(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
 }
 
 // One 256 x 64 operand tile, global -> registers -> LDS.
@@ -337,20 +343,39 @@ PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, in
   }
 }
 
+// Work items: the first n_full workgroups compute whole tiles (logical ids
+// 0 .. n_full - 1); the remaining tail * splits workgroups each compute one
+// K-slice of one of the last `tail` tiles and store its fp32 partial tile
+// (256 x 256, row-major) to part, for splitk_reduce.
 template <bool AK, bool BK, Epi EPI, bool GT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* __restrict__ A,
                                                                     int lda,
                                                                     const bf16* __restrict__ B,
                                                                     int ldb, int M, int N, int K,
-                                                                    EpiArgs ep) {
+                                                                    EpiArgs ep, int n_full,
+                                                                    int splits,
+                                                                    float* __restrict__ part) {
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
   auto a_off = [&](int s) { return (2 * s) * kTileBytes; };
   auto b_off = [&](int s) { return (2 * s + 1) * kTileBytes; };
 
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+  const int nk_all = K / kBK;
+  int lid, slice = -1, kt0 = 0, kt1 = nk_all;
+  if ((int)blockIdx.x < n_full) {
+    lid = xcd_remap(blockIdx.x, n_full);
+  } else {
+    const int tail = tiles_m * tiles_n - n_full;
+    const int j = xcd_remap(blockIdx.x - n_full, tail * splits);
+    lid = n_full + j / splits;
+    slice = j % splits;
+    const int chunk = (nk_all + splits - 1) / splits;
+    kt0 = min(nk_all, slice * chunk);
+    kt1 = min(nk_all, kt0 + chunk);
+  }
   int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
+  tile_of(lid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
@@ -363,16 +388,17 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  const int nk = K / kBK;
-  dma_tile<AK>(A, lda, m0, M, 0, lds0 + a_off(0), wave, lane);
-  dma_tile<BK>(B, ldb, n0, N, 0, lds0 + b_off(0), wave, lane);
+  if (kt0 < kt1) {
+    dma_tile<AK>(A, lda, m0, M, kt0 * kBK, lds0 + a_off(0), wave, lane);
+    dma_tile<BK>(B, ldb, n0, N, kt0 * kBK, lds0 + b_off(0), wave, lane);
+  }
 
   const int fr = lane & 31, fh = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
     wait_dma_all();   // this wave's pieces of stage cur have landed
     block_barrier();  // everyone's have; everyone is done reading stage cur ^ 1
-    if (kt + 1 < nk) {
+    if (kt + 1 < kt1) {
       dma_tile<AK>(A, lda, m0, M, (kt + 1) * kBK, lds0 + a_off(cur ^ 1), wave, lane);
       dma_tile<BK>(B, ldb, n0, N, (kt + 1) * kBK, lds0 + b_off(cur ^ 1), wave, lane);
     }
@@ -398,6 +424,24 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     }
   }
 
+  if (slice >= 0) {
+    // partial tile of one K-slice, stored whole (bounds are applied on reduce)
+    float* pt = part + ((size_t)(lid - n_full) * splits + slice) * (kBM * kBN);
+#pragma unroll
+    for (int i = 0; i < kTM; ++i) {
+      const int ml = wm + 32 * i + fr;
+#pragma unroll
+      for (int j = 0; j < kTN; ++j)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int nl = wn + 32 * j + 8 * jj + 4 * fh;
+          *reinterpret_cast<f32x4*>(pt + ml * kBN + nl) =
+              f32x4{acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
+                    acc[i][j][4 * jj + 3]};
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < kTM; ++i) {
     const int m = m0 + wm + 32 * i + fr;
@@ -414,6 +458,27 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
         }
       }
   }
+}
+
+// Sum of the K-slice partials of each tail tile, in slice order (so the
+// result does not depend on timing), then the epilogue.  64 workgroups per
+// tile, each thread four consecutive columns of one row.
+template <Epi EPI, bool GT>
+__global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part, int M, int N,
+                                                     int n_full, int splits, EpiArgs ep) {
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+  const int t_local = blockIdx.x / 64;
+  const int g = (blockIdx.x % 64) * 256 + threadIdx.x;  // 0 .. 16383
+  const int row = g / (kBN / 4), col = (g % (kBN / 4)) * 4;
+  int tm, tn;
+  tile_of(n_full + t_local, tiles_m, tiles_n, tm, tn);
+  const int m = tm * kBM + row, n = tn * kBN + col;
+  if (m >= M || n >= N) return;
+  const float* p = part + (size_t)t_local * splits * (kBM * kBN) + row * kBN + col;
+  f32x4 sum = *reinterpret_cast<const f32x4*>(p);
+  for (int sl = 1; sl < splits; ++sl) sum += *reinterpret_cast<const f32x4*>(p + (size_t)sl * kBM * kBN);
+  float v[4] = {sum[0], sum[1], sum[2], sum[3]};
+  epi_store4<bf16, EPI, GT>(ep, m, n, v);
 }
 
 // ----------------------------------------------------------- fp32 SIMT GEMM
@@ -464,14 +529,20 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 
 template <bool AK, bool BK, Epi EPI, bool GT>
 void gemm_dispatch_layout(Dt dt, const void* A, int lda, const void* B, int ldb, int M, int N,
-                          int K, const EpiArgs& ep, hipStream_t s) {
+                          int K, const EpiArgs& ep, float* split_ws, size_t split_ws_floats,
+                          hipStream_t s) {
   if (dt == Dt::BF16) {
     const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
     const size_t lds = 4 * (size_t)kTileBytes;
-    if (K % kBK == 0)
-      gemm_bf16_dma_kernel<AK, BK, EPI, GT><<<tiles, kThreads, lds, s>>>(
-          (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
-    else
+    if (K % kBK == 0) {
+      SplitPlan sp = gemm_split_plan(dt, M, N, K);
+      if (sp.tail > 0 && (!split_ws || split_ws_floats < gemm_split_floats(sp)))
+        sp = SplitPlan{tiles, 0, 1};
+      gemm_bf16_dma_kernel<AK, BK, EPI, GT><<<sp.n_full + sp.tail * sp.splits, kThreads, lds, s>>>(
+          (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep, sp.n_full, sp.splits, split_ws);
+      if (sp.tail > 0)
+        splitk_reduce<EPI, GT><<<sp.tail * 64, 256, 0, s>>>(split_ws, M, N, sp.n_full, sp.splits, ep);
+    } else
       gemm_bf16_kernel<AK, BK, EPI, GT><<<tiles, kThreads, lds, s>>>(
           (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, ep);
   } else {
@@ -483,32 +554,52 @@ void gemm_dispatch_layout(Dt dt, const void* A, int lda, const void* B, int ldb,
 
 template <Epi EPI, bool GT>
 void gemm_dispatch(Dt dt, bool ak, bool bk, const void* A, int lda, const void* B, int ldb,
-                   int M, int N, int K, const EpiArgs& ep, hipStream_t s) {
-  if (ak && bk) gemm_dispatch_layout<true, true, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
-  else if (ak) gemm_dispatch_layout<true, false, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
-  else if (bk) gemm_dispatch_layout<false, true, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
-  else gemm_dispatch_layout<false, false, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, s);
+                   int M, int N, int K, const EpiArgs& ep, float* ws, size_t wsf, hipStream_t s) {
+  if (ak && bk) gemm_dispatch_layout<true, true, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, ws, wsf, s);
+  else if (ak) gemm_dispatch_layout<true, false, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, ws, wsf, s);
+  else if (bk) gemm_dispatch_layout<false, true, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, ws, wsf, s);
+  else gemm_dispatch_layout<false, false, EPI, GT>(dt, A, lda, B, ldb, M, N, K, ep, ws, wsf, s);
 }
 
 }  // namespace
 
+SplitPlan gemm_split_plan(Dt dt, int M, int N, int K) {
+  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  SplitPlan none{tiles, 0, 1};
+  if (dt != Dt::BF16 || K % kBK != 0) return none;
+  constexpr int kCUs = 256;  // MI355X
+  const int n_full = tiles / kCUs * kCUs;
+  const int tail = tiles - n_full;
+  if (n_full == 0 || tail == 0) return none;
+  const int splits = std::min(kCUs / tail, K / kBK);
+  if (splits < 2) return none;
+  return SplitPlan{n_full, tail, splits};
+}
+
+size_t gemm_split_floats(const SplitPlan& p) {
+  return (size_t)p.tail * p.splits * kBM * kBN;
+}
+
 void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,
-                 const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, hipStream_t s) {
+                 const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, float* split_ws,
+                 size_t split_ws_floats, hipStream_t s) {
   const bool gt = ep.gelu_tanh != 0;
+  float* w = split_ws;
+  const size_t wf = split_ws_floats;
   switch (epi) {
     case Epi::StoreF32:
-      gemm_dispatch<Epi::StoreF32, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      gemm_dispatch<Epi::StoreF32, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
       break;
     case Epi::BiasGelu:
-      if (gt) gemm_dispatch<Epi::BiasGelu, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
-      else gemm_dispatch<Epi::BiasGelu, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      if (gt) gemm_dispatch<Epi::BiasGelu, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
+      else gemm_dispatch<Epi::BiasGelu, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
       break;
     case Epi::BiasResid:
-      gemm_dispatch<Epi::BiasResid, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      gemm_dispatch<Epi::BiasResid, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
       break;
     case Epi::DgeluSplit:
-      if (gt) gemm_dispatch<Epi::DgeluSplit, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
-      else gemm_dispatch<Epi::DgeluSplit, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, s);
+      if (gt) gemm_dispatch<Epi::DgeluSplit, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
+      else gemm_dispatch<Epi::DgeluSplit, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
       break;
   }
 }

@@ -57,8 +57,20 @@ struct EpiArgs {
   int col2 = 0;
   int gelu_tanh = 1;
 };
+// Tail split: the first n_full tiles (a whole number of 256-tile waves) are
+// computed whole; each of the last `tail` tiles is split into `splits`
+// K-slices whose fp32 partial tiles go to a workspace and are summed in slice
+// order by a second kernel that applies the epilogue.  Only for the bf16
+// LDS-DMA path (K a multiple of 64); {tiles, 0, 1} means no split.
+struct SplitPlan {
+  int n_full, tail, splits;
+};
+SplitPlan gemm_split_plan(Dt dt, int M, int N, int K);
+size_t gemm_split_floats(const SplitPlan& p);
+// split_ws may be NULL (or too small): the GEMM then runs unsplit.
 void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,
-                 const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, hipStream_t s);
+                 const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, float* split_ws,
+                 size_t split_ws_floats, hipStream_t s);
 
 // -------------------------------------------------------------- attention
 // Causal sliding-window attention over [batch, seq] rows; q/k/v/o/do/dq/dk/dv

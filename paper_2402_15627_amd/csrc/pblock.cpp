@@ -4,6 +4,8 @@
 #include "pblock.h"
 
 #include <math.h>
+
+#include <algorithm>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -109,8 +111,23 @@ SavedLayout saved_layout(const Dims& d) {
   return L;
 }
 
+// fp32 floats of tail-split partial tiles the forward / backward GEMMs use.
+size_t split_floats_fwd(const Dims& d, pb::Dt dt) {
+  const int T = (int)d.T, H = (int)d.H, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  return std::max(pb::gemm_split_floats(pb::gemm_split_plan(dt, T, N_in, H)),
+                  pb::gemm_split_floats(pb::gemm_split_plan(dt, T, H, K_out)));
+}
+size_t split_floats_bwd(const Dims& d, pb::Dt dt) {
+  const int T = (int)d.T, H = (int)d.H, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  size_t m = pb::gemm_split_floats(pb::gemm_split_plan(dt, T, K_out, H));
+  m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, H, K_out, T)));
+  m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, T, H, N_in)));
+  m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, N_in, H, T)));
+  return m;
+}
+
 struct BwdLayout {
-  size_t d_o, dz, dh, delta, pdg, pdb, part, total;
+  size_t d_o, dz, dh, delta, pdg, pdb, part, split, base, total;
 };
 BwdLayout bwd_layout(const Dims& d) {
   BwdLayout L;
@@ -133,6 +150,8 @@ BwdLayout bwd_layout(const Dims& d) {
   if (p2 > part) part = p2;
   if (p3 > part) part = p3;
   L.part = take(part * 4);
+  L.base = o;  // required; the tail-split region after it is optional
+  L.split = take(split_floats_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32) * 4);
   L.total = o;
   return L;
 }
@@ -221,10 +240,16 @@ pb_status pblock_saved_offsets(const pb_config* cfg, size_t* offsets) {
   return PB_OK;
 }
 
-size_t pblock_workspace_bytes(const pb_config* cfg, int backward) {
+size_t pblock_workspace_bytes(const pb_config* cfg, int mode) {
   if (check_config(cfg) != PB_OK) return 0;
   const Dims d = dims_of(cfg);
-  return backward ? bwd_layout(d).total : saved_layout(d).total;
+  const size_t split = align256(split_floats_fwd(d, dt_of(cfg)) * 4);
+  switch (mode) {
+    case PB_WS_FORWARD_WITH_STASH: return saved_layout(d).total + split;
+    case PB_WS_BACKWARD: return bwd_layout(d).total;
+    case PB_WS_FORWARD: return split;
+    default: return 0;
+  }
 }
 
 pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gamma,
@@ -242,17 +267,24 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   PB_CHECK(check_ptr(y, "y"));
   const Dims d = dims_of(cfg);
   const SavedLayout L = saved_layout(d);
+  const pb::Dt dt = dt_of(cfg);
   void* stash = saved;
+  char* split_base = (char*)ws;
+  size_t split_bytes = ws ? ws_bytes : 0;
   if (stash) {
     PB_CHECK(check_ptr(stash, "saved"));
+    if (ws) PB_CHECK(check_ptr(ws, "ws"));
   } else {
     PB_CHECK(check_ptr(ws, "ws (needed when saved is NULL)"));
     if (ws_bytes < L.total)
       return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed to hold the stash", ws_bytes,
                   L.total);
     stash = ws;
+    split_base = (char*)ws + L.total;
+    split_bytes = ws_bytes - L.total;
   }
-  const pb::Dt dt = dt_of(cfg);
+  float* split_ws = (float*)split_base;
+  const size_t split_f = split_bytes / 4;
   const size_t e = d.esz;
   char* sb = (char*)stash;
   void* h = sb + L.off[0];
@@ -280,7 +312,8 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   e1.gelu_tanh = cfg->gelu_tanh;
   {
     StepScope sc(PB_STEP_IN_PROJ, stream);
-    pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h, H, w_in, H, T, N_in, H, e1, stream);
+    pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h, H, w_in, H, T, N_in, H, e1, split_ws,
+                    split_f, stream);
   }
   // F3: sliding-window attention, O -> C[:, :A]
   {
@@ -297,7 +330,7 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   {
     StepScope sc(PB_STEP_OUT_PROJ, stream);
     pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, c, K_out, w_out, K_out, T, H, K_out, e2,
-                    stream);
+                    split_ws, split_f, stream);
   }
   return finish_launches();
 }
@@ -328,8 +361,8 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   PB_CHECK(check_ptr(ws, "ws"));
   const Dims d = dims_of(cfg);
   const BwdLayout W = bwd_layout(d);
-  if (ws_bytes < W.total)
-    return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, W.total);
+  if (ws_bytes < W.base)
+    return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, W.base);
   const SavedLayout L = saved_layout(d);
   const pb::Dt dt = dt_of(cfg);
   const size_t e = d.esz;
@@ -348,6 +381,8 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   float* pdg = (float*)(wb + W.pdg);
   float* pdb = (float*)(wb + W.pdb);
   float* part = (float*)(wb + W.part);
+  float* split_ws = (float*)(wb + W.split);
+  const size_t split_f = ws_bytes >= W.total ? (W.total - W.split) / 4 : 0;
   const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
   (void)ln_beta;
   (void)b_in;
@@ -366,7 +401,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   {
     StepScope sc(PB_STEP_DC, stream);
     pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
-                    stream);
+                    split_ws, split_f, stream);
   }
   // B2: dW_out = dy^T C (contraction over tokens); db_out = sum_t dy
   pb::EpiArgs e2;
@@ -375,7 +410,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   {
     StepScope sc(PB_STEP_DW_OUT, stream);
     pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
-                    stream);
+                    split_ws, split_f, stream);
   }
   {
     StepScope sc(PB_STEP_DB_OUT, stream);
@@ -395,7 +430,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   {
     StepScope sc(PB_STEP_DH, stream);
     pb::launch_gemm(dt, pb::Epi::StoreF32, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
-                    stream);
+                    split_ws, split_f, stream);
   }
   // B5: dW_in = dZ^T h; db_in = sum_t dZ
   pb::EpiArgs e5;
@@ -404,7 +439,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   {
     StepScope sc(PB_STEP_DW_IN, stream);
     pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5,
-                    stream);
+                    split_ws, split_f, stream);
   }
   {
     StepScope sc(PB_STEP_DB_IN, stream);

@@ -17,6 +17,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libpblock.so")
 
 PB_BF16, PB_F32 = 0, 1
+# pblock_workspace_bytes modes
+WS_FORWARD_WITH_STASH, WS_BACKWARD, WS_FORWARD = 0, 1, 2
 STATUS = {0: "PB_OK", 1: "PB_ERR_INVALID_ARG", 2: "PB_ERR_UNSUPPORTED", 3: "PB_ERR_WORKSPACE",
           4: "PB_ERR_HIP"}
 SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
@@ -139,8 +141,9 @@ def pblock_saved_offsets(cfg: PbConfig) -> dict:
     return dict(zip(SAVED_REGIONS, list(arr)))
 
 
-def pblock_workspace_bytes(cfg: PbConfig, backward: bool) -> int:
-    return load_library().pblock_workspace_bytes(ctypes.byref(cfg), int(bool(backward)))
+def pblock_workspace_bytes(cfg: PbConfig, mode: int) -> int:
+    """mode: WS_FORWARD, WS_FORWARD_WITH_STASH or WS_BACKWARD."""
+    return load_library().pblock_workspace_bytes(ctypes.byref(cfg), int(mode))
 
 
 def pblock_forward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, y, saved=None, ws=None,
@@ -222,7 +225,9 @@ class ParallelBlock:
         u8 = torch.uint8
         self.y = torch.empty((cfg.batch, cfg.seq, H), dtype=act, device=device)
         self.saved = torch.empty(pblock_saved_bytes(cfg), dtype=u8, device=device)
-        self.ws = torch.empty(pblock_workspace_bytes(cfg, True), dtype=u8, device=device)
+        self.ws = torch.empty(pblock_workspace_bytes(cfg, WS_BACKWARD), dtype=u8, device=device)
+        nf = pblock_workspace_bytes(cfg, WS_FORWARD)
+        self.ws_fwd = torch.empty(nf, dtype=u8, device=device) if nf else None
         self.grads = dict(
             dx=torch.empty((cfg.batch, cfg.seq, H), dtype=act, device=device),
             dgamma=torch.empty(H, dtype=f32, device=device),
@@ -237,7 +242,7 @@ class ParallelBlock:
     def forward(self, stream=None):
         t = self.t
         pblock_forward(self.cfg, t["x"], t["gamma"], t["beta"], t["w_in"], t["b_in"], t["w_out"],
-                       t["b_out"], self.y, self.saved, None, stream)
+                       t["b_out"], self.y, self.saved, self.ws_fwd, stream)
         return self.y
 
     def backward(self, dy=None, stream=None):

@@ -51,7 +51,7 @@ def test_validate_rejects(field, value, status):
     assert pb.pblock_validate(c) == status
     assert pb.pblock_last_error() != ""
     assert pb.pblock_saved_bytes(c) == 0
-    assert pb.pblock_workspace_bytes(c, True) == 0
+    assert pb.pblock_workspace_bytes(c, pb.WS_BACKWARD) == 0
 
 
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
@@ -77,9 +77,34 @@ def test_saved_layout(name):
         o = align(o + z)
     assert pb.pblock_saved_offsets(c) == dict(zip(pb.SAVED_REGIONS, off))
     assert pb.pblock_saved_bytes(c) == o
-    assert pb.pblock_workspace_bytes(c, False) == o
+    split = pb.pblock_workspace_bytes(c, pb.WS_FORWARD)
+    assert split % 256 == 0
+    assert pb.pblock_workspace_bytes(c, pb.WS_FORWARD_WITH_STASH) == o + split
     # backward workspace holds at least dO, dZ and dh
-    assert pb.pblock_workspace_bytes(c, True) >= T * s.attn_width * e + T * s.n_in * e + 4 * T * s.hidden
+    assert pb.pblock_workspace_bytes(c, pb.WS_BACKWARD) >= T * s.attn_width * e + T * s.n_in * e + 4 * T * s.hidden
+    assert pb.pblock_workspace_bytes(c, 3) == 0
+
+
+def tail_split(M, N, K, bf16=True):
+    """The tail-split plan the library uses for an M x N x K GEMM: tiles of
+    256 x 256, 256 CUs; the last partial wave is split along K."""
+    tiles = -(-M // 256) * -(-N // 256)
+    n_full = tiles // 256 * 256
+    tail = tiles - n_full
+    if not bf16 or K % 64 or n_full == 0 or tail == 0:
+        return 0
+    splits = min(256 // tail, K // 64)
+    return tail * splits * 65536 if splits >= 2 else 0
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_split_workspace_sizes(name):
+    s = WORKLOADS[name]
+    c = pb.config_from_shape(s)
+    bf = s.dtype == "bf16"
+    T, H, n_in, k_out = s.tokens, s.hidden, s.n_in, s.k_out
+    fwd = max(tail_split(T, n_in, H, bf), tail_split(T, H, k_out, bf)) * 4
+    assert pb.pblock_workspace_bytes(c, pb.WS_FORWARD) == align(fwd)
 
 
 FAKE = 1 << 40  # a 16-byte aligned address; never dereferenced: every call below fails its checks
@@ -109,7 +134,7 @@ def test_forward_rejects_small_workspace():
     lib = pb.load_library()
     a = fwd_args(saved=None)
     c = good_cfg()
-    need = pb.pblock_workspace_bytes(c, False)
+    need = pb.pblock_saved_bytes(c)
     st = lib.pblock_forward(ctypes.byref(c), a["x"], a["ln_gamma"], a["ln_beta"], a["w_in"],
                             a["b_in"], a["w_out"], a["b_out"], a["y"], None, FAKE, need - 1, None)
     assert st == 3
@@ -119,9 +144,9 @@ def test_forward_rejects_small_workspace():
 def test_backward_rejects_small_workspace_and_nulls():
     lib = pb.load_library()
     c = good_cfg()
-    need = pb.pblock_workspace_bytes(c, True)
+    need = pb.pblock_workspace_bytes(c, pb.WS_BACKWARD)
     args = [FAKE] * 16
-    st = lib.pblock_backward(ctypes.byref(c), *args, FAKE, need - 1, None)
+    st = lib.pblock_backward(ctypes.byref(c), *args, FAKE, 1024, None)
     assert st == 3
     args[9] = None  # dx
     st = lib.pblock_backward(ctypes.byref(c), *args, FAKE, need, None)

@@ -40,6 +40,10 @@ CASES = [
     shape("bf16_seq1", batch=4, seq=1, hidden=64, heads=1, head_dim=64, ffn=64, window=8),
     shape("bf16_w_edge_tiles", batch=1, seq=512, hidden=256, heads=2, head_dim=128, ffn=256,
           window=64),
+    # in-projection: 3 x 86 = 258 output tiles, ragged in M and N: 256 whole
+    # tiles plus 2 tail tiles split 8 ways along K
+    shape("bf16_split_tail", batch=1, seq=520, hidden=512, heads=4, head_dim=128, ffn=20360,
+          window=100),
 ]
 
 
@@ -86,6 +90,30 @@ def test_forward_stash_matches_oracle(s):
         e = normwise(g, r)
         _say(f"      {name}: {e:.2e}")
         assert e <= tol, (name, e)
+
+
+def test_split_and_unsplit_gemms_agree():
+    """Without the optional partial-tile workspace the GEMMs run unsplit; both
+    runs must match the oracle, and each other to rounding."""
+    import torch
+    from paper_2402_15627_amd import pblock as pb
+    s = [c for c in CASES if c.name == "bf16_split_tail"][0]
+    _say(f"[gpu] split vs unsplit {s.name}")
+    inp = case(s, seed=4)
+    from tests.parity_util import to_device
+    blk = pb.ParallelBlock(pb.config_from_shape(s), to_device(s, inp))
+    assert blk.ws_fwd is not None  # this shape does split
+    y_split = blk.forward().float().cpu().numpy()
+    t = blk.t
+    y2 = torch.empty_like(blk.y)
+    pb.pblock_forward(blk.cfg, t["x"], t["gamma"], t["beta"], t["w_in"], t["b_in"], t["w_out"],
+                      t["b_out"], y2, blk.saved, None)
+    torch.cuda.synchronize()
+    y_unsplit = y2.float().cpu().numpy()
+    ref = run_oracle(s, inp)["y"].reshape(y_split.shape)
+    assert normwise(y_split, ref) <= 2e-2
+    assert normwise(y_unsplit, ref) <= 2e-2
+    assert normwise(y_split, y_unsplit) <= 1e-2
 
 
 def test_causal_locality_is_bitwise():
