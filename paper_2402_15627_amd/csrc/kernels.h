@@ -15,12 +15,13 @@ enum class Dt { BF16, F32 };
 void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta, void* h,
                        float* mean, float* rstd, int rows, int H, float eps, hipStream_t s);
 // dx = dy + rstd * (g - mean(g) - xhat * mean(g * xhat)), g = gamma * dh, per
-// row; per-block partial column sums of dh * xhat and dh go to part_dgamma and
-// part_dbeta [ln_backward_blocks(rows), H].
+// row; per-block partial column sums of dh * xhat, dh and dy go to
+// part_dgamma, part_dbeta and part_dy [ln_backward_blocks(rows), H].
 int ln_backward_blocks(int rows);
 void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
                         const void* gamma, const float* dh, const void* dy, void* dx,
-                        float* part_dgamma, float* part_dbeta, int rows, int H, hipStream_t s);
+                        float* part_dgamma, float* part_dbeta, float* part_dy, int rows, int H,
+                        hipStream_t s);
 
 // ------------------------------------------------------------ column sums
 // out[c] = sum over r of src[r * ld + c] for a [rows, cols] matrix (cols a

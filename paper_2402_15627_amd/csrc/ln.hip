@@ -85,44 +85,97 @@ __global__ __launch_bounds__(kLnThreads) void ln_fwd_kernel(const T* __restrict_
 }
 
 // Rows are strided over the grid; each workgroup keeps running column sums of
-// dh * xhat and dh in registers and writes them once as a partial row.
+// dh * xhat, dh and dy in registers and writes them once as a partial row
+// (dy's column sum is db_out, the output bias gradient).  The raw loads of
+// the next row are issued before the current row's reductions, so the
+// memory latency of one row hides behind the arithmetic of the previous.
+template <typename T>
+struct RowRaw;
+template <>
+struct RowRaw<bf16> {
+  u32x4 v;
+  PB_DEV void load(const bf16* p) { v = *reinterpret_cast<const u32x4*>(p); }
+  PB_DEV void get(float* o) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { o[2 * i] = lo_bf(v[i]); o[2 * i + 1] = hi_bf(v[i]); }
+  }
+};
+template <>
+struct RowRaw<float> {
+  f32x4 a, b;
+  PB_DEV void load(const float* p) {
+    a = *reinterpret_cast<const f32x4*>(p);
+    b = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+  PB_DEV void get(float* o) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { o[i] = a[i]; o[4 + i] = b[i]; }
+  }
+};
+
 template <typename T, int NV>
 __global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(
     const T* __restrict__ x, const float* __restrict__ mean, const float* __restrict__ rstd,
     const T* __restrict__ gamma, const float* __restrict__ dh, const T* __restrict__ dy,
-    T* __restrict__ dx, float* __restrict__ part_dg, float* __restrict__ part_db, int rows,
-    int H) {
+    T* __restrict__ dx, float* __restrict__ part_dg, float* __restrict__ part_db,
+    float* __restrict__ part_dy, int rows, int H) {
   __shared__ float red[2][kLnWaves];
-  float gm[NV][8], adg[NV][8], adb[NV][8];
+  float adg[NV][8], adb[NV][8], ady[NV][8];
+  RowRaw<T> graw[NV];  // gamma, kept packed to save registers
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int c = (threadIdx.x + j * kLnThreads) * 8;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) adg[j][e] = adb[j][e] = gm[j][e] = 0.f;
-    if (c < H) load8(gamma + c, gm[j]);
+    for (int e = 0; e < 8; ++e) adg[j][e] = adb[j][e] = ady[j][e] = 0.f;
+    if (c < H) graw[j].load(gamma + c);
   }
   const float inv_h = 1.0f / (float)H;
-  for (int row = blockIdx.x; row < rows; row += gridDim.x) {
+  RowRaw<T> nx[NV], ny[NV];
+  RowRaw<float> nd[NV];
+  auto fetch = [&](int row) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int c = (threadIdx.x + j * kLnThreads) * 8;
+      if (c < H) {
+        nx[j].load(x + (size_t)row * H + c);
+        nd[j].load(dh + (size_t)row * H + c);
+        ny[j].load(dy + (size_t)row * H + c);
+      }
+    }
+  };
+  int row = blockIdx.x;
+  if (row < rows) fetch(row);
+  for (; row < rows; row += gridDim.x) {
+    // the current row stays packed; values are unpacked where they are used
+    RowRaw<T> cx[NV], cy[NV];
+    RowRaw<float> cd[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      cx[j] = nx[j];
+      cd[j] = nd[j];
+      cy[j] = ny[j];
+    }
+    if (row + (int)gridDim.x < rows) fetch(row + gridDim.x);
     const float mu = mean[row], rs = rstd[row];
-    const T* xr = x + (size_t)row * H;
-    const float* dr = dh + (size_t)row * H;
-    float xh[NV][8], g[NV][8];
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
       const int c = (threadIdx.x + j * kLnThreads) * 8;
       if (c < H) {
-        float xv[8], d[8];
-        load8(xr + c, xv);
-        load8(dr + c, d);
+        float xv[8], d[8], r[8], gm[8];
+        cx[j].get(xv);
+        cd[j].get(d);
+        cy[j].get(r);
+        graw[j].get(gm);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          xh[j][e] = (xv[e] - mu) * rs;
-          adg[j][e] += d[e] * xh[j][e];
+          const float xh = (xv[e] - mu) * rs;
+          adg[j][e] += d[e] * xh;
           adb[j][e] += d[e];
-          g[j][e] = gm[j][e] * d[e];
-          s1 += g[j][e];
-          s2 += g[j][e] * xh[j][e];
+          ady[j][e] += r[e];
+          const float g = gm[e] * d[e];
+          s1 += g;
+          s2 += g * xh;
         }
       }
     }
@@ -142,16 +195,21 @@ __global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(
     }
     __syncthreads();
     const float m1 = t1 * inv_h, m2 = t2 * inv_h;
-    const T* dyr = dy + (size_t)row * H;
     T* dxr = dx + (size_t)row * H;
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
       const int c = (threadIdx.x + j * kLnThreads) * 8;
       if (c < H) {
-        float r[8], o[8];
-        load8(dyr + c, r);
+        float xv[8], d[8], r[8], gm[8], o[8];
+        cx[j].get(xv);
+        cd[j].get(d);
+        cy[j].get(r);
+        graw[j].get(gm);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = r[e] + rs * (g[j][e] - m1 - xh[j][e] * m2);
+        for (int e = 0; e < 8; ++e) {
+          const float xh = (xv[e] - mu) * rs;
+          o[e] = r[e] + rs * (gm[e] * d[e] - m1 - xh * m2);
+        }
         store8(dxr + c, o);
       }
     }
@@ -162,6 +220,7 @@ __global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(
     if (c < H) {
       store8(part_dg + (size_t)blockIdx.x * H + c, adg[j]);
       store8(part_db + (size_t)blockIdx.x * H + c, adb[j]);
+      store8(part_dy + (size_t)blockIdx.x * H + c, ady[j]);
     }
   }
 }
@@ -237,10 +296,11 @@ void ln_fwd_nv(const void* x, const void* gamma, const void* beta, void* h, floa
 
 template <typename T, int NV>
 void ln_bwd_nv(const void* x, const float* mean, const float* rstd, const void* gamma,
-               const float* dh, const void* dy, void* dx, float* pdg, float* pdb, int rows,
-               int H, hipStream_t s) {
+               const float* dh, const void* dy, void* dx, float* pdg, float* pdb, float* pdy,
+               int rows, int H, hipStream_t s) {
   ln_bwd_kernel<T, NV><<<ln_backward_blocks(rows), kLnThreads, 0, s>>>(
-      (const T*)x, mean, rstd, (const T*)gamma, dh, (const T*)dy, (T*)dx, pdg, pdb, rows, H);
+      (const T*)x, mean, rstd, (const T*)gamma, dh, (const T*)dy, (T*)dx, pdg, pdb, pdy, rows,
+      H);
 }
 
 template <typename T>
@@ -261,18 +321,18 @@ void ln_fwd_t(const void* x, const void* gamma, const void* beta, void* h, float
 
 template <typename T>
 void ln_bwd_t(const void* x, const float* mean, const float* rstd, const void* gamma,
-              const float* dh, const void* dy, void* dx, float* pdg, float* pdb, int rows, int H,
-              hipStream_t s) {
+              const float* dh, const void* dy, void* dx, float* pdg, float* pdb, float* pdy,
+              int rows, int H, hipStream_t s) {
   const int nv = (H + kLnThreads * 8 - 1) / (kLnThreads * 8);
   switch (nv) {
-    case 1: ln_bwd_nv<T, 1>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    case 2: ln_bwd_nv<T, 2>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    case 3: ln_bwd_nv<T, 3>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    case 4: ln_bwd_nv<T, 4>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    case 5: ln_bwd_nv<T, 5>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    case 6: ln_bwd_nv<T, 6>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    case 7: ln_bwd_nv<T, 7>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
-    default: ln_bwd_nv<T, 8>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, rows, H, s); break;
+    case 1: ln_bwd_nv<T, 1>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    case 2: ln_bwd_nv<T, 2>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    case 3: ln_bwd_nv<T, 3>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    case 4: ln_bwd_nv<T, 4>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    case 5: ln_bwd_nv<T, 5>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    case 6: ln_bwd_nv<T, 6>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    case 7: ln_bwd_nv<T, 7>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
+    default: ln_bwd_nv<T, 8>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
   }
 }
 
@@ -290,11 +350,14 @@ void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta
 
 void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
                         const void* gamma, const float* dh, const void* dy, void* dx,
-                        float* part_dgamma, float* part_dbeta, int rows, int H, hipStream_t s) {
+                        float* part_dgamma, float* part_dbeta, float* part_dy, int rows, int H,
+                        hipStream_t s) {
   if (dt == Dt::BF16)
-    ln_bwd_t<bf16>(x, mean, rstd, gamma, dh, dy, dx, part_dgamma, part_dbeta, rows, H, s);
+    ln_bwd_t<bf16>(x, mean, rstd, gamma, dh, dy, dx, part_dgamma, part_dbeta, part_dy, rows, H,
+                   s);
   else
-    ln_bwd_t<float>(x, mean, rstd, gamma, dh, dy, dx, part_dgamma, part_dbeta, rows, H, s);
+    ln_bwd_t<float>(x, mean, rstd, gamma, dh, dy, dx, part_dgamma, part_dbeta, part_dy, rows,
+                    H, s);
 }
 
 size_t colsum_partial_floats(int rows, int cols) {

@@ -127,7 +127,7 @@ size_t split_floats_bwd(const Dims& d, pb::Dt dt) {
 }
 
 struct BwdLayout {
-  size_t d_o, dz, dh, delta, pdg, pdb, part, split, base, total;
+  size_t d_o, dz, dh, delta, pdg, pdb, pdy, part, split, base, total;
 };
 BwdLayout bwd_layout(const Dims& d) {
   BwdLayout L;
@@ -144,6 +144,7 @@ BwdLayout bwd_layout(const Dims& d) {
   L.delta = take((size_t)(d.B * d.heads * d.S) * 4);
   L.pdg = take((size_t)nblk * d.H * 4);
   L.pdb = take((size_t)nblk * d.H * 4);
+  L.pdy = take((size_t)nblk * d.H * 4);
   size_t part = pb::colsum_partial_floats((int)d.T, (int)d.H);
   size_t p2 = pb::colsum_partial_floats((int)d.T, (int)d.N_in);
   size_t p3 = pb::colsum_partial_floats(nblk, (int)d.H);
@@ -380,6 +381,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   float* delta = (float*)(wb + W.delta);
   float* pdg = (float*)(wb + W.pdg);
   float* pdb = (float*)(wb + W.pdb);
+  float* pdy = (float*)(wb + W.pdy);
   float* part = (float*)(wb + W.part);
   float* split_ws = (float*)(wb + W.split);
   const size_t split_f = ws_bytes >= W.total ? (W.total - W.split) / 4 : 0;
@@ -412,10 +414,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
                     split_ws, split_f, stream);
   }
-  {
-    StepScope sc(PB_STEP_DB_OUT, stream);
-    pb::launch_colsum(dt, dy, H, T, H, part, db_out, stream);
-  }
+
   // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
   {
     StepScope sc(PB_STEP_ATTN_BWD, stream);
@@ -448,10 +447,15 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
   {
     StepScope sc(PB_STEP_LN_BWD, stream);
-    pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, dy, dx, pdg, pdb, T, H, stream);
+    pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, dy, dx, pdg, pdb, pdy, T, H, stream);
     const int nblk = pb::ln_backward_blocks(T);
     pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
     pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
+  }
+  {
+    // db_out = sum over tokens of dy, from the LN backward's partial sums
+    StepScope sc(PB_STEP_DB_OUT, stream);
+    pb::launch_colsum_f32(pdy, H, pb::ln_backward_blocks(T), H, part, db_out, stream);
   }
   return finish_launches();
 }
