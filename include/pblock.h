@@ -156,17 +156,31 @@ pb_status pblock_backward(const pb_config* cfg, const void* x,
  * q, k, v: element (b, s, head, e) at ptr[(b*seq + s)*ld + head*head_dim + e],
  * ld in elements (>= heads*head_dim, multiple of 8).  o uses ld_o the same
  * way.  lse [batch, heads, seq] fp32 as in the stash.  Reads cfg->batch, seq,
- * heads, head_dim, window and dtype only.  No workspace. */
+ * heads, head_dim, window and dtype only.
+ *
+ * Workspace (pblock_swattn_workspace_bytes, by mode):
+ *   PB_ATTN_WS_FORWARD      optional space for the forward: when batch*heads
+ *                           is too small to fill the GPU, the key range of
+ *                           each query block is split over several
+ *                           workgroups whose fp32 partial results are merged
+ *                           afterwards.  ws may be NULL (or smaller), which
+ *                           runs unsplit; 0 means no split is planned.
+ *   PB_ATTN_WS_BACKWARD_MIN bytes the backward requires (one fp32 softmax row
+ *                           term per query).
+ *   PB_ATTN_WS_BACKWARD     the same plus the split backward's partials; any
+ *                           size from _MIN up works, below this one unsplit.
+ * Results of the split and unsplit runs agree to fp32 rounding; each is
+ * deterministic (fixed merge order, no atomics). */
+enum { PB_ATTN_WS_FORWARD = 0, PB_ATTN_WS_BACKWARD_MIN = 1, PB_ATTN_WS_BACKWARD = 2 };
+size_t pblock_swattn_workspace_bytes(const pb_config* cfg, int mode);
 pb_status pblock_swattn_forward(const pb_config* cfg, const void* q,
                                 const void* k, const void* v, int ld_qkv,
-                                void* o, int ld_o, float* lse,
-                                hipStream_t stream);
+                                void* o, int ld_o, float* lse, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
 
 /* Gradient of pblock_swattn_forward: given q, k, v, o (ld_o), lse and the
- * output gradient d_o (ld_do), writes dq, dk, dv (ld_dqkv).  ws must hold
- * pblock_swattn_workspace_bytes(cfg) bytes (one fp32 softmax row term per
- * query).  Deterministic: no atomics. */
-size_t pblock_swattn_workspace_bytes(const pb_config* cfg);
+ * output gradient d_o (ld_do), writes dq, dk, dv (ld_dqkv).  ws: see above
+ * (at least PB_ATTN_WS_BACKWARD_MIN bytes, else PB_ERR_WORKSPACE). */
 pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
                                  const void* k, const void* v, int ld_qkv,
                                  const void* o, int ld_o, const void* d_o,

@@ -21,6 +21,8 @@
 // accumulation: results are deterministic.
 //
 // fp32 kernels: one thread per query (or key), plain loops; parity path.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -30,12 +32,31 @@ namespace {
 constexpr float kNegInf = -__builtin_huge_valf();
 
 // Waves per workgroup and tile length (tokens per LDS tile):
-//   forward and dQ: 32 NW queries per workgroup, key tiles of kTL
-//   dK/dV         : 32 NW keys per workgroup, query tiles of kTLdkv
-constexpr int NW = 2;
-constexpr int kThreads = 64 * NW;
+//   forward and dQ: 32 kWavesQ queries per workgroup, key tiles of kTL
+//   dK/dV         : 32 kWavesK keys per workgroup, query tiles of kTLdkv
+// Four forward / dQ waves share each K/V tile, which with two workgroups per
+// CU (64 KB of LDS each) keeps two waves on every SIMD, so one wave's
+// softmax arithmetic overlaps another's matrix instructions.
+constexpr int kWavesQ = 4;
+constexpr int kWavesK = 2;
 constexpr int kTL = 64;      // forward and dQ key tiles
 constexpr int kTLdkv = 32;   // dK/dV query tiles (keeps its registers and LDS in budget)
+constexpr int kBlockQ = 32 * kWavesQ;  // queries per forward / dQ workgroup
+constexpr int kBlockK = 32 * kWavesK;  // keys per dK/dV workgroup
+constexpr int kUnsplit = 1 << 30;
+
+// Key tiles (of kTL) that the query block q0 .. q0 + kBlockQ - 1 visits.
+__host__ __device__ inline int qblock_tiles(int q0, int S, int W) {
+  const int q_last = q0 + kBlockQ - 1 < S - 1 ? q0 + kBlockQ - 1 : S - 1;
+  const int lo = q0 - W + 1 > 0 ? q0 - W + 1 : 0;
+  return (q_last - (lo / kTL) * kTL) / kTL + 1;
+}
+// Query tiles (of kTLdkv) that the key block k0 .. k0 + kBlockK - 1 visits.
+__host__ __device__ inline int kblock_tiles(int k0, int S, int W) {
+  const int k_last = k0 + kBlockK - 1 < S - 1 ? k0 + kBlockK - 1 : S - 1;
+  const int q_end = k_last + W - 1 < S - 1 ? k_last + W - 1 : S - 1;
+  return (q_end - k0) / kTLdkv + 1;
+}
 
 PB_DEV float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
 
@@ -68,12 +89,13 @@ PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" :
 // [rows_valid, ld] token-major matrix, by LDS-DMA (each lane's 16 bytes land
 // at the piece's LDS base + 16 * lane).  Rows past rows_valid are read from
 // the last valid row: finite values that the window mask always zeroes.
-template <int D, int TL>
+template <int D, int TL, int NW>
 PB_DEV void dma_tile(const bf16* __restrict__ base, int ld, int row0, int rows_valid,
                      uint32_t lds_tile, int wave, int lane) {
   constexpr int RB = 2 * D;
   constexpr int BYTES = TL * RB;
   constexpr int PER_WAVE = BYTES / NW;
+  static_assert(PER_WAVE % 1024 == 0, "each wave moves whole 1 KB pieces");
 #pragma unroll
   for (int i = 0; i < PER_WAVE / 1024; ++i) {
     const int piece = wave * PER_WAVE + i * 1024;
@@ -135,15 +157,16 @@ PB_DEV bf16x8 load_row_frag(const bf16* p, bool ok) {
 }
 
 // ============================================================== forward
-// Workgroup: 32 NW queries of one (batch row, head); wave w owns queries
+// Workgroup: 32 kWavesQ queries of one (batch row, head); wave w owns queries
 // q0 + 32 w .. +31, lane l query q0 + 32 w + (l & 31).  Per key tile:
 // S^T = K Q^T (keys x queries), online softmax per lane, O^T += V^T P^T.
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_fwd_bf16(
+__global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2))) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
-    bf16* __restrict__ O, int ld_o, float* __restrict__ lse, int S, int H, int W, float scale) {
+    bf16* __restrict__ O, int ld_o, float* __restrict__ lse, int S, int H, int W, float scale,
+    int cs, int nc, float* __restrict__ po, float* __restrict__ plse) {
   constexpr int TL = kTL;
-  constexpr int NB = 32 * NW;
+  constexpr int NB = kBlockQ;
   constexpr int TB = TL * 2 * D;  // bytes per tile
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
@@ -151,7 +174,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   auto v_off = [&](int s) { return (2 * s + 1) * TB; };
 
   const int nqb = (S + NB - 1) / NB;
-  const int q0 = (nqb - 1 - (int)blockIdx.x) * NB;  // longest rows first
+  const int chunk = (int)blockIdx.x % nc;
+  const int q0 = (nqb - 1 - (int)blockIdx.x / nc) * NB;  // longest rows first
+  const int ntot = qblock_tiles(q0, S, W);
+  const int t_begin = chunk * cs;
+  if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
+  const int t_end = min(ntot, t_begin + cs);
+  const bool split = ntot > cs;
   const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
@@ -173,22 +202,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) o[i] = zero16();
 
-  const int q_last = min(q0 + NB - 1, S - 1);
   const int kv_begin = (max(0, q0 - W + 1) / TL) * TL;
-  const int ntiles = (q_last - kv_begin) / TL + 1;
   const int w_lo = qw0 - W + 1, w_hi = min(qw0 + 31, S - 1);
 
-  dma_tile<D, TL>(kb, ld, kv_begin, S, lds0 + k_off(0), wave, lane);
-  dma_tile<D, TL>(vb, ld, kv_begin, S, lds0 + v_off(0), wave, lane);
+  dma_tile<D, TL, kWavesQ>(kb, ld, kv_begin + t_begin * TL, S, lds0 + k_off(0), wave, lane);
+  dma_tile<D, TL, kWavesQ>(vb, ld, kv_begin + t_begin * TL, S, lds0 + v_off(0), wave, lane);
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
+  for (int t = t_begin; t < t_end; ++t) {
+    const int cur = (t - t_begin) & 1;
     const int kv0 = kv_begin + t * TL;
     wait_dma_all();
     block_barrier();
-    if (t + 1 < ntiles) {
-      dma_tile<D, TL>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
-      dma_tile<D, TL>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
+    if (t + 1 < t_end) {
+      dma_tile<D, TL, kWavesQ>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
+      dma_tile<D, TL, kWavesQ>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
     }
     if (qw0 < S && kv0 <= w_hi && kv0 + TL - 1 >= w_lo) {
       const unsigned char* kt = smem + k_off(cur);
@@ -248,19 +275,105 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (q < S) {
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-    bf16* orow = O + (tok0 + q) * ld_o + head * D;
+    const float m_use = m_run == kNegInf ? 0.f : m_run;
+    const size_t row = ((size_t)b * H + head) * S + q;
+    if (!split) {
+      bf16* orow = O + (tok0 + q) * ld_o + head * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float v[4] = {o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
-                      o[db][4 * j + 3] * inv};
-        store4(orow + 32 * db + 8 * j + 4 * fh, v);
-      }
-    if (fh == 0) {
-      const float m_use = m_run == kNegInf ? 0.f : m_run;
-      lse[((size_t)b * H + head) * S + q] = (m_use + log2f(l_tot)) * kLn2;
+        for (int j = 0; j < 4; ++j) {
+          float v[4] = {o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
+                        o[db][4 * j + 3] * inv};
+          store4(orow + 32 * db + 8 * j + 4 * fh, v);
+        }
+      if (fh == 0) lse[row] = (m_use + log2f(l_tot)) * kLn2;
+    } else {
+      // this chunk's normalised output and its base-2 log-sum-exp (-inf when
+      // none of the chunk's keys is visible to the query)
+      const size_t bhs = (size_t)gridDim.z * H * S;
+      float* prow = po + ((size_t)chunk * bhs + row) * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(prow + 32 * db + 8 * j + 4 * fh) =
+              f32x4{o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
+                    o[db][4 * j + 3] * inv};
+      if (fh == 0) plse[(size_t)chunk * bhs + row] = l_tot > 0.f ? m_use + log2f(l_tot) : kNegInf;
     }
+  }
+}
+
+// Merge of a split forward: per row, the chunks' normalised outputs weighted
+// by 2^(lse_c - lse), lse = log2 sum_c 2^lse_c.  Rows of unsplit blocks are
+// left alone (their workgroup wrote the result).  Thread: one row, 8 features.
+template <int D>
+__global__ __launch_bounds__(256) void attn_fwd_combine(const float* __restrict__ po,
+                                                        const float* __restrict__ plse, int cs,
+                                                        bf16* __restrict__ O, int ld_o,
+                                                        float* __restrict__ lse, int B, int S,
+                                                        int H, int W) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t bhs = (size_t)B * H * S;
+  const int g = (int)(idx % (D / 8));
+  const size_t row = idx / (D / 8);
+  if (row >= bhs) return;
+  const int t = (int)(row % S);
+  const int bh = (int)(row / S), head = bh % H, b = bh / H;
+  const int ntot = qblock_tiles((t / kBlockQ) * kBlockQ, S, W);
+  if (ntot <= cs) return;
+  const int nch = (ntot + cs - 1) / cs;
+  float m = kNegInf;
+  for (int c = 0; c < nch; ++c) m = fmaxf(m, plse[(size_t)c * bhs + row]);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, l = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float w = exp2_hw(plse[(size_t)c * bhs + row] - m);
+    float v[8];
+    load8(po + ((size_t)c * bhs + row) * D + 8 * g, v);
+    l += w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = fmaf(w, v[e], acc[e]);
+  }
+  const float inv = 1.0f / l;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] *= inv;
+  store8(O + ((size_t)b * S + t) * ld_o + head * D + 8 * g, acc);
+  if (g == 0) lse[row] = (m + log2f(l)) * kLn2;
+}
+
+// Merge of a split dQ or dK/dV: the chunks' fp32 partial sums added in chunk
+// order (KEYS: rows are key blocks, else query blocks).  p2 / o2 may be NULL.
+template <int D, bool KEYS>
+__global__ __launch_bounds__(256) void attn_sum_combine(const float* __restrict__ p1,
+                                                        const float* __restrict__ p2, int cs,
+                                                        bf16* __restrict__ o1,
+                                                        bf16* __restrict__ o2, int ld, int B,
+                                                        int S, int H, int W) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t bhs = (size_t)B * H * S;
+  const int g = (int)(idx % (D / 8));
+  const size_t row = idx / (D / 8);
+  if (row >= bhs) return;
+  const int t = (int)(row % S);
+  const int bh = (int)(row / S), head = bh % H, b = bh / H;
+  const int nb = KEYS ? kBlockK : kBlockQ;
+  const int ntot = KEYS ? kblock_tiles((t / nb) * nb, S, W) : qblock_tiles((t / nb) * nb, S, W);
+  if (ntot <= cs) return;
+  const int nch = (ntot + cs - 1) / cs;
+  const size_t out = ((size_t)b * S + t) * ld + head * D + 8 * g;
+  for (int which = 0; which < 2; ++which) {
+    const float* p = which ? p2 : p1;
+    bf16* o = which ? o2 : o1;
+    if (!p) break;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < nch; ++c) {
+      float v[8];
+      load8(p + ((size_t)c * bhs + row) * D + 8 * g, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += v[e];
+    }
+    store8(o + out, acc);
   }
 }
 
@@ -288,18 +401,19 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(const T* __restrict__ O
 }
 
 // ====================================================== backward: dK, dV
-// Workgroup: 32 NW keys; wave w owns keys k0 + 32 w .. +31 (lane: one key).
+// Workgroup: 32 kWavesK keys; wave w owns keys k0 + 32 w .. +31 (lane: one key).
 // Per query tile: S = Q K^T and dP = dO V^T (queries x keys), P and
 // dS = P (dP - delta), then dV^T += dO^T P and dK^T += Q^T dS, the
 // transposed operands read from the natural Q and dO tiles.
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
+__global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV, int ld_d,
-    int S, int H, int W, float scale) {
+    int S, int H, int W, float scale, int cs, int nc, float* __restrict__ pdk,
+    float* __restrict__ pdv) {
   constexpr int TL = kTLdkv;
-  constexpr int NB = 32 * NW;
+  constexpr int NB = kBlockK;
   constexpr int TB = TL * 2 * D;
   constexpr int STAGE = 2 * TB + 2 * TL * 4;  // Q, dO, then lse*log2e and delta
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
@@ -308,7 +422,13 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
   auto g_off = [&](int s) { return s * STAGE + TB; };
   auto l_off = [&](int s) { return s * STAGE + 2 * TB; };
 
-  const int k0 = (int)blockIdx.x * NB;
+  const int chunk = (int)blockIdx.x % nc;
+  const int k0 = ((int)blockIdx.x / nc) * NB;
+  const int ntot = kblock_tiles(k0, S, W);
+  const int t_begin = chunk * cs;
+  if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
+  const int t_end = min(ntot, t_begin + cs);
+  const bool split = ntot > cs;
   const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
@@ -334,30 +454,27 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
   for (int i = 0; i < D / 32; ++i) dk[i] = dv[i] = zero16();
 
   const float c2 = scale * kLog2e;
-  const int k_last = min(k0 + NB - 1, S - 1);
-  const int q_end = min(S - 1, k_last + W - 1);
-  const int ntiles = (q_end - k0) / TL + 1;
   const int w_lo = kw0, w_hi = min(S - 1, kw0 + 31 + W - 1);  // queries this wave needs
 
   float rl = 0.f;
   auto issue_stage = [&](int qs, int s) {
-    dma_tile<D, TL>(qb, ld, qs, S, lds0 + q_off(s), wave, lane);
-    dma_tile<D, TL>(gb, ld_o, qs, S, lds0 + g_off(s), wave, lane);
+    dma_tile<D, TL, kWavesK>(qb, ld, qs, S, lds0 + q_off(s), wave, lane);
+    dma_tile<D, TL, kWavesK>(gb, ld_o, qs, S, lds0 + g_off(s), wave, lane);
     if (tid < TL) rl = qs + tid < S ? lseb[qs + tid] * kLog2e : __builtin_huge_valf();
     else if (tid < 2 * TL) rl = qs + tid - TL < S ? delb[qs + tid - TL] : 0.f;
   };
   auto finish_stage = [&](int s) {
     if (tid < 2 * TL) ((float*)(smem + l_off(s)))[tid] = rl;
   };
-  issue_stage(k0, 0);
+  issue_stage(k0 + t_begin * TL, 0);
   finish_stage(0);
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
+  for (int t = t_begin; t < t_end; ++t) {
+    const int cur = (t - t_begin) & 1;
     const int qs = k0 + t * TL;
     wait_dma_all();
     block_barrier();
-    if (t + 1 < ntiles) issue_stage(qs + TL, cur ^ 1);
+    if (t + 1 < t_end) issue_stage(qs + TL, cur ^ 1);
     if (kw0 < S && qs <= w_hi && qs + TL - 1 >= w_lo) {
       const unsigned char* qt = smem + q_off(cur);
       const unsigned char* gt = smem + g_off(cur);
@@ -407,10 +524,24 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
               frag_tr<D>(qt, 32 * db + fr, s2, fh, lane), probs_frag(ds, s2), dk[db], 0, 0, 0);
         }
     }
-    if (t + 1 < ntiles) finish_stage(cur ^ 1);
+    if (t + 1 < t_end) finish_stage(cur ^ 1);
   }
 
-  if (key < S) {
+  if (key < S && split) {
+    const size_t bhs = (size_t)gridDim.z * H * S;
+    const size_t prow = ((size_t)chunk * bhs + ((size_t)b * H + head) * S + key) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int e = 32 * db + 8 * j + 4 * fh;
+        *reinterpret_cast<f32x4*>(pdk + prow + e) =
+            f32x4{dk[db][4 * j] * scale, dk[db][4 * j + 1] * scale, dk[db][4 * j + 2] * scale,
+                  dk[db][4 * j + 3] * scale};
+        *reinterpret_cast<f32x4*>(pdv + prow + e) =
+            f32x4{dv[db][4 * j], dv[db][4 * j + 1], dv[db][4 * j + 2], dv[db][4 * j + 3]};
+      }
+  } else if (key < S) {
     bf16* dkr = dK + (tok0 + key) * ld_d + head * D;
     bf16* dvr = dV + (tok0 + key) * ld_d + head * D;
 #pragma unroll
@@ -430,17 +561,17 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
 }
 
 // ============================================================ backward: dQ
-// Workgroup: 32 NW queries; per key tile: S^T = K Q^T and dP^T = V dO^T,
+// Workgroup: 32 kWavesQ queries; per key tile: S^T = K Q^T and dP^T = V dO^T,
 // dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T (K^T read from the natural K
 // tile).
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_dq_bf16(
+__global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2))) void attn_dq_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dQ, int ld_d, int S, int H, int W,
-    float scale) {
+    float scale, int cs, int nc, float* __restrict__ pdq) {
   constexpr int TL = kTL;
-  constexpr int NB = 32 * NW;
+  constexpr int NB = kBlockQ;
   constexpr int TB = TL * 2 * D;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
@@ -448,7 +579,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   auto v_off = [&](int s) { return (2 * s + 1) * TB; };
 
   const int nqb = (S + NB - 1) / NB;
-  const int q0 = (nqb - 1 - (int)blockIdx.x) * NB;
+  const int chunk = (int)blockIdx.x % nc;
+  const int q0 = (nqb - 1 - (int)blockIdx.x / nc) * NB;
+  const int ntot = qblock_tiles(q0, S, W);
+  const int t_begin = chunk * cs;
+  if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
+  const int t_end = min(ntot, t_begin + cs);
+  const bool split = ntot > cs;
   const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
@@ -476,22 +613,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) dq[i] = zero16();
 
-  const int q_last = min(q0 + NB - 1, S - 1);
   const int kv_begin = (max(0, q0 - W + 1) / TL) * TL;
-  const int ntiles = (q_last - kv_begin) / TL + 1;
   const int w_lo = qw0 - W + 1, w_hi = min(qw0 + 31, S - 1);
 
-  dma_tile<D, TL>(kb, ld, kv_begin, S, lds0 + k_off(0), wave, lane);
-  dma_tile<D, TL>(vb, ld, kv_begin, S, lds0 + v_off(0), wave, lane);
+  dma_tile<D, TL, kWavesQ>(kb, ld, kv_begin + t_begin * TL, S, lds0 + k_off(0), wave, lane);
+  dma_tile<D, TL, kWavesQ>(vb, ld, kv_begin + t_begin * TL, S, lds0 + v_off(0), wave, lane);
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
+  for (int t = t_begin; t < t_end; ++t) {
+    const int cur = (t - t_begin) & 1;
     const int kv0 = kv_begin + t * TL;
     wait_dma_all();
     block_barrier();
-    if (t + 1 < ntiles) {
-      dma_tile<D, TL>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
-      dma_tile<D, TL>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
+    if (t + 1 < t_end) {
+      dma_tile<D, TL, kWavesQ>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
+      dma_tile<D, TL, kWavesQ>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
     }
     if (qw0 < S && kv0 <= w_hi && kv0 + TL - 1 >= w_lo) {
       const unsigned char* kt = smem + k_off(cur);
@@ -532,7 +667,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
   }
 
-  if (q < S) {
+  if (q < S && split) {
+    const size_t bhs = (size_t)gridDim.z * H * S;
+    float* prow = pdq + ((size_t)chunk * bhs + row_off + q) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<f32x4*>(prow + 32 * db + 8 * j + 4 * fh) =
+            f32x4{dq[db][4 * j] * scale, dq[db][4 * j + 1] * scale, dq[db][4 * j + 2] * scale,
+                  dq[db][4 * j + 3] * scale};
+  } else if (q < S) {
     bf16* dqr = dQ + (tok0 + q) * ld_d + head * D;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -659,15 +804,33 @@ size_t dkdv_lds() { return 2 * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4); }
 template <int D>
 size_t dq_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 
+size_t part_floats(const AttnShape& a, int n) {
+  return n > 1 ? (size_t)n * a.batch * a.heads * a.seq * a.head_dim : 0;
+}
+size_t lse_floats(const AttnShape& a, int n) {
+  return n > 1 ? (size_t)n * a.batch * a.heads * a.seq : 0;
+}
+size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
+unsigned combine_grid(const AttnShape& a) {
+  return (unsigned)(((size_t)a.batch * a.heads * a.seq * (a.head_dim / 8) + 255) / 256);
+}
+
 template <int D>
 void fwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v, int ld,
-           void* o, int ld_o, float* lse, hipStream_t s) {
+           void* o, int ld_o, float* lse, void* part, size_t part_bytes, hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)D);
   if (dt == Dt::BF16) {
-    dim3 g((a.seq + 32 * NW - 1) / (32 * NW), a.heads, a.batch);
-    attn_fwd_bf16<D><<<g, kThreads, fwd_lds<D>(), s>>>(
+    AttnSplit p = attn_split_plan(dt, a);
+    if (!part || part_bytes < attn_fwd_partial_bytes(a, p)) p.fwd_chunk = kUnsplit, p.fwd_n = 1;
+    float* po = (float*)part;
+    float* plse = po ? (float*)((char*)part + round256(part_floats(a, p.fwd_n) * 4)) : nullptr;
+    dim3 g((a.seq + kBlockQ - 1) / kBlockQ * p.fwd_n, a.heads, a.batch);
+    attn_fwd_bf16<D><<<g, 64 * kWavesQ, fwd_lds<D>(), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (bf16*)o, ld_o, lse, a.seq, a.heads,
-        a.window, scale);
+        a.window, scale, p.fwd_chunk, p.fwd_n, po, plse);
+    if (p.fwd_n > 1)
+      attn_fwd_combine<D><<<combine_grid(a), 256, 0, s>>>(po, plse, p.fwd_chunk, (bf16*)o, ld_o,
+                                                          lse, a.batch, a.seq, a.heads, a.window);
   } else {
     dim3 g((a.seq + 63) / 64, a.heads, a.batch);
     attn_fwd_f32<D><<<g, 64, 0, s>>>((const float*)q, (const float*)k, (const float*)v, ld,
@@ -678,19 +841,36 @@ void fwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
 template <int D>
 void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v, int ld,
            const void* o, int ld_o, const void* d_o, int ld_do, const float* lse, float* delta,
-           void* dq, void* dk, void* dv, int ld_d, hipStream_t s) {
+           void* dq, void* dk, void* dv, int ld_d, void* part, size_t part_bytes, hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)D);
   const int nrows = a.batch * a.seq * a.heads;
   if (dt == Dt::BF16) {
     attn_delta_kernel<bf16><<<(nrows + 255) / 256, 256, 0, s>>>(
         (const bf16*)o, ld_o, (const bf16*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
-    dim3 g((a.seq + 32 * NW - 1) / (32 * NW), a.heads, a.batch);
-    attn_dkdv_bf16<D><<<g, kThreads, dkdv_lds<D>(), s>>>(
+    AttnSplit p = attn_split_plan(dt, a);
+    if (!part || part_bytes < attn_bwd_partial_bytes(a, p)) {
+      p.fwd_chunk = p.kv_chunk = kUnsplit;
+      p.fwd_n = p.kv_n = 1;
+    }
+    // dK/dV partials, then (after their merge) dQ partials, in the same space
+    float* pdk = (float*)part;
+    float* pdv = pdk ? pdk + part_floats(a, p.kv_n) : nullptr;
+    dim3 gk((a.seq + kBlockK - 1) / kBlockK * p.kv_n, a.heads, a.batch);
+    attn_dkdv_bf16<D><<<gk, 64 * kWavesK, dkdv_lds<D>(), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (const bf16*)d_o, ld_do, lse, delta,
-        (bf16*)dk, (bf16*)dv, ld_d, a.seq, a.heads, a.window, scale);
-    attn_dq_bf16<D><<<g, kThreads, dq_lds<D>(), s>>>(
+        (bf16*)dk, (bf16*)dv, ld_d, a.seq, a.heads, a.window, scale, p.kv_chunk, p.kv_n, pdk,
+        pdv);
+    if (p.kv_n > 1)
+      attn_sum_combine<D, true><<<combine_grid(a), 256, 0, s>>>(
+          pdk, pdv, p.kv_chunk, (bf16*)dk, (bf16*)dv, ld_d, a.batch, a.seq, a.heads, a.window);
+    dim3 gq((a.seq + kBlockQ - 1) / kBlockQ * p.fwd_n, a.heads, a.batch);
+    attn_dq_bf16<D><<<gq, 64 * kWavesQ, dq_lds<D>(), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (const bf16*)d_o, ld_do, lse, delta,
-        (bf16*)dq, ld_d, a.seq, a.heads, a.window, scale);
+        (bf16*)dq, ld_d, a.seq, a.heads, a.window, scale, p.fwd_chunk, p.fwd_n, (float*)part);
+    if (p.fwd_n > 1)
+      attn_sum_combine<D, false><<<combine_grid(a), 256, 0, s>>>(
+          (const float*)part, nullptr, p.fwd_chunk, (bf16*)dq, nullptr, ld_d, a.batch, a.seq,
+          a.heads, a.window);
   } else {
     attn_delta_kernel<float><<<(nrows + 255) / 256, 256, 0, s>>>(
         (const float*)o, ld_o, (const float*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
@@ -706,20 +886,60 @@ void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
 
 }  // namespace
 
+// Split only when a kernel's grid has fewer than kSplitBelow waves; then aim
+// for about kSplitTarget waves, with chunks of at least two tiles.
+constexpr long long kSplitBelow = 2048;
+constexpr long long kSplitTarget = 3072;
+
+AttnSplit attn_split_plan(Dt dt, const AttnShape& a) {
+  AttnSplit p{kUnsplit, 1, kUnsplit, 1};
+  if (dt != Dt::BF16) return p;
+  auto choose = [&](int block, int waves, bool keys, int& chunk, int& n) {
+    const int nb = (a.seq + block - 1) / block;
+    const long long w = (long long)nb * a.heads * a.batch * waves;
+    if (w >= kSplitBelow) return;
+    int max_tiles = 1;
+    for (int i = 0; i < nb; ++i)
+      max_tiles = std::max(max_tiles, keys ? kblock_tiles(i * block, a.seq, a.window)
+                                           : qblock_tiles(i * block, a.seq, a.window));
+    const int want = (int)((kSplitTarget + w - 1) / w);
+    const int m = std::min(want, (max_tiles + 1) / 2);
+    if (m < 2) return;
+    chunk = (max_tiles + m - 1) / m;
+    n = (max_tiles + chunk - 1) / chunk;
+    if (n < 2) chunk = kUnsplit, n = 1;
+  };
+  choose(kBlockQ, kWavesQ, false, p.fwd_chunk, p.fwd_n);
+  choose(kBlockK, kWavesK, true, p.kv_chunk, p.kv_n);
+  return p;
+}
+
+size_t attn_fwd_partial_bytes(const AttnShape& a, const AttnSplit& p) {
+  if (p.fwd_n < 2) return 0;
+  return round256(part_floats(a, p.fwd_n) * 4) + round256(lse_floats(a, p.fwd_n) * 4);
+}
+
+size_t attn_bwd_partial_bytes(const AttnShape& a, const AttnSplit& p) {
+  return std::max(2 * part_floats(a, p.kv_n) * 4, part_floats(a, p.fwd_n) * 4);
+}
+
 void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
-                         int ld_qkv, void* o, int ld_o, float* lse, hipStream_t s) {
-  if (a.head_dim == 64) fwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, s);
-  else fwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, s);
+                         int ld_qkv, void* o, int ld_o, float* lse, void* part,
+                         size_t part_bytes, hipStream_t s) {
+  if (a.head_dim == 64) fwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, part, part_bytes, s);
+  else fwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, part, part_bytes, s);
 }
 
 void launch_attn_backward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
                           int ld_qkv, const void* o, int ld_o, const void* d_o, int ld_do,
                           const float* lse, float* delta, void* dq, void* dk, void* dv, int ld_d,
-                          hipStream_t s) {
+                          void* part, size_t part_bytes, hipStream_t s) {
   if (a.head_dim == 64)
-    bwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, s);
+    bwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
+              part_bytes, s);
   else
-    bwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, s);
+    bwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
+               part_bytes, s);
 }
 
 }  // namespace pb

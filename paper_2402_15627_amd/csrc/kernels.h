@@ -79,13 +79,35 @@ void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, 
 struct AttnShape {
   int batch, seq, heads, head_dim, window;
 };
+
+// Work split of the bf16 attention kernels.  Each workgroup owns a block of 64
+// queries (forward, dQ) or 64 keys (dK/dV) and walks tiles of the other axis.
+// When there are too few blocks to fill the chip, a block's tile range is cut
+// into chunks of at most *_chunk tiles handled by separate workgroups; those
+// write fp32 partial results that a combine kernel merges in chunk order, so
+// results stay deterministic.  *_n is the chunk count of the longest block
+// (1: unsplit).
+struct AttnSplit {
+  int fwd_chunk, fwd_n;  // forward and dQ: key tiles of 64
+  int kv_chunk, kv_n;    // dK/dV: query tiles of 32
+};
+AttnSplit attn_split_plan(Dt dt, const AttnShape& a);
+// Bytes of partial results the split forward / backward needs (0: unsplit).
+size_t attn_fwd_partial_bytes(const AttnShape& a, const AttnSplit& p);
+size_t attn_bwd_partial_bytes(const AttnShape& a, const AttnSplit& p);
+
+// O = softmax(Q K^T / sqrt(d), sliding-window causal mask) V per head; lse
+// [batch, heads, seq] is the natural-log row log-sum-exp.  part may be NULL;
+// the split plan is used only when part_bytes >= attn_fwd_partial_bytes.
 void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
-                         int ld_qkv, void* o, int ld_o, float* lse, hipStream_t s);
+                         int ld_qkv, void* o, int ld_o, float* lse, void* part,
+                         size_t part_bytes, hipStream_t s);
 // delta[b, head, t] = sum_e do * o (softmax row term of the backward pass).
-// o uses ld_o, d_o uses ld_do; delta holds batch*heads*seq floats.
+// o uses ld_o, d_o uses ld_do; delta holds batch*heads*seq floats.  part as
+// for the forward, against attn_bwd_partial_bytes.
 void launch_attn_backward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
                           int ld_qkv, const void* o, int ld_o, const void* d_o, int ld_do,
                           const float* lse, float* delta, void* dq, void* dk, void* dv, int ld_d,
-                          hipStream_t s);
+                          void* part, size_t part_bytes, hipStream_t s);
 
 }  // namespace pb

@@ -93,6 +93,18 @@ pb_status check_config(const pb_config* c) {
   return PB_OK;
 }
 
+pb::AttnShape attn_shape(const Dims& d) {
+  pb::AttnShape a;
+  a.batch = (int)d.B;
+  a.seq = (int)d.S;
+  a.heads = (int)d.heads;
+  a.head_dim = (int)d.d;
+  // a window of at least seq keys is full causal attention; clamping keeps
+  // the kernels' index arithmetic within int range
+  a.window = (int)(d.W < d.S ? d.W : d.S);
+  return a;
+}
+
 struct SavedLayout {
   size_t off[6];  // h, z, c, mean, rstd, lse
   size_t total;
@@ -111,19 +123,24 @@ SavedLayout saved_layout(const Dims& d) {
   return L;
 }
 
-// fp32 floats of tail-split partial tiles the forward / backward GEMMs use.
-size_t split_floats_fwd(const Dims& d, pb::Dt dt) {
+// Optional space for split work: the GEMMs' tail-split partial tiles and the
+// attention kernels' chunk partials.  They are never live at the same time,
+// so one region serves both.
+size_t split_bytes_fwd(const Dims& d, pb::Dt dt) {
   const int T = (int)d.T, H = (int)d.H, N_in = (int)d.N_in, K_out = (int)d.K_out;
-  return std::max(pb::gemm_split_floats(pb::gemm_split_plan(dt, T, N_in, H)),
-                  pb::gemm_split_floats(pb::gemm_split_plan(dt, T, H, K_out)));
+  size_t m = std::max(pb::gemm_split_floats(pb::gemm_split_plan(dt, T, N_in, H)),
+                      pb::gemm_split_floats(pb::gemm_split_plan(dt, T, H, K_out))) * 4;
+  const pb::AttnShape a = attn_shape(d);
+  return std::max(m, pb::attn_fwd_partial_bytes(a, pb::attn_split_plan(dt, a)));
 }
-size_t split_floats_bwd(const Dims& d, pb::Dt dt) {
+size_t split_bytes_bwd(const Dims& d, pb::Dt dt) {
   const int T = (int)d.T, H = (int)d.H, N_in = (int)d.N_in, K_out = (int)d.K_out;
   size_t m = pb::gemm_split_floats(pb::gemm_split_plan(dt, T, K_out, H));
   m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, H, K_out, T)));
   m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, T, H, N_in)));
   m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, N_in, H, T)));
-  return m;
+  const pb::AttnShape a = attn_shape(d);
+  return std::max(m * 4, pb::attn_bwd_partial_bytes(a, pb::attn_split_plan(dt, a)));
 }
 
 struct BwdLayout {
@@ -152,7 +169,7 @@ BwdLayout bwd_layout(const Dims& d) {
   if (p3 > part) part = p3;
   L.part = take(part * 4);
   L.base = o;  // required; the tail-split region after it is optional
-  L.split = take(split_floats_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32) * 4);
+  L.split = take(split_bytes_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32));
   L.total = o;
   return L;
 }
@@ -184,18 +201,6 @@ const void* at(const void* base, long long elems, size_t esz) {
 }
 void* at(void* base, long long elems, size_t esz) { return (char*)base + (size_t)elems * esz; }
 
-pb::AttnShape attn_shape(const Dims& d) {
-  pb::AttnShape a;
-  a.batch = (int)d.B;
-  a.seq = (int)d.S;
-  a.heads = (int)d.heads;
-  a.head_dim = (int)d.d;
-  // a window of at least seq keys is full causal attention; clamping keeps
-  // the kernels' index arithmetic within int range
-  a.window = (int)(d.W < d.S ? d.W : d.S);
-  return a;
-}
-
 pb_status check_attn_config(const pb_config* c) {
   if (!c) return fail(PB_ERR_INVALID_ARG, "cfg is NULL");
   if (c->dtype != PB_BF16 && c->dtype != PB_F32)
@@ -209,6 +214,10 @@ pb_status check_attn_config(const pb_config* c) {
   if ((long long)c->batch * c->seq * c->heads > kMaxInt)
     return fail(PB_ERR_UNSUPPORTED, "batch*seq*heads exceeds 32-bit indexing");
   return PB_OK;
+}
+
+size_t swattn_delta_bytes(const pb_config* c) {
+  return align256((size_t)c->batch * c->heads * c->seq * 4);
 }
 
 pb_status check_ld(int ld, const pb_config* c, const char* name) {
@@ -244,7 +253,7 @@ pb_status pblock_saved_offsets(const pb_config* cfg, size_t* offsets) {
 size_t pblock_workspace_bytes(const pb_config* cfg, int mode) {
   if (check_config(cfg) != PB_OK) return 0;
   const Dims d = dims_of(cfg);
-  const size_t split = align256(split_floats_fwd(d, dt_of(cfg)) * 4);
+  const size_t split = align256(split_bytes_fwd(d, dt_of(cfg)));
   switch (mode) {
     case PB_WS_FORWARD_WITH_STASH: return saved_layout(d).total + split;
     case PB_WS_BACKWARD: return bwd_layout(d).total;
@@ -320,7 +329,7 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   {
     StepScope sc(PB_STEP_ATTN_FWD, stream);
     pb::launch_attn_forward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
-                            lse, stream);
+                            lse, split_base, split_bytes, stream);
   }
   // F5: y = x + C W_out^T + b_out (both branches and the residual of Eq. 2)
   pb::EpiArgs e2;
@@ -420,7 +429,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     StepScope sc(PB_STEP_ATTN_BWD, stream);
     pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
                              K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
-                             N_in, stream);
+                             N_in, split_ws, split_f * 4, stream);
   }
   // B4: dh = dZ W_in (fp32)
   pb::EpiArgs e4;
@@ -462,7 +471,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
 
 pb_status pblock_swattn_forward(const pb_config* cfg, const void* q, const void* k,
                                 const void* v, int ld_qkv, void* o, int ld_o, float* lse,
-                                hipStream_t stream) {
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
   PB_CHECK(check_attn_config(cfg));
   PB_CHECK(check_ptr(q, "q"));
   PB_CHECK(check_ptr(k, "k"));
@@ -477,13 +486,28 @@ pb_status pblock_swattn_forward(const pb_config* cfg, const void* q, const void*
   a.heads = cfg->heads;
   a.head_dim = cfg->head_dim;
   a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
-  pb::launch_attn_forward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, lse, stream);
+  if (ws) PB_CHECK(check_ptr(ws, "ws"));
+  pb::launch_attn_forward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, lse, ws, ws ? ws_bytes : 0,
+                          stream);
   return finish_launches();
 }
 
-size_t pblock_swattn_workspace_bytes(const pb_config* cfg) {
+size_t pblock_swattn_workspace_bytes(const pb_config* cfg, int mode) {
   if (check_attn_config(cfg) != PB_OK) return 0;
-  return align256((size_t)cfg->batch * cfg->heads * cfg->seq * 4);
+  pb::AttnShape a;
+  a.batch = cfg->batch;
+  a.seq = cfg->seq;
+  a.heads = cfg->heads;
+  a.head_dim = cfg->head_dim;
+  a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
+  const pb::AttnSplit p = pb::attn_split_plan(dt_of(cfg), a);
+  switch (mode) {
+    case PB_ATTN_WS_FORWARD: return pb::attn_fwd_partial_bytes(a, p);
+    case PB_ATTN_WS_BACKWARD_MIN: return swattn_delta_bytes(cfg);
+    case PB_ATTN_WS_BACKWARD:
+      return swattn_delta_bytes(cfg) + align256(pb::attn_bwd_partial_bytes(a, p));
+    default: return 0;
+  }
 }
 
 pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void* k,
@@ -506,7 +530,7 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void
   PB_CHECK(check_ld(ld_o, cfg, "ld_o"));
   PB_CHECK(check_ld(ld_do, cfg, "ld_do"));
   PB_CHECK(check_ld(ld_dqkv, cfg, "ld_dqkv"));
-  const size_t need = pblock_swattn_workspace_bytes(cfg);
+  const size_t need = swattn_delta_bytes(cfg);
   if (ws_bytes < need) return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, need);
   pb::AttnShape a;
   a.batch = cfg->batch;
@@ -515,7 +539,7 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void
   a.head_dim = cfg->head_dim;
   a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
   pb::launch_attn_backward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, (float*)ws,
-                           dq, dk, dv, ld_dqkv, stream);
+                           dq, dk, dv, ld_dqkv, (char*)ws + need, ws_bytes - need, stream);
   return finish_launches();
 }
 

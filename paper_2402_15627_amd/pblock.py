@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_PKG, "libpblock.so")
 PB_BF16, PB_F32 = 0, 1
 # pblock_workspace_bytes modes
 WS_FORWARD_WITH_STASH, WS_BACKWARD, WS_FORWARD = 0, 1, 2
+# pblock_swattn_workspace_bytes modes
+ATTN_WS_FORWARD, ATTN_WS_BACKWARD_MIN, ATTN_WS_BACKWARD = 0, 1, 2
 STATUS = {0: "PB_OK", 1: "PB_ERR_INVALID_ARG", 2: "PB_ERR_UNSUPPORTED", 3: "PB_ERR_WORKSPACE",
           4: "PB_ERR_HIP"}
 SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
@@ -70,8 +72,8 @@ def load_library(path: str = LIB_PATH):
         "pblock_forward": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, c_size_t, P]),
         "pblock_backward": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P,
                                     c_size_t, P]),
-        "pblock_swattn_forward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, P]),
-        "pblock_swattn_workspace_bytes": (c_size_t, [cfgp]),
+        "pblock_swattn_forward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, P, c_size_t, P]),
+        "pblock_swattn_workspace_bytes": (c_size_t, [cfgp, c_int]),
         "pblock_swattn_backward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, c_int, P, P, P, P,
                                            c_int, P, c_size_t, P]),
         "pblock_set_step_events": (c_int, [P, P]),
@@ -162,14 +164,15 @@ def pblock_backward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, saved, 
         _stream(stream)))
 
 
-def pblock_swattn_forward(cfg, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
+def pblock_swattn_forward(cfg, q, k, v, ld_qkv, o, ld_o, lse, ws=None, stream=None):
     _check(load_library().pblock_swattn_forward(
-        ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(lse),
-        _stream(stream)))
+        ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(lse), _ptr(ws),
+        _nbytes(ws), _stream(stream)))
 
 
-def pblock_swattn_workspace_bytes(cfg) -> int:
-    return load_library().pblock_swattn_workspace_bytes(ctypes.byref(cfg))
+def pblock_swattn_workspace_bytes(cfg, mode: int) -> int:
+    """mode: ATTN_WS_FORWARD, ATTN_WS_BACKWARD_MIN or ATTN_WS_BACKWARD."""
+    return load_library().pblock_swattn_workspace_bytes(ctypes.byref(cfg), int(mode))
 
 
 def pblock_swattn_backward(cfg, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, dq, dk, dv, ld_dqkv,

@@ -157,9 +157,11 @@ def test_swattn_rejects_bad_leading_dimension():
     lib = pb.load_library()
     c = good_cfg()
     A = c.heads * c.head_dim
-    st = lib.pblock_swattn_forward(ctypes.byref(c), FAKE, FAKE, FAKE, A - 8, FAKE, A, FAKE, None)
+    st = lib.pblock_swattn_forward(ctypes.byref(c), FAKE, FAKE, FAKE, A - 8, FAKE, A, FAKE, None,
+                                   0, None)
     assert st == 1 and "ld_qkv" in pb.pblock_last_error()
-    st = lib.pblock_swattn_forward(ctypes.byref(c), FAKE, FAKE, FAKE, A + 4, FAKE, A, FAKE, None)
+    st = lib.pblock_swattn_forward(ctypes.byref(c), FAKE, FAKE, FAKE, A + 4, FAKE, A, FAKE, None,
+                                   0, None)
     assert st == 1
     st = lib.pblock_swattn_backward(ctypes.byref(c), FAKE, FAKE, FAKE, A, FAKE, A, FAKE, A, FAKE,
                                     FAKE, FAKE, FAKE, A, FAKE, 0, None)
@@ -168,3 +170,22 @@ def test_swattn_rejects_bad_leading_dimension():
 
 def test_status_strings():
     assert [pb.pblock_status_string(i) for i in range(5)] == [pb.STATUS[i] for i in range(5)]
+
+
+def test_swattn_workspace_modes():
+    """The split workspace is planned only when batch * heads * (seq / 64)
+    blocks are too few to fill the GPU; the backward's minimum is one fp32
+    row term per query."""
+    lib_ws = pb.pblock_swattn_workspace_bytes
+    small = pb.make_config(1, 2048, 1536, 12, 128, 64, 2048, "bf16")
+    big = pb.make_config(1, 8192, 5120, 40, 128, 64, 1024, "bf16")
+    f32 = pb.make_config(1, 2048, 1536, 12, 128, 64, 2048, "f32")
+    for c in (small, big, f32):
+        assert lib_ws(c, pb.ATTN_WS_BACKWARD_MIN) == -(-c.batch * c.heads * c.seq * 4 // 256) * 256
+        assert lib_ws(c, pb.ATTN_WS_BACKWARD) >= lib_ws(c, pb.ATTN_WS_BACKWARD_MIN)
+    assert lib_ws(small, pb.ATTN_WS_FORWARD) > 0
+    assert lib_ws(small, pb.ATTN_WS_BACKWARD) > lib_ws(small, pb.ATTN_WS_BACKWARD_MIN)
+    for c in (big, f32):
+        assert lib_ws(c, pb.ATTN_WS_FORWARD) == 0
+        assert lib_ws(c, pb.ATTN_WS_BACKWARD) == lib_ws(c, pb.ATTN_WS_BACKWARD_MIN)
+    assert lib_ws(small, 7) == 0

@@ -150,11 +150,13 @@ def test_repeat_runs_are_bitwise_identical():
 @pytest.mark.parametrize("W", [1, 5, 64, 65, 200, 10000])
 @pytest.mark.parametrize("d", [64, 128])
 def test_swattn_entry_points_match_oracle(W, d):
-    """pblock_swattn_forward / _backward on q, k, v with padded rows."""
+    """pblock_swattn_forward / _backward on q, k, v with padded rows, with the
+    split workspace (B * heads is small, so long blocks are split) and
+    without it; both must match the oracle and agree with each other."""
     import torch
     from oracle import pblock_oracle as orc
     from paper_2402_15627_amd import pblock as pb
-    B, S, nh = 2, 193, 3
+    B, S, nh = 2, 1193, 3
     _say(f"[gpu] swattn B={B} S={S} heads={nh} d={d} W={W}")
     rng = np.random.default_rng(W * 7 + d)
     A = nh * d
@@ -164,27 +166,38 @@ def test_swattn_entry_points_match_oracle(W, d):
     q, k, v, do = (round_to_bf16(a) for a in (q, k, v, do))
     dev = lambda a: torch.from_numpy(a).to(torch.bfloat16).cuda()
     cfg = pb.make_config(B, S, 64, nh, d, 64, W, "bf16")
-    o = torch.zeros((B, S, ld), dtype=torch.bfloat16, device="cuda")
-    lse = torch.zeros((B, nh, S), dtype=torch.float32, device="cuda")
-    pb.pblock_swattn_forward(cfg, dev(q), dev(k), dev(v), ld, o, ld, lse)
-    dq, dk, dv = (torch.zeros((B, S, ld), dtype=torch.bfloat16, device="cuda") for _ in range(3))
-    ws = torch.empty(pb.pblock_swattn_workspace_bytes(cfg), dtype=torch.uint8, device="cuda")
-    pb.pblock_swattn_backward(cfg, dev(q), dev(k), dev(v), ld, o, ld, dev(do), ld, lse, dq, dk, dv,
-                              ld, ws)
-    torch.cuda.synchronize()
-    on = o.float().cpu().numpy()
-    got = {n: t.float().cpu().numpy() for n, t in (("dq", dq), ("dk", dk), ("dv", dv))}
+    u8 = dict(dtype=torch.uint8, device="cuda")
+    runs = {}
+    for split in (True, False):
+        o = torch.zeros((B, S, ld), dtype=torch.bfloat16, device="cuda")
+        lse = torch.zeros((B, nh, S), dtype=torch.float32, device="cuda")
+        nf = pb.pblock_swattn_workspace_bytes(cfg, pb.ATTN_WS_FORWARD)
+        wsf = torch.empty(nf, **u8) if split and nf else None
+        pb.pblock_swattn_forward(cfg, dev(q), dev(k), dev(v), ld, o, ld, lse, wsf)
+        dq, dk, dv = (torch.zeros((B, S, ld), dtype=torch.bfloat16, device="cuda")
+                      for _ in range(3))
+        mode = pb.ATTN_WS_BACKWARD if split else pb.ATTN_WS_BACKWARD_MIN
+        ws = torch.empty(pb.pblock_swattn_workspace_bytes(cfg, mode), **u8)
+        pb.pblock_swattn_backward(cfg, dev(q), dev(k), dev(v), ld, o, ld, dev(do), ld, lse, dq,
+                                  dk, dv, ld, ws)
+        torch.cuda.synchronize()
+        runs[split] = {n: t.float().cpu().numpy()
+                       for n, t in (("o", o), ("lse", lse), ("dq", dq), ("dk", dk), ("dv", dv))}
+        # padding columns are never written
+        assert torch.count_nonzero(o[..., A:]) == 0
+        assert torch.count_nonzero(dq[..., A:]) == 0
+    got = runs[True]
     for b in range(B):
         for h in range(nh):
             sl = slice(h * d, (h + 1) * d)
             qq, kk, vv, gg = (a[b, :, sl].astype(np.float64) for a in (q, k, v, do))
             o_ref, l_ref = orc.swa_head_forward(qq, kk, vv, W)
             dq_r, dk_r, dv_r = orc.swa_head_backward(qq, kk, vv, gg, W)
-            assert normwise(on[b, :, sl], o_ref) <= 2e-2
-            np.testing.assert_allclose(lse[b, h].cpu().numpy(), l_ref, rtol=0, atol=2e-2)
+            assert normwise(got["o"][b, :, sl], o_ref) <= 2e-2
+            np.testing.assert_allclose(got["lse"][b, h], l_ref, rtol=0, atol=2e-2)
             for n, r in (("dq", dq_r), ("dk", dk_r), ("dv", dv_r)):
                 e = normwise(got[n][b, :, sl], r)
                 assert e <= 2e-2, (b, h, n, e)
-    # padding columns are never written
-    assert torch.count_nonzero(o[..., A:]) == 0
-    assert torch.count_nonzero(dq[..., A:]) == 0
+    for n in got:
+        e = normwise(runs[False][n], got[n])
+        assert e <= 1e-2, (n, e)
