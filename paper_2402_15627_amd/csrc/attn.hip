@@ -182,7 +182,8 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
   const int t_end = min(ntot, t_begin + cs);
   const bool split = ntot > cs;
   const int head = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int fr = lane & 31, fh = lane >> 5;
   const size_t tok0 = (size_t)b * S;
   const bf16* qb = Q + tok0 * ld + head * D;
@@ -231,39 +232,51 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
       }
       const bool full = (kv0 + TL - 1 <= qw0) && (qw0 + 31 - kv0 < W) && (kv0 + TL <= S) &&
                         (qw0 + 32 <= S);
+      if (!full) {
+        // element r of block h2 is key kv0 + 32 h2 + 8 (r >> 2) + 4 fh + (r & 3)
+        const int d0 = q - kv0 - 4 * fh, s0 = S - kv0 - 4 * fh;
+#pragma unroll
+        for (int h2 = 0; h2 < TL / 32; ++h2)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int c = 32 * h2 + 8 * (r >> 2) + (r & 3);
+            const bool ok = (unsigned)(d0 - c) < (unsigned)W && c < s0;
+            s[h2][r] = ok ? s[h2][r] : kNegInf;
+          }
+      }
       float mx = kNegInf;
 #pragma unroll
       for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float x = s[h2][r] * c2;
-          if (!full) {
-            const int key = kv0 + 32 * h2 + 8 * (r >> 2) + 4 * fh + (r & 3);
-            const int dist = q - key;
-            if (dist < 0 || dist >= W || key >= S) x = kNegInf;
-          }
-          s[h2][r] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = m_new == kNegInf ? 0.f : m_new;
-      const float alpha = exp2_hw(m_run - m_use);
-      m_run = m_new;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[h2][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+      // The reference maximum moves only when some query's scores exceed it
+      // by more than 8 (base 2): probabilities then stay below 256 and most
+      // tiles skip the rescale.  Output and sum share the reference, so the
+      // final quotient is unchanged.
+      if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = m_new == kNegInf ? 1.f : exp2_hw(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
+      }
+      const float m_use = m_run == kNegInf ? 0.f : m_run;
       float ls = 0.f;
 #pragma unroll
       for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = exp2_hw(s[h2][r] - m_use);
+          const float p = exp2_hw(fmaf(s[h2][r], c2, -m_use));
           s[h2][r] = p;
           ls += p;
         }
-      l_run = l_run * alpha + ls;
+      l_run += ls;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
 #pragma unroll
         for (int s2 = 0; s2 < TL / 16; ++s2)
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -430,7 +443,8 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   const int t_end = min(ntot, t_begin + cs);
   const bool split = ntot > cs;
   const int head = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int fr = lane & 31, fh = lane >> 5;
   const size_t tok0 = (size_t)b * S;
   const bf16* qb = Q + tok0 * ld + head * D;
@@ -495,6 +509,17 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
       // lane holds key `key` and queries qs + 32 h2 + 8 j + 4 fh + i (r = 4 j + i)
       const bool full = (qs >= kw0 + 31) && (qs + TL - 1 - kw0 < W) && (qs + TL <= S) &&
                         (kw0 + 32 <= S);
+      if (!full) {
+        const int d0 = qs + 4 * fh - key, s0 = S - qs - 4 * fh;
+#pragma unroll
+        for (int h2 = 0; h2 < TL / 32; ++h2)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int c = 32 * h2 + 8 * (r >> 2) + (r & 3);
+            const bool ok = (unsigned)(d0 + c) < (unsigned)W && c < s0;
+            p[h2][r] = ok ? p[h2][r] : kNegInf;
+          }
+      }
 #pragma unroll
       for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
@@ -505,11 +530,7 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int r = 4 * j + i;
-            float pv = exp2_hw(p[h2][r] * c2 - L4[i]);
-            if (!full) {
-              const int dist = qs + ql + i - key;
-              if (dist < 0 || dist >= W || qs + ql + i >= S) pv = 0.f;
-            }
+            const float pv = exp2_hw(fmaf(p[h2][r], c2, -L4[i]));
             p[h2][r] = pv;
             ds[h2][r] = pv * (ds[h2][r] - D4[i]);
           }
@@ -587,7 +608,8 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
   const int t_end = min(ntot, t_begin + cs);
   const bool split = ntot > cs;
   const int head = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int fr = lane & 31, fh = lane >> 5;
   const size_t tok0 = (size_t)b * S;
   const bf16* qb = Q + tok0 * ld + head * D;
@@ -646,18 +668,22 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
       }
       const bool full = (kv0 + TL - 1 <= qw0) && (qw0 + 31 - kv0 < W) && (kv0 + TL <= S) &&
                         (qw0 + 32 <= S);
+      if (!full) {
+        const int d0 = q - kv0 - 4 * fh, s0 = S - kv0 - 4 * fh;
+#pragma unroll
+        for (int h2 = 0; h2 < TL / 32; ++h2)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int c = 32 * h2 + 8 * (r >> 2) + (r & 3);
+            const bool ok = (unsigned)(d0 - c) < (unsigned)W && c < s0;
+            p[h2][r] = ok ? p[h2][r] : kNegInf;
+          }
+      }
 #pragma unroll
       for (int h2 = 0; h2 < TL / 32; ++h2)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float pv = exp2_hw(p[h2][r] * c2 - L2);
-          if (!full) {
-            const int k = kv0 + 32 * h2 + 8 * (r >> 2) + 4 * fh + (r & 3);
-            const int dist = q - k;
-            if (dist < 0 || dist >= W || k >= S) pv = 0.f;
-          }
-          ds[h2][r] = pv * (ds[h2][r] - Dq);
-        }
+        for (int r = 0; r < 16; ++r)
+          ds[h2][r] = exp2_hw(fmaf(p[h2][r], c2, -L2)) * (ds[h2][r] - Dq);
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
