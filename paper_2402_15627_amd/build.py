@@ -26,6 +26,12 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE, "-I", CSRC,
 ]
+# Per-source extras.  The attention kernels post-process every matrix result
+# with vector arithmetic; keeping all matrix results in ordinary vector
+# registers avoids per-tile copies between the two register files.
+EXTRA = {
+    "attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
 
 
 def sources():
@@ -35,7 +41,7 @@ def sources():
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")

@@ -33,16 +33,16 @@ constexpr float kNegInf = -__builtin_huge_valf();
 
 // Waves per workgroup and tile length (tokens per LDS tile):
 //   forward and dQ: 32 kWavesQ queries per workgroup, key tiles of kTL
-//   dK/dV         : 32 kWavesK keys per workgroup, query tiles of kTLdkv
+//   dK/dV         : kBlockK keys per workgroup (kWavesK waves), query tiles of kTLdkv
 // Four forward / dQ waves share each K/V tile, which with two workgroups per
 // CU (64 KB of LDS each) keeps two waves on every SIMD, so one wave's
 // softmax arithmetic overlaps another's matrix instructions.
 constexpr int kWavesQ = 4;
-constexpr int kWavesK = 2;
+constexpr int kWavesK = 4;  // two key groups of 32, each with a P wave and a dS wave
 constexpr int kTL = 64;      // forward and dQ key tiles
 constexpr int kTLdkv = 32;   // dK/dV query tiles (keeps its registers and LDS in budget)
 constexpr int kBlockQ = 32 * kWavesQ;  // queries per forward / dQ workgroup
-constexpr int kBlockK = 32 * kWavesK;  // keys per dK/dV workgroup
+constexpr int kBlockK = 64;            // keys per dK/dV workgroup
 constexpr int kUnsplit = 1 << 30;
 
 // Key tiles (of kTL) that the query block q0 .. q0 + kBlockQ - 1 visits.
@@ -414,10 +414,14 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(const T* __restrict__ O
 }
 
 // ====================================================== backward: dK, dV
-// Workgroup: 32 kWavesK keys; wave w owns keys k0 + 32 w .. +31 (lane: one key).
-// Per query tile: S = Q K^T and dP = dO V^T (queries x keys), P and
-// dS = P (dP - delta), then dV^T += dO^T P and dK^T += Q^T dS, the
-// transposed operands read from the natural Q and dO tiles.
+// Workgroup: 64 keys in two groups of 32, four waves.  Per key group, wave
+// "P" computes S = Q K^T and P = exp(S - lse), hands P to its partner through
+// LDS, and accumulates dV^T += dO^T P; wave "dS" computes dP = dO V^T, forms
+// dS = P (dP - delta) and accumulates dK^T += Q^T dS.  Each wave so holds one
+// operand fragment set (K or V of its 32 keys) and one accumulator block
+// instead of two, and both roles run the same matrix code on different
+// tiles: half the registers of one wave doing both, and no repeated work.
+// The transposed operands are read from the natural Q and dO tiles.
 template <int D>
 __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
@@ -429,6 +433,8 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   constexpr int NB = kBlockK;
   constexpr int TB = TL * 2 * D;
   constexpr int STAGE = 2 * TB + 2 * TL * 4;  // Q, dO, then lse*log2e and delta
+  constexpr int PBUF = 64 * 16 * 4;           // one wave's P: 16 fp32 per lane
+  static_assert(TL == 32 && NB == 64 && kWavesK == 4, "two key groups x two roles");
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
   auto q_off = [&](int s) { return s * STAGE; };
@@ -445,30 +451,29 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int grp = wave & 1;
+  const bool pside = wave < 2;
   const int fr = lane & 31, fh = lane >> 5;
   const size_t tok0 = (size_t)b * S;
   const bf16* qb = Q + tok0 * ld + head * D;
-  const bf16* kb = K + tok0 * ld + head * D;
-  const bf16* vb = V + tok0 * ld + head * D;
   const bf16* gb = dO + tok0 * ld_o + head * D;
   const float* lseb = lse + ((size_t)b * H + head) * S;
   const float* delb = delta + ((size_t)b * H + head) * S;
+  float* pbuf = (float*)(smem + 2 * STAGE + grp * PBUF);
 
-  const int kw0 = k0 + 32 * wave;
+  const int kw0 = k0 + 32 * grp;
   const int key = kw0 + fr;
-  bf16x8 kf[D / 16], vf[D / 16];
+  // K (P side) or V (dS side) rows of this wave's 32 keys
+  const bf16* kvb = (pside ? K : V) + tok0 * ld + head * D;
+  bf16x8 kvf[D / 16];
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    const size_t off = (size_t)min(key, S - 1) * ld + 16 * ks + 8 * fh;
-    kf[ks] = load_row_frag(kb + off, key < S);
-    vf[ks] = load_row_frag(vb + off, key < S);
-  }
-  f32x16 dk[D / 32], dv[D / 32];
+  for (int ks = 0; ks < D / 16; ++ks)
+    kvf[ks] = load_row_frag(kvb + (size_t)min(key, S - 1) * ld + 16 * ks + 8 * fh, key < S);
+  f32x16 acc[D / 32];
 #pragma unroll
-  for (int i = 0; i < D / 32; ++i) dk[i] = dv[i] = zero16();
+  for (int i = 0; i < D / 32; ++i) acc[i] = zero16();
 
   const float c2 = scale * kLog2e;
-  const int w_lo = kw0, w_hi = min(S - 1, kw0 + 31 + W - 1);  // queries this wave needs
 
   float rl = 0.f;
   auto issue_stage = [&](int qs, int s) {
@@ -489,95 +494,84 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
     wait_dma_all();
     block_barrier();
     if (t + 1 < t_end) issue_stage(qs + TL, cur ^ 1);
-    if (kw0 < S && qs <= w_hi && qs + TL - 1 >= w_lo) {
-      const unsigned char* qt = smem + q_off(cur);
-      const unsigned char* gt = smem + g_off(cur);
-      const float* ls = (const float*)(smem + l_off(cur));
-      f32x16 p[TL / 32], ds[TL / 32];
+    const unsigned char* qt = smem + q_off(cur);
+    const unsigned char* gt = smem + g_off(cur);
+    const float* ls = (const float*)(smem + l_off(cur));
+    // Every tile runs unconditionally: where none of a key group's pairs is
+    // inside the window the mask zeroes P, hence dS, and the sums stay exact.
+    // Lane holds key `key` and queries qs + 8 j + 4 fh + i of element 4 j + i.
+    f32x16 sc = zero16();  // S (P side) or dP (dS side)
+    const unsigned char* nt = pside ? qt : gt;
 #pragma unroll
-      for (int h2 = 0; h2 < TL / 32; ++h2) {
-        p[h2] = zero16();
-        ds[h2] = zero16();
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          p[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(qt, 32 * h2 + fr, ks, fh),
-                                                          kf[ks], p[h2], 0, 0, 0);
-          ds[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(gt, 32 * h2 + fr, ks, fh),
-                                                           vf[ks], ds[h2], 0, 0, 0);
-        }
-      }
-      // lane holds key `key` and queries qs + 32 h2 + 8 j + 4 fh + i (r = 4 j + i)
+    for (int ks = 0; ks < D / 16; ++ks)
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(nt, fr, ks, fh), kvf[ks], sc, 0,
+                                                   0, 0);
+    if (pside) {
       const bool full = (qs >= kw0 + 31) && (qs + TL - 1 - kw0 < W) && (qs + TL <= S) &&
                         (kw0 + 32 <= S);
       if (!full) {
         const int d0 = qs + 4 * fh - key, s0 = S - qs - 4 * fh;
 #pragma unroll
-        for (int h2 = 0; h2 < TL / 32; ++h2)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int c = 32 * h2 + 8 * (r >> 2) + (r & 3);
-            const bool ok = (unsigned)(d0 + c) < (unsigned)W && c < s0;
-            p[h2][r] = ok ? p[h2][r] : kNegInf;
-          }
+        for (int r = 0; r < 16; ++r) {
+          const int c = 8 * (r >> 2) + (r & 3);
+          const bool ok = (unsigned)(d0 + c) < (unsigned)W && c < s0;
+          sc[r] = ok ? sc[r] : kNegInf;
+        }
       }
 #pragma unroll
-      for (int h2 = 0; h2 < TL / 32; ++h2)
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 L4 = *reinterpret_cast<const f32x4*>(ls + 8 * j + 4 * fh);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int ql = 32 * h2 + 8 * j + 4 * fh;
-          const f32x4 L4 = *reinterpret_cast<const f32x4*>(ls + ql);
-          const f32x4 D4 = *reinterpret_cast<const f32x4*>(ls + TL + ql);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = 4 * j + i;
-            const float pv = exp2_hw(fmaf(p[h2][r], c2, -L4[i]));
-            p[h2][r] = pv;
-            ds[h2][r] = pv * (ds[h2][r] - D4[i]);
-          }
-        }
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int s2 = 0; s2 < TL / 16; ++s2) {
-          dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_tr<D>(gt, 32 * db + fr, s2, fh, lane), probs_frag(p, s2), dv[db], 0, 0, 0);
-          dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_tr<D>(qt, 32 * db + fr, s2, fh, lane), probs_frag(ds, s2), dk[db], 0, 0, 0);
-        }
+        for (int i = 0; i < 4; ++i) sc[4 * j + i] = exp2_hw(fmaf(sc[4 * j + i], c2, -L4[i]));
+        *reinterpret_cast<f32x4*>(pbuf + (j * 64 + lane) * 4) =
+            f32x4{sc[4 * j], sc[4 * j + 1], sc[4 * j + 2], sc[4 * j + 3]};
+      }
     }
+    block_barrier();  // P of this tile is visible to the dS side
+    if (!pside) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 P4 = *reinterpret_cast<const f32x4*>(pbuf + (j * 64 + lane) * 4);
+        const f32x4 D4 = *reinterpret_cast<const f32x4*>(ls + TL + 8 * j + 4 * fh);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sc[4 * j + i] = P4[i] * (sc[4 * j + i] - D4[i]);
+      }
+    }
+    const unsigned char* tt = pside ? gt : qt;  // dO^T with P, Q^T with dS
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int s2 = 0; s2 < TL / 16; ++s2)
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            frag_tr<D>(tt, 32 * db + fr, s2, fh, lane), probs_frag(&sc, s2), acc[db], 0, 0, 0);
     if (t + 1 < t_end) finish_stage(cur ^ 1);
   }
 
-  if (key < S && split) {
-    const size_t bhs = (size_t)gridDim.z * H * S;
-    const size_t prow = ((size_t)chunk * bhs + ((size_t)b * H + head) * S + key) * D;
+  if (key < S) {
+    const float mul = pside ? 1.f : scale;  // dV, or dK with the score scale
+    if (split) {
+      const size_t bhs = (size_t)gridDim.z * H * S;
+      float* prow =
+          (pside ? pdv : pdk) + ((size_t)chunk * bhs + ((size_t)b * H + head) * S + key) * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = 32 * db + 8 * j + 4 * fh;
-        *reinterpret_cast<f32x4*>(pdk + prow + e) =
-            f32x4{dk[db][4 * j] * scale, dk[db][4 * j + 1] * scale, dk[db][4 * j + 2] * scale,
-                  dk[db][4 * j + 3] * scale};
-        *reinterpret_cast<f32x4*>(pdv + prow + e) =
-            f32x4{dv[db][4 * j], dv[db][4 * j + 1], dv[db][4 * j + 2], dv[db][4 * j + 3]};
-      }
-  } else if (key < S) {
-    bf16* dkr = dK + (tok0 + key) * ld_d + head * D;
-    bf16* dvr = dV + (tok0 + key) * ld_d + head * D;
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(prow + 32 * db + 8 * j + 4 * fh) =
+              f32x4{acc[db][4 * j] * mul, acc[db][4 * j + 1] * mul, acc[db][4 * j + 2] * mul,
+                    acc[db][4 * j + 3] * mul};
+    } else {
+      bf16* orow = (pside ? dV : dK) + (tok0 + key) * ld_d + head * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float a[4], c[4];
+        for (int j = 0; j < 4; ++j) {
+          float a[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          a[i] = dk[db][4 * j + i] * scale;
-          c[i] = dv[db][4 * j + i];
+          for (int i = 0; i < 4; ++i) a[i] = acc[db][4 * j + i] * mul;
+          store4(orow + 32 * db + 8 * j + 4 * fh, a);
         }
-        store4(dkr + 32 * db + 8 * j + 4 * fh, a);
-        store4(dvr + 32 * db + 8 * j + 4 * fh, c);
-      }
+    }
   }
 }
 
@@ -826,7 +820,7 @@ __global__ __launch_bounds__(64) void attn_dkdv_f32(const float* __restrict__ Q,
 template <int D>
 size_t fwd_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 template <int D>
-size_t dkdv_lds() { return 2 * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4); }
+size_t dkdv_lds() { return 2 * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4) + 2 * 64 * 16 * 4; }
 template <int D>
 size_t dq_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 
