@@ -14,12 +14,30 @@ Prints one JSON line.  Besides the contract fields it carries:
   steps         per-step times from a separate pass with events around every
                 step;
   cpu_baseline  the fp64 CPU oracle timed on this host on one full step.
+
+Profiling helpers (see the commands recorded in profiles/):
+  --copy-calibration   run a plain copy-like kernel of known size, for scaling
+                       the FETCH_SIZE / WRITE_SIZE counters;
+  --traffic-summary D1 D2 D3 D4
+                       turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE
+                       of the bench, then of the copy) into the measured HBM
+                       traffic per launch of the dominant kernel, written to
+                       profiles/ with a fingerprint of the kernel's sources;
+                       the bench reports it as roofline.traffic while the
+                       sources are unchanged (null otherwise);
+  --trace-summary D    markdown table of a rocprofv3 --kernel-trace --stats run,
+                       per kernel and launch grid, with the block step each
+                       GEMM launch belongs to.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -55,6 +73,180 @@ def step_work(s):
     }
 
 
+# Sources whose code a step's dominant kernel is built from.
+KERNEL_SOURCES = {
+    "gemm": ["gemm.hip", "common.h", "kernels.h"],
+    "attn": ["attn.hip", "common.h", "kernels.h"],
+    "ln": ["ln.hip", "common.h", "kernels.h"],
+}
+STEP_SOURCE = {"in_proj": "gemm", "out_proj": "gemm", "dc": "gemm", "dw_out": "gemm", "dh": "gemm",
+               "dw_in": "gemm", "attn_fwd": "attn", "attn_bwd": "attn", "ln_fwd": "ln",
+               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln"}
+COPY_BYTES = 1 << 30  # read and written once by the calibration copy
+
+
+def source_fingerprint(step):
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2402_15627_amd", "csrc")
+    for f in KERNEL_SOURCES[STEP_SOURCE[step]] + ["../build.py"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def gemm_steps(s):
+    """(M, N, K) of each GEMM step as launched."""
+    T, H, n_in, k_out = s.tokens, s.hidden, s.n_in, s.k_out
+    return {"in_proj": (T, n_in, H), "out_proj": (T, H, k_out), "dc": (T, k_out, H),
+            "dw_out": (H, k_out, T), "dh": (T, H, n_in), "dw_in": (n_in, H, T)}
+
+
+# Template arguments of each GEMM step's kernel as they appear in demangled
+# names: A K-contiguous, B K-contiguous, epilogue (pb::Epi value).
+GEMM_SIGNATURE = {"in_proj": "<true, true, (pb::Epi)1", "out_proj": "<true, true, (pb::Epi)2",
+                  "dc": "<true, false, (pb::Epi)3", "dw_out": "<false, false, (pb::Epi)0",
+                  "dh": "<true, false, (pb::Epi)0", "dw_in": "<false, false, (pb::Epi)0"}
+
+
+def demangle(name):
+    if not name.startswith("_Z"):
+        return name
+    try:
+        import subprocess
+        return subprocess.run(["c++filt", name], capture_output=True, text=True).stdout.strip()
+    except OSError:
+        return name
+
+
+def gemm_step_of(name, grid, s):
+    """Block step a GEMM launch belongs to ("" if none)."""
+    for st, mnk in gemm_steps(s).items():
+        if ("gemm_bf16" in name and GEMM_SIGNATURE[st] in name
+                and gemm_grid_threads(*mnk) == grid):
+            return st
+    return ""
+
+
+def gemm_grid_threads(M, N, K):
+    """Work-items of a bf16 GEMM launch: 256 x 256 output tiles of 512 threads;
+    when the tiles leave a partial last wave over the 256 CUs, those tail tiles
+    are split along K (the plan the library uses with a full workspace)."""
+    tiles = -(-M // 256) * -(-N // 256)
+    n_full = tiles // 256 * 256
+    tail = tiles - n_full
+    if K % 64 == 0 and n_full and tail:
+        splits = min(256 // tail, K // 64)
+        if splits >= 2:
+            return (n_full + tail * splits) * 512
+    return tiles * 512
+
+
+def traffic_path(step, workload):
+    return os.path.join(ROOT, "profiles", f"{step}_{workload}_traffic.md")
+
+
+def _counter_rows(d):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    with open(files[0]) as fh:
+        return list(csv.DictReader(fh))
+
+
+def _per_dispatch(rows, counter, pick):
+    """Mean over the picked dispatches of a counter (summed over its instances)."""
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] == counter and pick(r):
+            per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    if not per:
+        raise SystemExit(f"no dispatch with {counter} matched")
+    return sum(per.values()) / len(per), len(per)
+
+
+def traffic_summary(dirs, workload, step):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the step's kernel, scaled
+    by what the same counters read for the calibration copy of COPY_BYTES."""
+    from paper_2402_15627_amd.inputs import WORKLOADS
+    s = WORKLOADS[workload]
+    if step not in gemm_steps(s):
+        raise SystemExit(f"traffic summary supports the GEMM steps, not {step}")
+    grid = gemm_grid_threads(*gemm_steps(s)[step])
+    pick = lambda r: gemm_step_of(r["Kernel_Name"], int(r["Grid_Size"]), s) == step  # noqa: E731
+    copy_pick = lambda r: "neg_kernel" in r["Kernel_Name"]  # noqa: E731
+    fetch, n1 = _per_dispatch(_counter_rows(dirs[0]), "FETCH_SIZE", pick)
+    write, n2 = _per_dispatch(_counter_rows(dirs[1]), "WRITE_SIZE", pick)
+    cfetch, _ = _per_dispatch(_counter_rows(dirs[2]), "FETCH_SIZE", copy_pick)
+    cwrite, _ = _per_dispatch(_counter_rows(dirs[3]), "WRITE_SIZE", copy_pick)
+    ff, wf = COPY_BYTES / 1024 / cfetch, COPY_BYTES / 1024 / cwrite
+    M, N, K = gemm_steps(s)[step]
+    e = 2 if s.dtype == "bf16" else 4
+    out_bytes = 4 if step in ("dw_in", "dw_out", "dh") else e
+    rec = {
+        "step": step, "workload": workload, "grid_threads": grid, "dispatches": [n1, n2],
+        "fetch_kib": round(fetch, 1), "write_kib": round(write, 1),
+        "copy_bytes": COPY_BYTES, "copy_fetch_kib": round(cfetch, 1),
+        "copy_write_kib": round(cwrite, 1), "fetch_scale": round(ff, 4),
+        "write_scale": round(wf, 4),
+        "traffic_bytes": int(fetch * 1024 * ff + write * 1024 * wf),
+        "algorithmic_bytes": (M * K + N * K) * e + M * N * out_bytes,
+        "source_fingerprint": source_fingerprint(step),
+    }
+    return rec
+
+
+def read_traffic(step, workload):
+    """Measured HBM bytes per launch from profiles/, if the sources still match."""
+    try:
+        with open(traffic_path(step, workload)) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_fingerprint") != source_fingerprint(step):
+        return None
+    return rec["traffic_bytes"]
+
+
+def trace_summary(d, workload):
+    """Markdown table of a kernel-trace run: one row per (kernel, grid)."""
+    from paper_2402_15627_amd.inputs import WORKLOADS
+    s = WORKLOADS[workload]
+    files = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_trace.csv under {d}")
+    groups = {}
+    with open(files[0]) as fh:
+        for r in csv.DictReader(fh):
+            name = demangle(r["Kernel_Name"])
+            grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+            dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            groups.setdefault((name, grid), []).append(dur)
+    total = sum(sum(v) for v in groups.values())
+    rows = []
+    for (name, grid), v in groups.items():
+        short = re.sub(r"^void ", "", name).replace("pb::(anonymous namespace)::", "")
+        for i, e in enumerate(("StoreF32", "BiasGelu", "BiasResid", "DgeluSplit")):
+            short = short.replace(f"(pb::Epi){i}", e)
+        m = re.match(r"_ZN2pb12_GLOBAL__N_1\d+(\w+?)I", short)  # names c++filt leaves
+        if m:
+            d = re.search(r"Li(\d+)E", short)
+            short = m.group(1) + (f"<{d.group(1)}>" if d else "")
+        short = re.sub(r"\(.*", "", short)
+        step = gemm_step_of(name, grid, s)
+        rows.append((sum(v), short[:70], grid, step, len(v), sum(v) / len(v), min(v), max(v)))
+    rows.sort(reverse=True)
+    out = ["| kernel | grid (work-items) | block step | calls | avg us | min us | max us | "
+           "% of GPU time |", "|---|---:|---|---:|---:|---:|---:|---:|"]
+    for tot, short, grid, step, n, avg, lo, hi in rows:
+        out.append(f"| `{short}` | {grid} | {step} | {n} | {avg:.1f} | {lo:.1f} | {hi:.1f} | "
+                   f"{100 * tot / total:.1f} |")
+    return "\n".join(out)
+
+
 def cpu_baseline(shape, inputs):
     """Time the fp64 oracle (as it stands) on one full forward + backward step."""
     import numpy as np  # noqa: F401
@@ -83,7 +275,32 @@ def main():
     ap.add_argument("--workload", default="175b_tp8_share")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run the counter calibration copy and exit")
+    ap.add_argument("--traffic-summary", nargs=4, metavar="DIR",
+                    help="rocprofv3 --pmc output dirs: FETCH_SIZE and WRITE_SIZE of the bench, "
+                         "then of --copy-calibration; writes profiles/<step>_<workload>_traffic.md")
+    ap.add_argument("--traffic-step", default="dw_in")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="print a markdown table of a rocprofv3 --kernel-trace output dir")
+    ap.add_argument("--command", default="", help="command line recorded with a summary")
     args = ap.parse_args()
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary, args.workload))
+        return
+    if args.traffic_summary:
+        rec = traffic_summary(args.traffic_summary, args.workload, args.traffic_step)
+        path = traffic_path(args.traffic_step, args.workload)
+        with open(path, "w") as fh:
+            fh.write(f"# HBM traffic of the {args.traffic_step} GEMM, {args.workload}\n\n"
+                     "FETCH_SIZE and WRITE_SIZE (KiB per dispatch, rocprofv3 --pmc, one counter "
+                     "per run) of the launches with this step's grid, each scaled by "
+                     f"{COPY_BYTES} bytes over what the same counter reads for one dispatch of "
+                     "the calibration copy (a read-once, write-once elementwise kernel).\n\n"
+                     f"Commands (repository root on the GPU host):\n\n```\n{args.command}\n```\n\n"
+                     f"```json\n{json.dumps(rec, indent=1)}\n```\n")
+        print(json.dumps(rec))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the block's kernels run on a single MI355X and this "
               "build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
@@ -91,6 +308,16 @@ def main():
 
     import numpy as np  # noqa: F401
     import torch
+
+    if args.copy_calibration:
+        # a plain elementwise pass: reads COPY_BYTES once and writes them once
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": COPY_BYTES}))
+        return
 
     from paper_2402_15627_amd import pblock as pb
     from paper_2402_15627_amd.inputs import WORKLOADS, make_inputs, model_flops
@@ -158,12 +385,13 @@ def main():
         achieved = amount / (dom_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None, "kernel": dominant, "flops_per_launch": amount,
-                "avg_ms": round(dom_ms, 4)}
+                "traffic": read_traffic(dominant, shape.name), "kernel": dominant,
+                "flops_per_launch": amount, "avg_ms": round(dom_ms, 4)}
     else:
         achieved = amount / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": read_traffic(dominant, shape.name),
                 "kernel": dominant, "bytes_per_launch": amount, "avg_ms": round(dom_ms, 4)}
 
     steps_out = {}

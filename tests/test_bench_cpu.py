@@ -1,0 +1,68 @@
+"""Host-side pieces of bench.py: the one-GPU guard, the GEMM launch-grid
+labelling used by the profile summaries, and the traffic record check."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+from paper_2402_15627_amd.inputs import WORKLOADS  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_gemm_grid_matches_the_split_plan():
+    s = WORKLOADS["175b_tp8_share"]
+    steps = bench.gemm_steps(s)
+    # dw_in: 42 x 48 = 2016 tiles, tail of 224 is too large to split
+    assert bench.gemm_grid_threads(*steps["dw_in"]) == 2016 * 512
+    # out_proj: 8 x 48 = 384 tiles -> 256 whole + 128 tail tiles split 2 ways
+    assert bench.gemm_grid_threads(*steps["out_proj"]) == (256 + 128 * 2) * 512
+    # in_proj: 8 x 42 = 336 tiles -> 256 + 80 tail tiles split 3 ways
+    assert bench.gemm_grid_threads(*steps["in_proj"]) == (256 + 80 * 3) * 512
+    # no whole wave: unsplit
+    assert bench.gemm_grid_threads(512, 512, 4096) == 4 * 512
+    # K not a multiple of 64: unsplit
+    assert bench.gemm_grid_threads(2048, 12288 + 256, 1000) == 8 * 49 * 512
+
+
+def test_gemm_steps_are_told_apart():
+    s = WORKLOADS["175b_tp8_share"]
+    name = "void pb::(anonymous namespace)::gemm_bf16_dma_kernel<true, true, (pb::Epi)2, true>()"
+    g = bench.gemm_grid_threads(*bench.gemm_steps(s)["out_proj"])
+    assert bench.gemm_step_of(name, g, s) == "out_proj"
+    dh = name.replace("<true, true, (pb::Epi)2", "<true, false, (pb::Epi)0")
+    assert bench.gemm_step_of(dh, g, s) == "dh"   # same grid, other template
+    assert bench.gemm_step_of(name, g + 512, s) == ""
+
+
+def test_traffic_is_reported_only_for_unchanged_sources(tmp_path, monkeypatch):
+    rec = {"traffic_bytes": 123, "source_fingerprint": bench.source_fingerprint("dw_in")}
+    path = tmp_path / "dw_in_x_traffic.md"
+    path.write_text(f"# t\n\n```json\n{json.dumps(rec)}\n```\n")
+    monkeypatch.setattr(bench, "traffic_path", lambda step, wl: str(path))
+    assert bench.read_traffic("dw_in", "x") == 123
+    rec["source_fingerprint"] = "0" * 16
+    path.write_text(f"# t\n\n```json\n{json.dumps(rec)}\n```\n")
+    assert bench.read_traffic("dw_in", "x") is None
+    monkeypatch.setattr(bench, "traffic_path", lambda step, wl: str(tmp_path / "missing.md"))
+    assert bench.read_traffic("dw_in", "x") is None
+
+
+def test_committed_traffic_profile_parses():
+    p = bench.traffic_path("dw_in", "175b_tp8_share")
+    if not os.path.exists(p):
+        pytest.skip("no traffic profile committed")
+    text = open(p).read()
+    assert "rocprofv3 --pmc FETCH_SIZE" in text and "rocprofv3 --pmc WRITE_SIZE" in text
+    rec = json.loads(text.split("```json\n")[1].split("\n```")[0])
+    assert rec["traffic_bytes"] > 0 and rec["algorithmic_bytes"] > 0
