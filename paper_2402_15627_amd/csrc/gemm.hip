@@ -1,15 +1,18 @@
 // Projection GEMMs of the parallel block with fused epilogues.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 256x256 output tile per
-// workgroup of eight waves (each wave 64x128), K-tile 64, double-buffered
-// LDS (128 KB).  LDS holds both operands K-contiguous, 128-byte rows with
-// the 16-byte chunk index XOR-swizzled by the row so that fragment reads and
-// tile writes touch distinct banks.  An operand that is M- or N-contiguous in
-// HBM (the token-contracted weight-gradient GEMMs, and the weights of the
-// input-gradient GEMMs) is loaded as 8x8 blocks and transposed in registers
-// on its way into LDS.  The MFMA is issued with the roles of the operands
-// swapped (the N tile as MFMA "A"), so each lane ends up holding four
-// consecutive output columns of one row: 8- or 16-byte epilogue stores.
+// workgroup of eight waves (each wave 64x128).  Two kernels share the tile,
+// the wave layout and the epilogues:
+//   - K a multiple of 64 (every GEMM of the block at the benchmarked sizes):
+//     operands reach LDS by LDS-DMA, K-tiles of 32 through four stages, the
+//     barrier placed mid-tile (see the DMA kernel below);
+//   - otherwise (ragged token counts in the weight-gradient GEMMs): K-tile
+//     64, double-buffered LDS, loads staged through registers with zero fill;
+//     an M- or N-contiguous operand is loaded as 8x8 blocks and transposed in
+//     registers on its way into LDS.
+// The MFMA is issued with the roles of the operands swapped (the N tile as
+// MFMA "A"), so each lane ends up holding four consecutive output columns of
+// one row: 8- or 16-byte epilogue stores.
 //
 // The epilogues carry the block's elementwise work (MegaScale Section 3.3
 // fuses these fine-grained ops): in-projection bias + GeLU writing both U and
@@ -277,46 +280,60 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
 // Used when K is a multiple of 64.  The operand tiles go from global memory
 // straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
 // LDS base + 16 * lane), so there is no register staging and no LDS write
-// instruction.  A K-contiguous operand is stored K-major (as above); an
-// MN-contiguous operand is stored MN-major, 64 k-rows of 512 bytes with the
-// 16-byte chunk index XOR-ed by 4 (k mod 4), and its MFMA fragments are read
-// with ds_read_b64_tr_b16, which transposes 4 (k) x 16 (mn) blocks across a
-// 16-lane group.  The DMA instructions are issued from inline assembly and
-// waited for explicitly, so the compiler adds no conservative waits between
-// them and the LDS reads of the other stage.
+// instruction.  The loop runs over K-tiles of 32 through four LDS stages
+// (4 x 32 KB): a tile's loads are issued two tiles ahead of its use, which
+// covers their latency.  The one workgroup barrier of each K-tile sits
+// between its two k-steps, so the first k-step's MFMAs are still executing
+// while the waves synchronise, and the next tile's first fragments are read
+// before the tile boundary: the matrix pipe does not drain at the barrier.
+//
+// A K-contiguous operand is stored K-major (64-byte rows, the 16-byte chunk
+// index XOR-ed by (row / 4) mod 4); an MN-contiguous operand is stored
+// MN-major, 32 k-rows of 512 bytes with the chunk index XOR-ed by
+// 4 (k mod 4), and its MFMA fragments are read with ds_read_b64_tr_b16, which
+// transposes 4 (k) x 16 (mn) blocks across a 16-lane group.  Both patterns
+// are free of bank conflicts.  The DMA instructions are issued from inline
+// assembly as scalar base + per-lane offset (no per-load address arithmetic)
+// and waited for explicitly, so the compiler adds no conservative waits
+// between them and the LDS reads of other stages.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 #define PB_LDS __attribute__((address_space(3)))
 
+constexpr int kDK = 32;                     // K-tile of the DMA path
+constexpr int kStages = 4;
+constexpr int kDTile = kBM * kDK * 2;       // one operand tile: 16 KB
+constexpr int kPieces = kDTile / kThreads / 16;  // 1 KB DMA pieces per operand per wave: 2
+constexpr int kDmaPerStage = 2 * kPieces;   // DMA instructions per wave per stage
+static_assert(kBM == kBN && kPieces * 1024 * (kThreads / 64) == kDTile, "tile split over waves");
+
+PB_DEV int swz_k(int row, int c) { return c ^ ((row >> 2) & 3); }
 PB_DEV int swz_mn(int krow, int c) { return c ^ (4 * (krow & 3)); }
 
-PB_DEV void dma16(const void* g, uint32_t lds_byte_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_byte_addr)
+PB_DEV void dma16s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
+               "s"(lds_byte_addr)
                : "memory", "m0");
 }
-PB_DEV void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+template <int N>
+PB_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// This wave's 4 KB share of one 256 x 64 operand tile (four 1 KB DMA pieces).
+// Byte offset, from the operand tile's base (its first row, or first column,
+// at the tile's k), of this lane's 16 bytes in DMA piece i of this wave.
+// KC: row r of the tile at X[(R0 + r) * ld + k]; rows past Rmax are clamped
+// (their results are never stored).  Else X[k * ld + R0 + c], columns past
+// Rmax clamped the same way.
 template <bool KC>
-PB_DEV void dma_tile(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k0,
-                     uint32_t lds_tile, int wave, int lane) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int base = wave * 4096 + i * 1024;
-    const int p = base + 16 * lane;
-    const bf16* g;
-    if constexpr (KC) {
-      const int row = p >> 7, c = swz(row, (p >> 4) & 7);
-      int r = R0 + row;
-      r = r < Rmax ? r : Rmax - 1;  // clamped rows: results never stored
-      g = X + (size_t)r * ld + k0 + 8 * c;
-    } else {
-      const int krow = p >> 9, c = swz_mn(krow, (p >> 4) & 31);
-      int col = R0 + 8 * c;
-      col = col < Rmax ? col : Rmax - 8;
-      g = X + (size_t)(k0 + krow) * ld + col;
-    }
-    dma16(g, __builtin_amdgcn_readfirstlane(lds_tile + base));
+PB_DEV uint32_t dma_lane_off(int ld, int R0, int Rmax, int wave, int lane, int i) {
+  const int p = wave * (kPieces * 1024) + i * 1024 + 16 * lane;
+  if constexpr (KC) {
+    const int row = p >> 6, c = swz_k(row, (p >> 4) & 3);
+    const int r = min(R0 + row, Rmax - 1) - R0;
+    return (uint32_t)(r * ld + 8 * c) * 2u;
+  } else {
+    const int krow = p >> 9, c = swz_mn(krow, (p >> 4) & 31);
+    const int col = min(R0 + 8 * c, Rmax - 8) - R0;
+    return (uint32_t)(krow * ld + col) * 2u;
   }
 }
 
@@ -324,7 +341,7 @@ PB_DEV void dma_tile(const bf16* __restrict__ X, int ld, int R0, int Rmax, int k
 template <bool KC>
 PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, int lane) {
   if constexpr (KC) {
-    return *reinterpret_cast<const bf16x8*>(lds_tile + row * 128 + swz(row, 2 * ks + h) * 16);
+    return *reinterpret_cast<const bf16x8*>(lds_tile + row * 64 + swz_k(row, 2 * ks + h) * 16);
   } else {
     // lane 4 j + q of a 16-lane group reads k-row kb + j, mn (row & ~15) + 4 q;
     // the transposing read hands lane i the four k values of mn (row & ~15) + i
@@ -357,11 +374,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
                                                                     float* __restrict__ part) {
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
-  auto a_off = [&](int s) { return (2 * s) * kTileBytes; };
-  auto b_off = [&](int s) { return (2 * s + 1) * kTileBytes; };
+  auto a_off = [&](int s) { return (2 * s) * kDTile; };
+  auto b_off = [&](int s) { return (2 * s + 1) * kDTile; };
 
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
-  const int nk_all = K / kBK;
+  const int nk_all = K / kBK;  // slices are planned in units of 64
   int lid, slice = -1, kt0 = 0, kt1 = nk_all;
   if ((int)blockIdx.x < n_full) {
     lid = xcd_remap(blockIdx.x, n_full);
@@ -377,8 +394,38 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
   int tm, tn;
   tile_of(lid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
+  const int fr = lane & 31, fh = lane >> 5;
+
+  // 32-wide K-tiles [t_first, t_first + nt) of this work item
+  const int t_first = kDK == kBK ? kt0 : kt0 * (kBK / kDK);
+  const int nt = (kt1 - kt0) * (kBK / kDK);
+  uint32_t aoff[kPieces], boff[kPieces];
+#pragma unroll
+  for (int i = 0; i < kPieces; ++i) {
+    aoff[i] = dma_lane_off<AK>(lda, m0, M, wave, lane, i);
+    boff[i] = dma_lane_off<BK>(ldb, n0, N, wave, lane, i);
+  }
+  const bf16* abase = (AK ? A + (size_t)m0 * lda : A + m0) +
+                      (size_t)t_first * (AK ? kDK : (size_t)kDK * lda);
+  const bf16* bbase = (BK ? B + (size_t)n0 * ldb : B + n0) +
+                      (size_t)t_first * (BK ? kDK : (size_t)kDK * ldb);
+  const size_t astep = AK ? kDK : (size_t)kDK * lda;  // elements per K-tile
+  const size_t bstep = BK ? kDK : (size_t)kDK * ldb;
+  auto issue = [&](int t) {
+    const int s = t % kStages;
+    const bf16* ab = abase + (size_t)t * astep;
+    const bf16* bb = bbase + (size_t)t * bstep;
+    const uint32_t piece0 = wave * (kPieces * 1024);
+#pragma unroll
+    for (int i = 0; i < kPieces; ++i)
+      dma16s(ab, aoff[i], __builtin_amdgcn_readfirstlane(lds0 + a_off(s) + piece0 + i * 1024));
+#pragma unroll
+    for (int i = 0; i < kPieces; ++i)
+      dma16s(bb, boff[i], __builtin_amdgcn_readfirstlane(lds0 + b_off(s) + piece0 + i * 1024));
+  };
 
   f32x16 acc[kTM][kTN];
 #pragma unroll
@@ -388,40 +435,60 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  if (kt0 < kt1) {
-    dma_tile<AK>(A, lda, m0, M, kt0 * kBK, lds0 + a_off(0), wave, lane);
-    dma_tile<BK>(B, ldb, n0, N, kt0 * kBK, lds0 + b_off(0), wave, lane);
-  }
+  bf16x8 fa0[kTM], fb0[kTN], fa1[kTM], fb1[kTN];
+  auto read_frags = [&](int t, int ks, bf16x8* fa, bf16x8* fb) {
+    const int s = t % kStages;
+    const unsigned char* pa = smem + a_off(s);
+    const unsigned char* pb = smem + b_off(s);
+#pragma unroll
+    for (int i = 0; i < kTM; ++i) fa[i] = dma_frag<AK>(pa, wm + 32 * i + fr, ks, fh, lane);
+#pragma unroll
+    for (int j = 0; j < kTN; ++j) fb[j] = dma_frag<BK>(pb, wn + 32 * j + fr, ks, fh, lane);
+  };
+  // LDS read instructions per k-step (a transposed fragment takes two)
+  constexpr int kReads = (AK ? kTM : 2 * kTM) + (BK ? kTN : 2 * kTN);
+  constexpr int kMfma = kTM * kTN;
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+    for (int i = 0; i < kTM; ++i)
+#pragma unroll
+      for (int j = 0; j < kTN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+    // alternate one MFMA and one LDS read (the next k-step's fragments) so
+    // the reads are in flight early and the matrix pipe stays fed
+    constexpr int pairs = kReads < kMfma ? kReads : kMfma;
+#pragma unroll
+    for (int u = 0; u < pairs; ++u) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if constexpr (kMfma > pairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - pairs, 0);
+    if constexpr (kReads > pairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - pairs, 0);
+  };
 
-  const int fr = lane & 31, fh = lane >> 5;
-  for (int kt = kt0; kt < kt1; ++kt) {
-    const int cur = (kt - kt0) & 1;
-    wait_dma_all();   // this wave's pieces of stage cur have landed
-    block_barrier();  // everyone's have; everyone is done reading stage cur ^ 1
-    if (kt + 1 < kt1) {
-      dma_tile<AK>(A, lda, m0, M, (kt + 1) * kBK, lds0 + a_off(cur ^ 1), wave, lane);
-      dma_tile<BK>(B, ldb, n0, N, (kt + 1) * kBK, lds0 + b_off(cur ^ 1), wave, lane);
-    }
-    const unsigned char* pa = smem + a_off(cur);
-    const unsigned char* pb = smem + b_off(cur);
-    bf16x8 fa[2][kTM], fb[2][kTN];
-    auto read_frags = [&](int ks, int buf) {
 #pragma unroll
-      for (int i = 0; i < kTM; ++i) fa[buf][i] = dma_frag<AK>(pa, wm + 32 * i + fr, ks, fh, lane);
-#pragma unroll
-      for (int j = 0; j < kTN; ++j) fb[buf][j] = dma_frag<BK>(pb, wn + 32 * j + fr, ks, fh, lane);
-    };
-    read_frags(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      const int b = ks & 1;
-      if (ks + 1 < kBK / 16) read_frags(ks + 1, b ^ 1);
-#pragma unroll
-      for (int i = 0; i < kTM; ++i)
-#pragma unroll
-        for (int j = 0; j < kTN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[b][j], fa[b][i], acc[i][j], 0, 0, 0);
-    }
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < nt) issue(t);
+  // tile 0 has landed when at most kStages - 2 newer tiles are in flight
+  if (nt >= kStages - 1) wait_dma<(kStages - 2) * kDmaPerStage>();
+  else wait_dma<0>();
+  block_barrier();
+  read_frags(0, 0, fa0, fb0);
+  for (int t = 0; t < nt; ++t) {
+    // k-step 0 of tile t; the fragments of its k-step 1 are read meanwhile
+    read_frags(t, 1, fa1, fb1);
+    mma(fa0, fb0);
+    // Tile t + 1 has landed for this wave (only tiles t + 2 .. t + kStages - 2
+    // may still be in flight); after the barrier it has for every wave, and
+    // every wave is done with tile t - 1, whose stage the next loads reuse.
+    if (t + kStages - 2 < nt) wait_dma<(kStages - 3) * kDmaPerStage>();
+    else wait_dma<0>();
+    block_barrier();
+    if (t + kStages - 1 < nt) issue(t + kStages - 1);
+    // k-step 1 of tile t; the next tile's first fragments are read meanwhile
+    // (past the last tile this reads a stale stage, never used)
+    read_frags(t + 1, 0, fa0, fb0);
+    mma(fa1, fb1);
   }
 
   if (slice >= 0) {
@@ -527,14 +594,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
+// The DMA path addresses a tile as scalar base + 32-bit lane offset.
+bool dma_offsets_fit(bool ak, int lda, bool bk, int ldb) {
+  auto fits = [](bool kc, int ld) {
+    return (kc ? (long long)kBM : (long long)kDK) * ld * 2 < (1LL << 31);
+  };
+  return fits(ak, lda) && fits(bk, ldb);
+}
+
 template <bool AK, bool BK, Epi EPI, bool GT>
 void gemm_dispatch_layout(Dt dt, const void* A, int lda, const void* B, int ldb, int M, int N,
                           int K, const EpiArgs& ep, float* split_ws, size_t split_ws_floats,
                           hipStream_t s) {
   if (dt == Dt::BF16) {
     const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-    const size_t lds = 4 * (size_t)kTileBytes;
-    if (K % kBK == 0) {
+    const size_t lds = 4 * (size_t)kTileBytes;  // both kernels: 128 KB
+    static_assert(kStages * 2 * kDTile == 4 * kTileBytes, "DMA path LDS");
+    if (K % kBK == 0 && dma_offsets_fit(AK, lda, BK, ldb)) {
       SplitPlan sp = gemm_split_plan(dt, M, N, K);
       if (sp.tail > 0 && (!split_ws || split_ws_floats < gemm_split_floats(sp)))
         sp = SplitPlan{tiles, 0, 1};
