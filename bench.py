@@ -105,7 +105,7 @@ def gemm_steps(s):
 # names: A K-contiguous, B K-contiguous, epilogue (pb::Epi value).
 GEMM_SIGNATURE = {"in_proj": "<true, true, (pb::Epi)1", "out_proj": "<true, true, (pb::Epi)2",
                   "dc": "<true, false, (pb::Epi)3", "dw_out": "<false, false, (pb::Epi)0",
-                  "dh": "<true, false, (pb::Epi)0", "dw_in": "<false, false, (pb::Epi)0"}
+                  "dh": "<true, false, (pb::Epi)4", "dw_in": "<false, false, (pb::Epi)0"}
 
 
 def demangle(name):
@@ -229,7 +229,7 @@ def trace_summary(d, workload):
     rows = []
     for (name, grid), v in groups.items():
         short = re.sub(r"^void ", "", name).replace("pb::(anonymous namespace)::", "")
-        for i, e in enumerate(("StoreF32", "BiasGelu", "BiasResid", "DgeluSplit")):
+        for i, e in enumerate(("StoreF32", "BiasGelu", "BiasResid", "DgeluSplit", "LnGrad")):
             short = short.replace(f"(pb::Epi){i}", e)
         m = re.match(r"_ZN2pb12_GLOBAL__N_1\d+(\w+?)I", short)  # names c++filt leaves
         if m:

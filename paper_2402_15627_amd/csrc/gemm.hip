@@ -32,7 +32,7 @@ namespace {
 // Four consecutive output columns n..n+3 of row m.  GT: tanh form of GeLU.
 template <typename T, Epi EPI, bool GT>
 PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
-  if constexpr (EPI == Epi::StoreF32) {
+  if constexpr (EPI == Epi::StoreF32 || EPI == Epi::LnGrad) {
     store4((float*)ep.out + (size_t)m * ep.ld_out + n, v);
   } else if constexpr (EPI == Epi::BiasGelu) {
     float b[4], z[4];
@@ -64,6 +64,22 @@ PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
       for (int e = 0; e < 4; ++e) o[e] = v[e] * gelu_grad<GT>(u[e]);
       store4((T*)ep.out2 + off, o);
     }
+  }
+}
+
+// LnGrad: the LayerNorm backward's row terms of four columns n..n+3 of row m,
+// added to s1 (sum g) and s2 (sum g xhat), g = gamma dh.
+template <typename T>
+PB_DEV void ln_terms4(const EpiArgs& ep, int m, int n, const float* v, float mu, float rs,
+                      float& s1, float& s2) {
+  float gm[4], xv[4];
+  load4((const T*)ep.bias + n, gm);
+  load4((const T*)ep.aux + (size_t)m * ep.ld_out + n, xv);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float g = gm[e] * v[e];
+    s1 += g;
+    s2 += g * ((xv[e] - mu) * rs);
   }
 }
 
@@ -101,6 +117,52 @@ PB_DEV void tile_of(int lid, int tiles_m, int tiles_n, int& tm, int& tn) {
 }
 PB_DEV void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
   tile_of(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
+}
+
+// Epilogue of one wave's 64 x 128 block of a 256 x 256 tile.  acc[i][j][4 jj +
+// e] is C(m, n) with m = mw + 32 i + (lane & 31), n = nw + 32 j + 8 jj +
+// 4 (lane >> 5) + e.  For LnGrad, lanes l and l ^ 32 together hold all 128
+// columns of a row, 64 per column group j / 2: their row terms are summed
+// across the pair and written once per (row, group).
+template <Epi EPI, bool GT>
+PB_DEV void wave_epilogue(const EpiArgs& ep, const f32x16 (&acc)[kTM][kTN], int mw, int nw,
+                          int M, int N, int fr, int fh) {
+#pragma unroll
+  for (int i = 0; i < kTM; ++i) {
+    const int m = mw + 32 * i + fr;
+    const bool mok = m < M;
+    float s1[kTN / 2], s2[kTN / 2], mu = 0.f, rs = 0.f;
+    if constexpr (EPI == Epi::LnGrad) {
+#pragma unroll
+      for (int h = 0; h < kTN / 2; ++h) s1[h] = s2[h] = 0.f;
+      if (mok) {
+        mu = ep.mean[m];
+        rs = ep.rstd[m];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int n = nw + 32 * j + 8 * jj + 4 * fh;
+        if (mok && n < N) {
+          float v[4] = {acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
+                        acc[i][j][4 * jj + 3]};
+          epi_store4<bf16, EPI, GT>(ep, m, n, v);
+          if constexpr (EPI == Epi::LnGrad) ln_terms4<bf16>(ep, m, n, v, mu, rs, s1[j / 2], s2[j / 2]);
+        }
+      }
+    if constexpr (EPI == Epi::LnGrad) {
+#pragma unroll
+      for (int h = 0; h < kTN / 2; ++h) {
+        s1[h] += __shfl_xor(s1[h], 32, 64);
+        s2[h] += __shfl_xor(s2[h], 32, 64);
+        const int n = nw + 64 * h;  // group start (a multiple of 64)
+        if (fh == 0 && mok && n < N)
+          ep.rowpart[(size_t)m * ep.rowpart_ld + n / 64] = make_float2(s1[h], s2[h]);
+      }
+    }
+  }
 }
 
 // One 256 x 64 operand tile, global -> registers -> LDS.
@@ -256,24 +318,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
     __syncthreads();
   }
 
-  // acc[i][j][4*jj + e] is C(m, n) with m = wm + 32 i + (lane & 31) and
-  // n = wn + 32 j + 8 jj + 4 (lane >> 5) + e.
-#pragma unroll
-  for (int i = 0; i < kTM; ++i) {
-    const int m = m0 + wm + 32 * i + fr;
-    if (m >= M) continue;
-#pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int n = n0 + wn + 32 * j + 8 * jj + 4 * fh;
-        if (n < N) {
-          float v[4] = {acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
-                        acc[i][j][4 * jj + 3]};
-          epi_store4<bf16, EPI, GT>(ep, m, n, v);
-        }
-      }
-  }
+  wave_epilogue<EPI, GT>(ep, acc, m0 + wm, n0 + wn, M, N, fr, fh);
 }
 
 // ------------------------------------------- bf16 MFMA GEMM, LDS-DMA path
@@ -509,22 +554,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     }
     return;
   }
-#pragma unroll
-  for (int i = 0; i < kTM; ++i) {
-    const int m = m0 + wm + 32 * i + fr;
-    if (m >= M) continue;
-#pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int n = n0 + wn + 32 * j + 8 * jj + 4 * fh;
-        if (n < N) {
-          float v[4] = {acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
-                        acc[i][j][4 * jj + 3]};
-          epi_store4<bf16, EPI, GT>(ep, m, n, v);
-        }
-      }
-  }
+  wave_epilogue<EPI, GT>(ep, acc, m0 + wm, n0 + wn, M, N, fr, fh);
 }
 
 // Sum of the K-slice partials of each tail tile, in slice order (so the
@@ -540,12 +570,28 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
   int tm, tn;
   tile_of(n_full + t_local, tiles_m, tiles_n, tm, tn);
   const int m = tm * kBM + row, n = tn * kBN + col;
-  if (m >= M || n >= N) return;
-  const float* p = part + (size_t)t_local * splits * (kBM * kBN) + row * kBN + col;
-  f32x4 sum = *reinterpret_cast<const f32x4*>(p);
-  for (int sl = 1; sl < splits; ++sl) sum += *reinterpret_cast<const f32x4*>(p + (size_t)sl * kBM * kBN);
-  float v[4] = {sum[0], sum[1], sum[2], sum[3]};
-  epi_store4<bf16, EPI, GT>(ep, m, n, v);
+  const bool ok = m < M && n < N;
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (ok) {
+    const float* p = part + (size_t)t_local * splits * (kBM * kBN) + row * kBN + col;
+    f32x4 sum = *reinterpret_cast<const f32x4*>(p);
+    for (int sl = 1; sl < splits; ++sl)
+      sum += *reinterpret_cast<const f32x4*>(p + (size_t)sl * kBM * kBN);
+    v[0] = sum[0], v[1] = sum[1], v[2] = sum[2], v[3] = sum[3];
+    epi_store4<bf16, EPI, GT>(ep, m, n, v);
+  }
+  if constexpr (EPI == Epi::LnGrad) {
+    // a wave is one row of the tile; 16 lanes cover one 64-column group
+    float s1 = 0.f, s2 = 0.f;
+    if (ok) ln_terms4<bf16>(ep, m, n, v, ep.mean[m], ep.rstd[m], s1, s2);
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) {
+      s1 += __shfl_xor(s1, off, 16);
+      s2 += __shfl_xor(s2, off, 16);
+    }
+    if ((threadIdx.x & 15) == 0 && ok)
+      ep.rowpart[(size_t)m * ep.rowpart_ld + n / 64] = make_float2(s1, s2);
+  }
 }
 
 // ----------------------------------------------------------- fp32 SIMT GEMM
@@ -590,7 +636,20 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i, n = n0 + tx * 4;
-    if (m < M && n < N) epi_store4<float, EPI, GT>(ep, m, n, acc[i]);
+    const bool ok = m < M && n < N;
+    if (ok) epi_store4<float, EPI, GT>(ep, m, n, acc[i]);
+    if constexpr (EPI == Epi::LnGrad) {
+      // the 16 lanes tx = 0..15 of a row cover its 64-column group n0 .. n0 + 63
+      float s1 = 0.f, s2 = 0.f;
+      if (ok) ln_terms4<float>(ep, m, n, acc[i], ep.mean[m], ep.rstd[m], s1, s2);
+#pragma unroll
+      for (int off = 8; off > 0; off >>= 1) {
+        s1 += __shfl_xor(s1, off, 16);
+        s2 += __shfl_xor(s2, off, 16);
+      }
+      if (tx == 0 && m < M && n0 < N)
+        ep.rowpart[(size_t)m * ep.rowpart_ld + n0 / 64] = make_float2(s1, s2);
+    }
   }
 }
 
@@ -676,6 +735,9 @@ void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, 
     case Epi::DgeluSplit:
       if (gt) gemm_dispatch<Epi::DgeluSplit, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
       else gemm_dispatch<Epi::DgeluSplit, false>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
+      break;
+    case Epi::LnGrad:
+      gemm_dispatch<Epi::LnGrad, true>(dt, a_kcontig, b_kcontig, A, lda, B, ldb, M, N, K, ep, w, wf, s);
       break;
   }
 }

@@ -15,13 +15,16 @@ enum class Dt { BF16, F32 };
 void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta, void* h,
                        float* mean, float* rstd, int rows, int H, float eps, hipStream_t s);
 // dx = dy + rstd * (g - mean(g) - xhat * mean(g * xhat)), g = gamma * dh, per
-// row; per-block partial column sums of dh * xhat, dh and dy go to
-// part_dgamma, part_dbeta and part_dy [ln_backward_blocks(rows), H].
-int ln_backward_blocks(int rows);
+// row, given the row terms sum g and sum g xhat as 64-column group partials
+// rowpart [rows, ln_row_groups(H)] (written by the dh GEMM's LnGrad
+// epilogue).  Column-parallel: workgroups of 16 rows x 2048 columns; partial
+// column sums of dh * xhat, dh and dy per 16-row chunk go to part_dgamma,
+// part_dbeta and part_dy [ln_backward_chunks(rows), H].
+int ln_backward_chunks(int rows);
 void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
-                        const void* gamma, const float* dh, const void* dy, void* dx,
-                        float* part_dgamma, float* part_dbeta, float* part_dy, int rows, int H,
-                        hipStream_t s);
+                        const void* gamma, const float* dh, const float2* rowpart,
+                        const void* dy, void* dx, float* part_dgamma, float* part_dbeta,
+                        float* part_dy, int rows, int H, hipStream_t s);
 
 // ------------------------------------------------------------ column sums
 // out[c] = sum over r of src[r * ld + c] for a [rows, cols] matrix (cols a
@@ -45,6 +48,10 @@ enum class Epi {
   DgeluSplit,  // n < split: out[m * ld_out + n] = acc;
                // n >= split: with c = n - split + col2,
                //   out2[m * ld_out2 + c] = acc * gelu'(aux[m * ld_out2 + c])
+  LnGrad,      // out_f32[m * ld_out + n] = acc (= dh), and the LayerNorm
+               // backward's row terms per 64-column group g = n / 64:
+               //   rowpart[m * rowpart_ld + g] = (sum gamma dh, sum gamma dh xhat)
+               // with gamma = bias[n], xhat = (aux[m * ld_out + n] - mean[m]) rstd[m]
 };
 struct EpiArgs {
   void* out = nullptr;
@@ -57,7 +64,13 @@ struct EpiArgs {
   int split = 0;
   int col2 = 0;
   int gelu_tanh = 1;
+  const float* mean = nullptr;  // LnGrad only
+  const float* rstd = nullptr;
+  float2* rowpart = nullptr;
+  int rowpart_ld = 0;
 };
+// 64-column groups of the LnGrad row terms for a row of n columns.
+inline int ln_row_groups(int n) { return (n + 63) / 64; }
 // Tail split: the first n_full tiles (a whole number of 256-tile waves) are
 // computed whole; each of the last `tail` tiles is split into `splits`
 // K-slices whose fp32 partial tiles go to a workspace and are summed in slice

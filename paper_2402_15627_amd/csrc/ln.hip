@@ -2,9 +2,11 @@
 // deterministic column sums for the bias and LN-parameter gradients.
 //
 // LN is the shared normalisation of the parallel block (MegaScale Section 3.1,
-// Eq. 2); Section 3.3 fuses its fine-grained kernels into one.  Here one
+// Eq. 2); Section 3.3 fuses its fine-grained kernels into one.  Forward: one
 // workgroup normalises one row held in registers: one HBM read of x, one
-// write of h, statistics from wavefront reductions.
+// write of h, statistics from wavefront reductions.  Backward: the two row
+// reductions it needs are formed by the dh GEMM's epilogue (Epi::LnGrad), so
+// the kernel here is column-parallel and streams x, dh and dy once.
 #include "common.h"
 #include "kernels.h"
 
@@ -84,145 +86,78 @@ __global__ __launch_bounds__(kLnThreads) void ln_fwd_kernel(const T* __restrict_
   }
 }
 
-// Rows are strided over the grid; each workgroup keeps running column sums of
-// dh * xhat, dh and dy in registers and writes them once as a partial row
-// (dy's column sum is db_out, the output bias gradient).  The raw loads of
-// the next row are issued before the current row's reductions, so the
-// memory latency of one row hides behind the arithmetic of the previous.
-template <typename T>
-struct RowRaw;
-template <>
-struct RowRaw<bf16> {
-  u32x4 v;
-  PB_DEV void load(const bf16* p) { v = *reinterpret_cast<const u32x4*>(p); }
-  PB_DEV void get(float* o) const {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { o[2 * i] = lo_bf(v[i]); o[2 * i + 1] = hi_bf(v[i]); }
-  }
-};
-template <>
-struct RowRaw<float> {
-  f32x4 a, b;
-  PB_DEV void load(const float* p) {
-    a = *reinterpret_cast<const f32x4*>(p);
-    b = *reinterpret_cast<const f32x4*>(p + 4);
-  }
-  PB_DEV void get(float* o) const {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { o[i] = a[i]; o[4 + i] = b[i]; }
-  }
-};
+// Column-parallel LayerNorm backward.  The row terms sum gamma dh and
+// sum gamma dh xhat arrive as 64-column group partials from the dh GEMM's
+// epilogue, so no row-wide reduction is left here: each workgroup owns 16
+// rows x 2048 columns, first folds its rows' partials (in a fixed order) into
+// mean(g) and mean(g xhat), then streams x, dh and dy once, writes dx, and
+// keeps the column sums of dh xhat (dgamma), dh (dbeta) and dy (db_out) of
+// its 16 rows in registers, written once as a partial row.
+constexpr int kApplyRows = 16;
+constexpr int kApplyThreads = 256;
+constexpr int kApplyCols = kApplyThreads * 8;
 
-template <typename T, int NV>
-__global__ __launch_bounds__(kLnThreads) void ln_bwd_kernel(
+template <typename T>
+__global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
     const T* __restrict__ x, const float* __restrict__ mean, const float* __restrict__ rstd,
-    const T* __restrict__ gamma, const float* __restrict__ dh, const T* __restrict__ dy,
-    T* __restrict__ dx, float* __restrict__ part_dg, float* __restrict__ part_db,
-    float* __restrict__ part_dy, int rows, int H) {
-  __shared__ float red[2][kLnWaves];
-  float adg[NV][8], adb[NV][8], ady[NV][8];
-  RowRaw<T> graw[NV];  // gamma, kept packed to save registers
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int c = (threadIdx.x + j * kLnThreads) * 8;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) adg[j][e] = adb[j][e] = ady[j][e] = 0.f;
-    if (c < H) graw[j].load(gamma + c);
-  }
-  const float inv_h = 1.0f / (float)H;
-  RowRaw<T> nx[NV], ny[NV];
-  RowRaw<float> nd[NV];
-  auto fetch = [&](int row) {
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int c = (threadIdx.x + j * kLnThreads) * 8;
-      if (c < H) {
-        nx[j].load(x + (size_t)row * H + c);
-        nd[j].load(dh + (size_t)row * H + c);
-        ny[j].load(dy + (size_t)row * H + c);
-      }
-    }
-  };
-  int row = blockIdx.x;
-  if (row < rows) fetch(row);
-  for (; row < rows; row += gridDim.x) {
-    // the current row stays packed; values are unpacked where they are used
-    RowRaw<T> cx[NV], cy[NV];
-    RowRaw<float> cd[NV];
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      cx[j] = nx[j];
-      cd[j] = nd[j];
-      cy[j] = ny[j];
-    }
-    if (row + (int)gridDim.x < rows) fetch(row + gridDim.x);
-    const float mu = mean[row], rs = rstd[row];
+    const T* __restrict__ gamma, const float* __restrict__ dh, const float2* __restrict__ rowpart,
+    int ngroups, const T* __restrict__ dy, T* __restrict__ dx, float* __restrict__ part_dg,
+    float* __restrict__ part_db, float* __restrict__ part_dy, int rows, int H) {
+  __shared__ float stat[kApplyRows][2];
+  const int ncb = (H + kApplyCols - 1) / kApplyCols;
+  const int cb = (int)blockIdx.x % ncb, chunk = (int)blockIdx.x / ncb;
+  const int r0 = chunk * kApplyRows;
+  const int nr = min(kApplyRows, rows - r0);
+  {
+    // 16 threads per row, each summing every 16th group, then a butterfly
+    const int rr = threadIdx.x >> 4, l = threadIdx.x & 15;
     float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int c = (threadIdx.x + j * kLnThreads) * 8;
-      if (c < H) {
-        float xv[8], d[8], r[8], gm[8];
-        cx[j].get(xv);
-        cd[j].get(d);
-        cy[j].get(r);
-        graw[j].get(gm);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float xh = (xv[e] - mu) * rs;
-          adg[j][e] += d[e] * xh;
-          adb[j][e] += d[e];
-          ady[j][e] += r[e];
-          const float g = gm[e] * d[e];
-          s1 += g;
-          s2 += g * xh;
-        }
+    if (rr < nr)
+      for (int g = l; g < ngroups; g += 16) {
+        const float2 p = rowpart[(size_t)(r0 + rr) * ngroups + g];
+        s1 += p.x;
+        s2 += p.y;
       }
-    }
-    s1 = wave_sum(s1);
-    s2 = wave_sum(s2);
-    const int w = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-      red[0][w] = s1;
-      red[1][w] = s2;
-    }
-    __syncthreads();
-    float t1 = 0.f, t2 = 0.f;
 #pragma unroll
-    for (int i = 0; i < kLnWaves; ++i) {
-      t1 += red[0][i];
-      t2 += red[1][i];
+    for (int off = 8; off > 0; off >>= 1) {
+      s1 += __shfl_xor(s1, off, 16);
+      s2 += __shfl_xor(s2, off, 16);
     }
-    __syncthreads();
-    const float m1 = t1 * inv_h, m2 = t2 * inv_h;
-    T* dxr = dx + (size_t)row * H;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int c = (threadIdx.x + j * kLnThreads) * 8;
-      if (c < H) {
-        float xv[8], d[8], r[8], gm[8], o[8];
-        cx[j].get(xv);
-        cd[j].get(d);
-        cy[j].get(r);
-        graw[j].get(gm);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float xh = (xv[e] - mu) * rs;
-          o[e] = r[e] + rs * (gm[e] * d[e] - m1 - xh * m2);
-        }
-        store8(dxr + c, o);
-      }
+    if (l == 0) {
+      stat[rr][0] = s1 / (float)H;
+      stat[rr][1] = s2 / (float)H;
     }
   }
+  __syncthreads();
+  const int c = (cb * kApplyThreads + threadIdx.x) * 8;
+  if (c >= H) return;
+  float gm[8], adg[8], adb[8], ady[8];
+  load8(gamma + c, gm);
 #pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int c = (threadIdx.x + j * kLnThreads) * 8;
-    if (c < H) {
-      store8(part_dg + (size_t)blockIdx.x * H + c, adg[j]);
-      store8(part_db + (size_t)blockIdx.x * H + c, adb[j]);
-      store8(part_dy + (size_t)blockIdx.x * H + c, ady[j]);
+  for (int e = 0; e < 8; ++e) adg[e] = adb[e] = ady[e] = 0.f;
+#pragma unroll 2
+  for (int rr = 0; rr < nr; ++rr) {
+    const size_t off = (size_t)(r0 + rr) * H + c;
+    float xv[8], d[8], yv[8], o[8];
+    load8(x + off, xv);
+    load8(dh + off, d);
+    load8(dy + off, yv);
+    const float mu = mean[r0 + rr], rs = rstd[r0 + rr];
+    const float m1 = stat[rr][0], m2 = stat[rr][1];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float xh = (xv[e] - mu) * rs;
+      adg[e] += d[e] * xh;
+      adb[e] += d[e];
+      ady[e] += yv[e];
+      o[e] = yv[e] + rs * (gm[e] * d[e] - m1 - xh * m2);
     }
+    store8(dx + off, o);
   }
+  const size_t prow = (size_t)chunk * H + c;
+  store8(part_dg + prow, adg);
+  store8(part_db + prow, adb);
+  store8(part_dy + prow, ady);
 }
 
 // ------------------------------------------------------------ column sums
@@ -294,15 +229,6 @@ void ln_fwd_nv(const void* x, const void* gamma, const void* beta, void* h, floa
                                                    (const T*)beta, (T*)h, mean, rstd, H, eps);
 }
 
-template <typename T, int NV>
-void ln_bwd_nv(const void* x, const float* mean, const float* rstd, const void* gamma,
-               const float* dh, const void* dy, void* dx, float* pdg, float* pdb, float* pdy,
-               int rows, int H, hipStream_t s) {
-  ln_bwd_kernel<T, NV><<<ln_backward_blocks(rows), kLnThreads, 0, s>>>(
-      (const T*)x, mean, rstd, (const T*)gamma, dh, (const T*)dy, (T*)dx, pdg, pdb, pdy, rows,
-      H);
-}
-
 template <typename T>
 void ln_fwd_t(const void* x, const void* gamma, const void* beta, void* h, float* mean,
               float* rstd, int rows, int H, float eps, hipStream_t s) {
@@ -319,26 +245,7 @@ void ln_fwd_t(const void* x, const void* gamma, const void* beta, void* h, float
   }
 }
 
-template <typename T>
-void ln_bwd_t(const void* x, const float* mean, const float* rstd, const void* gamma,
-              const float* dh, const void* dy, void* dx, float* pdg, float* pdb, float* pdy,
-              int rows, int H, hipStream_t s) {
-  const int nv = (H + kLnThreads * 8 - 1) / (kLnThreads * 8);
-  switch (nv) {
-    case 1: ln_bwd_nv<T, 1>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    case 2: ln_bwd_nv<T, 2>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    case 3: ln_bwd_nv<T, 3>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    case 4: ln_bwd_nv<T, 4>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    case 5: ln_bwd_nv<T, 5>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    case 6: ln_bwd_nv<T, 6>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    case 7: ln_bwd_nv<T, 7>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-    default: ln_bwd_nv<T, 8>(x, mean, rstd, gamma, dh, dy, dx, pdg, pdb, pdy, rows, H, s); break;
-  }
-}
-
 }  // namespace
-
-int ln_backward_blocks(int rows) { return rows < 256 ? rows : 256; }
 
 void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta, void* h,
                        float* mean, float* rstd, int rows, int H, float eps, hipStream_t s) {
@@ -348,16 +255,22 @@ void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta
     ln_fwd_t<float>(x, gamma, beta, h, mean, rstd, rows, H, eps, s);
 }
 
+int ln_backward_chunks(int rows) { return (rows + kApplyRows - 1) / kApplyRows; }
+
 void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
-                        const void* gamma, const float* dh, const void* dy, void* dx,
-                        float* part_dgamma, float* part_dbeta, float* part_dy, int rows, int H,
-                        hipStream_t s) {
+                        const void* gamma, const float* dh, const float2* rowpart,
+                        const void* dy, void* dx, float* part_dgamma, float* part_dbeta,
+                        float* part_dy, int rows, int H, hipStream_t s) {
+  const unsigned grid = (unsigned)((H + kApplyCols - 1) / kApplyCols) * ln_backward_chunks(rows);
+  const int ng = ln_row_groups(H);
   if (dt == Dt::BF16)
-    ln_bwd_t<bf16>(x, mean, rstd, gamma, dh, dy, dx, part_dgamma, part_dbeta, part_dy, rows, H,
-                   s);
+    ln_bwd_apply<bf16><<<grid, kApplyThreads, 0, s>>>(
+        (const bf16*)x, mean, rstd, (const bf16*)gamma, dh, rowpart, ng, (const bf16*)dy,
+        (bf16*)dx, part_dgamma, part_dbeta, part_dy, rows, H);
   else
-    ln_bwd_t<float>(x, mean, rstd, gamma, dh, dy, dx, part_dgamma, part_dbeta, part_dy, rows,
-                    H, s);
+    ln_bwd_apply<float><<<grid, kApplyThreads, 0, s>>>(
+        (const float*)x, mean, rstd, (const float*)gamma, dh, rowpart, ng, (const float*)dy,
+        (float*)dx, part_dgamma, part_dbeta, part_dy, rows, H);
 }
 
 size_t colsum_partial_floats(int rows, int cols) {

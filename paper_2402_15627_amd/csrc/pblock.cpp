@@ -144,7 +144,7 @@ size_t split_bytes_bwd(const Dims& d, pb::Dt dt) {
 }
 
 struct BwdLayout {
-  size_t d_o, dz, dh, delta, pdg, pdb, pdy, part, split, base, total;
+  size_t d_o, dz, dh, delta, rowpart, pdg, pdb, pdy, part, split, base, total;
 };
 BwdLayout bwd_layout(const Dims& d) {
   BwdLayout L;
@@ -154,11 +154,12 @@ BwdLayout bwd_layout(const Dims& d) {
     o = align256(o + bytes);
     return at;
   };
-  const int nblk = pb::ln_backward_blocks((int)d.T);
+  const int nblk = pb::ln_backward_chunks((int)d.T);
   L.d_o = take((size_t)(d.T * d.A) * d.esz);
   L.dz = take((size_t)(d.T * d.N_in) * d.esz);
   L.dh = take((size_t)(d.T * d.H) * 4);
   L.delta = take((size_t)(d.B * d.heads * d.S) * 4);
+  L.rowpart = take((size_t)d.T * pb::ln_row_groups((int)d.H) * sizeof(float2));
   L.pdg = take((size_t)nblk * d.H * 4);
   L.pdb = take((size_t)nblk * d.H * 4);
   L.pdy = take((size_t)nblk * d.H * 4);
@@ -388,6 +389,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   void* dz = wb + W.dz;
   float* dh = (float*)(wb + W.dh);
   float* delta = (float*)(wb + W.delta);
+  float2* rowpart = (float2*)(wb + W.rowpart);
   float* pdg = (float*)(wb + W.pdg);
   float* pdb = (float*)(wb + W.pdb);
   float* pdy = (float*)(wb + W.pdy);
@@ -398,6 +400,11 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   (void)ln_beta;
   (void)b_in;
   (void)b_out;
+
+  // Order: the chain dC -> attention -> dh -> LayerNorm runs first, each step
+  // reading what the previous one just wrote while it is still in the
+  // last-level cache; the two weight-gradient GEMMs, which write ~4 bytes
+  // per weight, come last so their write-back does not compete with it.
 
   // B1: dC = dy W_out; dO = dC[:, :A]; dU = dC[:, A:] * gelu'(U) -> dZ[:, 3A:]
   pb::EpiArgs e1;
@@ -414,7 +421,49 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
                     split_ws, split_f, stream);
   }
-  // B2: dW_out = dy^T C (contraction over tokens); db_out = sum_t dy
+  // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
+  {
+    StepScope sc(PB_STEP_ATTN_BWD, stream);
+    pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
+                             K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
+                             N_in, split_ws, split_f * 4, stream);
+  }
+  // B4: dh = dZ W_in (fp32); its epilogue also forms the LayerNorm
+  // backward's row terms (sums of gamma dh and gamma dh xhat per 64 columns)
+  pb::EpiArgs e4;
+  e4.out = dh;
+  e4.ld_out = H;
+  e4.aux = x;
+  e4.bias = ln_gamma;
+  e4.mean = mean;
+  e4.rstd = rstd;
+  e4.rowpart = rowpart;
+  e4.rowpart_ld = pb::ln_row_groups(H);
+  {
+    StepScope sc(PB_STEP_DH, stream);
+    pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
+                    split_ws, split_f, stream);
+  }
+  // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
+  {
+    StepScope sc(PB_STEP_LN_BWD, stream);
+    pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, rowpart, dy, dx, pdg, pdb, pdy, T, H,
+                           stream);
+    const int nblk = pb::ln_backward_chunks(T);
+    pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
+    pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
+  }
+  {
+    // db_out = sum over tokens of dy, from the LN backward's partial sums
+    StepScope sc(PB_STEP_DB_OUT, stream);
+    pb::launch_colsum_f32(pdy, H, pb::ln_backward_chunks(T), H, part, db_out, stream);
+  }
+  // db_in = sum over tokens of dZ
+  {
+    StepScope sc(PB_STEP_DB_IN, stream);
+    pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+  }
+  // B2: dW_out = dy^T C (contraction over tokens)
   pb::EpiArgs e2;
   e2.out = dw_out;
   e2.ld_out = K_out;
@@ -423,24 +472,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
                     split_ws, split_f, stream);
   }
-
-  // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
-  {
-    StepScope sc(PB_STEP_ATTN_BWD, stream);
-    pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
-                             K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
-                             N_in, split_ws, split_f * 4, stream);
-  }
-  // B4: dh = dZ W_in (fp32)
-  pb::EpiArgs e4;
-  e4.out = dh;
-  e4.ld_out = H;
-  {
-    StepScope sc(PB_STEP_DH, stream);
-    pb::launch_gemm(dt, pb::Epi::StoreF32, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
-                    split_ws, split_f, stream);
-  }
-  // B5: dW_in = dZ^T h; db_in = sum_t dZ
+  // B5: dW_in = dZ^T h
   pb::EpiArgs e5;
   e5.out = dw_in;
   e5.ld_out = H;
@@ -448,23 +480,6 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     StepScope sc(PB_STEP_DW_IN, stream);
     pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5,
                     split_ws, split_f, stream);
-  }
-  {
-    StepScope sc(PB_STEP_DB_IN, stream);
-    pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
-  }
-  // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
-  {
-    StepScope sc(PB_STEP_LN_BWD, stream);
-    pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, dy, dx, pdg, pdb, pdy, T, H, stream);
-    const int nblk = pb::ln_backward_blocks(T);
-    pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
-    pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
-  }
-  {
-    // db_out = sum over tokens of dy, from the LN backward's partial sums
-    StepScope sc(PB_STEP_DB_OUT, stream);
-    pb::launch_colsum_f32(pdy, H, pb::ln_backward_blocks(T), H, part, db_out, stream);
   }
   return finish_launches();
 }

@@ -40,7 +40,7 @@ def test_gemm_steps_are_told_apart():
     name = "void pb::(anonymous namespace)::gemm_bf16_dma_kernel<true, true, (pb::Epi)2, true>()"
     g = bench.gemm_grid_threads(*bench.gemm_steps(s)["out_proj"])
     assert bench.gemm_step_of(name, g, s) == "out_proj"
-    dh = name.replace("<true, true, (pb::Epi)2", "<true, false, (pb::Epi)0")
+    dh = name.replace("<true, true, (pb::Epi)2", "<true, false, (pb::Epi)4")
     assert bench.gemm_step_of(dh, g, s) == "dh"   # same grid, other template
     assert bench.gemm_step_of(name, g + 512, s) == ""
 
