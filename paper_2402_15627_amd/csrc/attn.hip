@@ -41,6 +41,7 @@ constexpr int kWavesQ = 4;
 constexpr int kWavesK = 4;  // two key groups of 32, each with a P wave and a dS wave
 constexpr int kTL = 64;      // forward and dQ key tiles
 constexpr int kTLdkv = 32;   // dK/dV query tiles (keeps its registers and LDS in budget)
+constexpr int kStagesDkdv = 4;  // dK/dV LDS stages: tile loads run three tiles ahead
 constexpr int kBlockQ = 32 * kWavesQ;  // queries per forward / dQ workgroup
 constexpr int kBlockK = 64;            // keys per dK/dV workgroup
 constexpr int kUnsplit = 1 << 30;
@@ -82,7 +83,24 @@ PB_DEV void dma16(const void* g, uint32_t lds_byte_addr) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_byte_addr)
                : "memory", "m0");
 }
+PB_DEV void dma4(const void* g, uint32_t lds_byte_addr) {  // lane l's 4 bytes -> base + 4 l
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_byte_addr)
+               : "memory", "m0");
+}
 PB_DEV void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most n DMA instructions of this wave are still in flight
+// (n uniform; values above 15 wait for all).
+PB_DEV void wait_dma_upto(int n) {
+#define PB_VMCNT_CASE(k) \
+  case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+  switch (n) {
+    PB_VMCNT_CASE(1) PB_VMCNT_CASE(2) PB_VMCNT_CASE(3) PB_VMCNT_CASE(4) PB_VMCNT_CASE(5)
+    PB_VMCNT_CASE(6) PB_VMCNT_CASE(7) PB_VMCNT_CASE(8) PB_VMCNT_CASE(9) PB_VMCNT_CASE(10)
+    PB_VMCNT_CASE(11) PB_VMCNT_CASE(12) PB_VMCNT_CASE(13) PB_VMCNT_CASE(14) PB_VMCNT_CASE(15)
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+#undef PB_VMCNT_CASE
+}
 PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // This wave's share of a natural tile, rows row0 .. row0 + kTL - 1 of a
@@ -432,8 +450,9 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   constexpr int TL = kTLdkv;
   constexpr int NB = kBlockK;
   constexpr int TB = TL * 2 * D;
-  constexpr int STAGE = 2 * TB + 2 * TL * 4;  // Q, dO, then lse*log2e and delta
+  constexpr int STAGE = 2 * TB + 2 * TL * 4;  // Q, dO, then lse and delta rows
   constexpr int PBUF = 64 * 16 * 4;           // one wave's P: 16 fp32 per lane
+  constexpr int NS = kStagesDkdv;             // tiles in flight: loads run NS - 1 ahead
   static_assert(TL == 32 && NB == 64 && kWavesK == 4, "two key groups x two roles");
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
@@ -459,7 +478,7 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   const bf16* gb = dO + tok0 * ld_o + head * D;
   const float* lseb = lse + ((size_t)b * H + head) * S;
   const float* delb = delta + ((size_t)b * H + head) * S;
-  float* pbuf = (float*)(smem + 2 * STAGE + grp * PBUF);
+  float* pbuf = (float*)(smem + NS * STAGE + grp * PBUF);
 
   const int kw0 = k0 + 32 * grp;
   const int key = kw0 + fr;
@@ -475,25 +494,35 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
 
   const float c2 = scale * kLog2e;
 
-  float rl = 0.f;
-  auto issue_stage = [&](int qs, int s) {
+  // Stage of the i-th tile of this chunk: Q and dO tiles, and the tile's 32
+  // lse and 32 delta values (one 4-byte DMA by wave 0; rows past the end are
+  // read from the last row: finite values that the mask always zeroes).
+  // DMA instructions per wave per stage: dma_tile moves 1 KB pieces.
+  constexpr int kPiecesQ = TB / kWavesK / 1024;
+  const int per_stage = 2 * kPiecesQ + (wave == 0 ? 1 : 0);
+  const int nt = t_end - t_begin;
+  auto issue_stage = [&](int i) {
+    const int s = i % NS;
+    const int qs = k0 + (t_begin + i) * TL;
     dma_tile<D, TL, kWavesK>(qb, ld, qs, S, lds0 + q_off(s), wave, lane);
     dma_tile<D, TL, kWavesK>(gb, ld_o, qs, S, lds0 + g_off(s), wave, lane);
-    if (tid < TL) rl = qs + tid < S ? lseb[qs + tid] * kLog2e : __builtin_huge_valf();
-    else if (tid < 2 * TL) rl = qs + tid - TL < S ? delb[qs + tid - TL] : 0.f;
+    if (wave == 0) {
+      const int r = min(qs + (lane & 31), S - 1);
+      dma4((lane < 32 ? lseb : delb) + r, __builtin_amdgcn_readfirstlane(lds0 + l_off(s)));
+    }
   };
-  auto finish_stage = [&](int s) {
-    if (tid < 2 * TL) ((float*)(smem + l_off(s)))[tid] = rl;
-  };
-  issue_stage(k0 + t_begin * TL, 0);
-  finish_stage(0);
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < nt) issue_stage(i);
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const int cur = (t - t_begin) & 1;
+  for (int i = 0; i < nt; ++i) {
+    const int t = t_begin + i;
+    const int cur = i % NS;
     const int qs = k0 + t * TL;
-    wait_dma_all();
-    block_barrier();
-    if (t + 1 < t_end) issue_stage(qs + TL, cur ^ 1);
+    // stage i has landed once at most the newer stages' loads are in flight
+    wait_dma_upto(min(nt - 1 - i, NS - 2) * per_stage);
+    block_barrier();  // ... for every wave; and every wave is done with tile i - 1
+    if (i + NS - 1 < nt) issue_stage(i + NS - 1);
     const unsigned char* qt = smem + q_off(cur);
     const unsigned char* gt = smem + g_off(cur);
     const float* ls = (const float*)(smem + l_off(cur));
@@ -522,7 +551,8 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
       for (int j = 0; j < 4; ++j) {
         const f32x4 L4 = *reinterpret_cast<const f32x4*>(ls + 8 * j + 4 * fh);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sc[4 * j + i] = exp2_hw(fmaf(sc[4 * j + i], c2, -L4[i]));
+        for (int i = 0; i < 4; ++i)
+          sc[4 * j + i] = exp2_hw(fmaf(sc[4 * j + i], c2, -L4[i] * kLog2e));
         *reinterpret_cast<f32x4*>(pbuf + (j * 64 + lane) * 4) =
             f32x4{sc[4 * j], sc[4 * j + 1], sc[4 * j + 2], sc[4 * j + 3]};
       }
@@ -544,7 +574,6 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
       for (int s2 = 0; s2 < TL / 16; ++s2)
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             frag_tr<D>(tt, 32 * db + fr, s2, fh, lane), probs_frag(&sc, s2), acc[db], 0, 0, 0);
-    if (t + 1 < t_end) finish_stage(cur ^ 1);
   }
 
   if (key < S) {
@@ -820,7 +849,9 @@ __global__ __launch_bounds__(64) void attn_dkdv_f32(const float* __restrict__ Q,
 template <int D>
 size_t fwd_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 template <int D>
-size_t dkdv_lds() { return 2 * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4) + 2 * 64 * 16 * 4; }
+size_t dkdv_lds() {
+  return kStagesDkdv * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4) + 2 * 64 * 16 * 4;
+}
 template <int D>
 size_t dq_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
 
