@@ -4,8 +4,9 @@
 // workgroup of eight waves (each wave 64x128).  Two kernels share the tile,
 // the wave layout and the epilogues:
 //   - K a multiple of 64 (every GEMM of the block at the benchmarked sizes):
-//     operands reach LDS by LDS-DMA, K-tiles of 32 through four stages, the
-//     barrier placed mid-tile (see the DMA kernel below);
+//     operands reach LDS by LDS-DMA, K-tiles of 64 through two stages,
+//     fragments read two k-steps ahead and the barrier placed mid-tile (see
+//     the DMA kernel below);
 //   - otherwise (ragged token counts in the weight-gradient GEMMs): K-tile
 //     64, double-buffered LDS, loads staged through registers with zero fill;
 //     an M- or N-contiguous operand is loaded as 8x8 blocks and transposed in
@@ -325,33 +326,35 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
 // Used when K is a multiple of 64.  The operand tiles go from global memory
 // straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
 // LDS base + 16 * lane), so there is no register staging and no LDS write
-// instruction.  The loop runs over K-tiles of 32 through four LDS stages
-// (4 x 32 KB): a tile's loads are issued two tiles ahead of its use, which
-// covers their latency.  The one workgroup barrier of each K-tile sits
-// between its two k-steps, so the first k-step's MFMAs are still executing
-// while the waves synchronise, and the next tile's first fragments are read
-// before the tile boundary: the matrix pipe does not drain at the barrier.
+// instruction.  K-tiles of 64 (a K-contiguous row then spans whole 128-byte
+// lines) through two LDS stages (2 x 64 KB).  Each wave keeps the MFMA
+// fragments of four k-steps in registers and reads them two k-steps ahead,
+// so a tile's last reads are issued before its second k-step's MFMAs; the one
+// workgroup barrier of the K-tile sits there.  After it the tile's stage is
+// free for the loads of tile t + 2 and tile t + 1 is visible, whose first
+// fragments are read while k-steps 2 and 3 multiply: the matrix pipe keeps
+// running through the barrier and the loads have a whole tile to land.
 //
-// A K-contiguous operand is stored K-major (64-byte rows, the 16-byte chunk
-// index XOR-ed by (row / 4) mod 4); an MN-contiguous operand is stored
-// MN-major, 32 k-rows of 512 bytes with the chunk index XOR-ed by
-// 4 (k mod 4), and its MFMA fragments are read with ds_read_b64_tr_b16, which
-// transposes 4 (k) x 16 (mn) blocks across a 16-lane group.  Both patterns
-// are free of bank conflicts.  The DMA instructions are issued from inline
-// assembly as scalar base + per-lane offset (no per-load address arithmetic)
-// and waited for explicitly, so the compiler adds no conservative waits
-// between them and the LDS reads of other stages.
+// A K-contiguous operand is stored K-major (128-byte rows, the 16-byte chunk
+// index XOR-swizzled by the row); an MN-contiguous operand is stored MN-major,
+// 64 k-rows of 512 bytes with the chunk index XOR-ed by 4 (k mod 4), and its
+// MFMA fragments are read with ds_read_b64_tr_b16, which transposes 4 (k) x
+// 16 (mn) blocks across a 16-lane group.  Both patterns are free of bank
+// conflicts.  The DMA instructions are issued from inline assembly as scalar
+// base + per-lane offset (no per-load address arithmetic) and waited for
+// explicitly, so the compiler adds no conservative waits between them and the
+// LDS reads of the other stage.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 #define PB_LDS __attribute__((address_space(3)))
 
-constexpr int kDK = 32;                     // K-tile of the DMA path
-constexpr int kStages = 4;
+constexpr int kDK = 64;                     // K-tile of the DMA path
+constexpr int kStages = 2;
 constexpr int kDTile = kBM * kDK * 2;       // one operand tile: 16 KB
-constexpr int kPieces = kDTile / kThreads / 16;  // 1 KB DMA pieces per operand per wave: 2
+constexpr int kPieces = kDTile / kThreads / 16;  // 1 KB DMA pieces per operand per wave: 4
 constexpr int kDmaPerStage = 2 * kPieces;   // DMA instructions per wave per stage
 static_assert(kBM == kBN && kPieces * 1024 * (kThreads / 64) == kDTile, "tile split over waves");
+static_assert(kDK == kBK, "the DMA path's K-tile is the planning unit");
 
-PB_DEV int swz_k(int row, int c) { return c ^ ((row >> 2) & 3); }
 PB_DEV int swz_mn(int krow, int c) { return c ^ (4 * (krow & 3)); }
 
 PB_DEV void dma16s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
@@ -372,7 +375,7 @@ template <bool KC>
 PB_DEV uint32_t dma_lane_off(int ld, int R0, int Rmax, int wave, int lane, int i) {
   const int p = wave * (kPieces * 1024) + i * 1024 + 16 * lane;
   if constexpr (KC) {
-    const int row = p >> 6, c = swz_k(row, (p >> 4) & 3);
+    const int row = p >> 7, c = swz(row, (p >> 4) & 7);
     const int r = min(R0 + row, Rmax - 1) - R0;
     return (uint32_t)(r * ld + 8 * c) * 2u;
   } else {
@@ -386,7 +389,7 @@ PB_DEV uint32_t dma_lane_off(int ld, int R0, int Rmax, int wave, int lane, int i
 template <bool KC>
 PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, int lane) {
   if constexpr (KC) {
-    return *reinterpret_cast<const bf16x8*>(lds_tile + row * 64 + swz_k(row, 2 * ks + h) * 16);
+    return *reinterpret_cast<const bf16x8*>(lds_tile + row * 128 + swz(row, 2 * ks + h) * 16);
   } else {
     // lane 4 j + q of a 16-lane group reads k-row kb + j, mn (row & ~15) + 4 q;
     // the transposing read hands lane i the four k values of mn (row & ~15) + i
@@ -444,19 +447,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
   const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
   const int fr = lane & 31, fh = lane >> 5;
 
-  // 32-wide K-tiles [t_first, t_first + nt) of this work item
-  const int t_first = kDK == kBK ? kt0 : kt0 * (kBK / kDK);
-  const int nt = (kt1 - kt0) * (kBK / kDK);
+  // K-tiles [kt0, kt1) of this work item
+  const int nt = kt1 - kt0;
   uint32_t aoff[kPieces], boff[kPieces];
 #pragma unroll
   for (int i = 0; i < kPieces; ++i) {
     aoff[i] = dma_lane_off<AK>(lda, m0, M, wave, lane, i);
     boff[i] = dma_lane_off<BK>(ldb, n0, N, wave, lane, i);
   }
-  const bf16* abase = (AK ? A + (size_t)m0 * lda : A + m0) +
-                      (size_t)t_first * (AK ? kDK : (size_t)kDK * lda);
-  const bf16* bbase = (BK ? B + (size_t)n0 * ldb : B + n0) +
-                      (size_t)t_first * (BK ? kDK : (size_t)kDK * ldb);
+  const bf16* abase = (AK ? A + (size_t)m0 * lda : A + m0) + (size_t)kt0 * (AK ? kDK : (size_t)kDK * lda);
+  const bf16* bbase = (BK ? B + (size_t)n0 * ldb : B + n0) + (size_t)kt0 * (BK ? kDK : (size_t)kDK * ldb);
   const size_t astep = AK ? kDK : (size_t)kDK * lda;  // elements per K-tile
   const size_t bstep = BK ? kDK : (size_t)kDK * ldb;
   auto issue = [&](int t) {
@@ -480,26 +480,28 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  bf16x8 fa0[kTM], fb0[kTN], fa1[kTM], fb1[kTN];
-  auto read_frags = [&](int t, int ks, bf16x8* fa, bf16x8* fb) {
+  constexpr int kSteps = kDK / 16;  // k-steps per K-tile: 4
+  bf16x8 fa[kSteps][kTM], fb[kSteps][kTN];
+  auto read_frags = [&](int t, int ks) {
     const int s = t % kStages;
     const unsigned char* pa = smem + a_off(s);
     const unsigned char* pb = smem + b_off(s);
 #pragma unroll
-    for (int i = 0; i < kTM; ++i) fa[i] = dma_frag<AK>(pa, wm + 32 * i + fr, ks, fh, lane);
+    for (int i = 0; i < kTM; ++i) fa[ks][i] = dma_frag<AK>(pa, wm + 32 * i + fr, ks, fh, lane);
 #pragma unroll
-    for (int j = 0; j < kTN; ++j) fb[j] = dma_frag<BK>(pb, wn + 32 * j + fr, ks, fh, lane);
+    for (int j = 0; j < kTN; ++j) fb[ks][j] = dma_frag<BK>(pb, wn + 32 * j + fr, ks, fh, lane);
   };
   // LDS read instructions per k-step (a transposed fragment takes two)
   constexpr int kReads = (AK ? kTM : 2 * kTM) + (BK ? kTN : 2 * kTN);
   constexpr int kMfma = kTM * kTN;
-  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+  auto mma = [&](int ks) {
 #pragma unroll
     for (int i = 0; i < kTM; ++i)
 #pragma unroll
       for (int j = 0; j < kTN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
-    // alternate one MFMA and one LDS read (the next k-step's fragments) so
+        acc[i][j] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+    // alternate one MFMA and one LDS read (fragments two k-steps ahead) so
     // the reads are in flight early and the matrix pipe stays fed
     constexpr int pairs = kReads < kMfma ? kReads : kMfma;
 #pragma unroll
@@ -511,29 +513,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     if constexpr (kReads > pairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - pairs, 0);
   };
 
-#pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
-    if (t < nt) issue(t);
-  // tile 0 has landed when at most kStages - 2 newer tiles are in flight
-  if (nt >= kStages - 1) wait_dma<(kStages - 2) * kDmaPerStage>();
+  if (nt > 0) issue(0);
+  if (nt > 1) issue(1);
+  if (nt > 1) wait_dma<kDmaPerStage>();  // tile 0 landed; tile 1 may be in flight
   else wait_dma<0>();
   block_barrier();
-  read_frags(0, 0, fa0, fb0);
+  read_frags(0, 0);
+  read_frags(0, 1);
   for (int t = 0; t < nt; ++t) {
-    // k-step 0 of tile t; the fragments of its k-step 1 are read meanwhile
-    read_frags(t, 1, fa1, fb1);
-    mma(fa0, fb0);
-    // Tile t + 1 has landed for this wave (only tiles t + 2 .. t + kStages - 2
-    // may still be in flight); after the barrier it has for every wave, and
-    // every wave is done with tile t - 1, whose stage the next loads reuse.
-    if (t + kStages - 2 < nt) wait_dma<(kStages - 3) * kDmaPerStage>();
-    else wait_dma<0>();
+    read_frags(t, 2);
+    mma(0);
+    read_frags(t, 3);
+    mma(1);
+    // Every wave has issued (and with the barrier, finished) its reads of
+    // tile t, so its stage can take tile t + 2; tile t + 1 has landed for
+    // this wave, and after the barrier for all.
+    wait_dma<0>();
     block_barrier();
-    if (t + kStages - 1 < nt) issue(t + kStages - 1);
-    // k-step 1 of tile t; the next tile's first fragments are read meanwhile
-    // (past the last tile this reads a stale stage, never used)
-    read_frags(t + 1, 0, fa0, fb0);
-    mma(fa1, fb1);
+    if (t + 2 < nt) issue(t + 2);
+    // the next tile's first fragments (past the last tile: a stale stage, unused)
+    read_frags(t + 1, 0);
+    mma(2);
+    read_frags(t + 1, 1);
+    mma(3);
   }
 
   if (slice >= 0) {
