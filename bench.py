@@ -247,8 +247,9 @@ def trace_summary(d, workload):
     return "\n".join(out)
 
 
-def cpu_baseline(shape, inputs):
-    """Time the fp64 oracle (as it stands) on one full forward + backward step."""
+def cpu_baseline(shape, inputs, min_seconds=10.0, max_steps=6):
+    """Time the fp64 oracle (as it stands) on whole forward + backward steps of
+    the same workload, repeated until at least min_seconds have elapsed."""
     import numpy as np  # noqa: F401
     from oracle import pblock_oracle as orc
     from paper_2402_15627_amd.inputs import model_flops
@@ -258,13 +259,17 @@ def cpu_baseline(shape, inputs):
     except Exception:  # threadpoolctl missing: report the host's CPU count
         threads = os.cpu_count()
     cfg = orc.config_from_shape(shape)
-    t0 = time.perf_counter()
-    orc.run_block(cfg, inputs)
-    dt = time.perf_counter() - t0
-    return {"value": model_flops(shape) / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        orc.run_block(cfg, inputs)
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds or steps >= max_steps:
+            break
+    return {"value": model_flops(shape) * steps / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "seconds": round(dt, 2),
-            "sample": f"one full forward+backward step of {shape.name} (fp64 numpy, "
-                      f"BLAS matmul), same seeded inputs as the GPU run"}
+            "sample": f"{steps} full forward+backward steps of {shape.name} (fp64 numpy, BLAS "
+                      f"matmul), same seeded inputs as the GPU run"}
 
 
 def main():
