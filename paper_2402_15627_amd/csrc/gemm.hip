@@ -459,17 +459,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
   const bf16* bbase = (BK ? B + (size_t)n0 * ldb : B + n0) + (size_t)kt0 * (BK ? kDK : (size_t)kDK * ldb);
   const size_t astep = AK ? kDK : (size_t)kDK * lda;  // elements per K-tile
   const size_t bstep = BK ? kDK : (size_t)kDK * ldb;
-  auto issue = [&](int t) {
+  // this wave's share of tile t: the A pieces (half 0) or the B pieces (half 1)
+  auto issue_half = [&](int t, int half) {
     const int s = t % kStages;
-    const bf16* ab = abase + (size_t)t * astep;
-    const bf16* bb = bbase + (size_t)t * bstep;
     const uint32_t piece0 = wave * (kPieces * 1024);
+    if (half == 0) {
+      const bf16* ab = abase + (size_t)t * astep;
 #pragma unroll
-    for (int i = 0; i < kPieces; ++i)
-      dma16s(ab, aoff[i], __builtin_amdgcn_readfirstlane(lds0 + a_off(s) + piece0 + i * 1024));
+      for (int i = 0; i < kPieces; ++i)
+        dma16s(ab, aoff[i], __builtin_amdgcn_readfirstlane(lds0 + a_off(s) + piece0 + i * 1024));
+    } else {
+      const bf16* bb = bbase + (size_t)t * bstep;
 #pragma unroll
-    for (int i = 0; i < kPieces; ++i)
-      dma16s(bb, boff[i], __builtin_amdgcn_readfirstlane(lds0 + b_off(s) + piece0 + i * 1024));
+      for (int i = 0; i < kPieces; ++i)
+        dma16s(bb, boff[i], __builtin_amdgcn_readfirstlane(lds0 + b_off(s) + piece0 + i * 1024));
+    }
+  };
+  auto issue = [&](int t) {
+    issue_half(t, 0);
+    issue_half(t, 1);
   };
 
   f32x16 acc[kTM][kTN];
@@ -530,12 +538,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     // this wave, and after the barrier for all.
     wait_dma<0>();
     block_barrier();
-    if (t + 2 < nt) issue(t + 2);
-    // the next tile's first fragments (past the last tile: a stale stage, unused)
+    // the next tile's first fragments (past the last tile: a stale stage,
+    // unused), and the loads of tile t + 2 spread over k-steps 2 and 3
     read_frags(t + 1, 0);
+    if (t + 2 < nt) issue_half(t + 2, 0);
     mma(2);
+    __builtin_amdgcn_sched_barrier(0);
     read_frags(t + 1, 1);
+    if (t + 2 < nt) issue_half(t + 2, 1);
     mma(3);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   if (slice >= 0) {
