@@ -120,13 +120,17 @@ def round_to_bf16(a: np.ndarray) -> np.ndarray:
     return r.view(np.float32)
 
 
-def make_inputs(s: BlockShape, seed: int = 0) -> dict[str, np.ndarray]:
+def make_inputs(s: BlockShape, seed: int = 0, serial: bool = False) -> dict[str, np.ndarray]:
     """Draw one block's inputs, parameters and upstream gradient.
 
     Returns float32 arrays (bf16-exact for bf16 workloads):
     x, dy [batch, seq, hidden]; gamma, beta, b_out [hidden];
     w_in [n_in, hidden] (rows Q | K | V | up, heads contiguous in each);
     b_in [n_in]; w_out [hidden, k_out] (columns attention-out | down).
+
+    serial=True is for the serial block (two LayerNorms, two output biases):
+    the same draws, renamed gamma1, beta1 and b_o, followed by gamma2, beta2
+    and b_down, so both blocks share x, the weights and dy for a seed.
     """
     rng = np.random.default_rng(seed)
     H = s.hidden
@@ -145,4 +149,11 @@ def make_inputs(s: BlockShape, seed: int = 0) -> dict[str, np.ndarray]:
     out["w_out"] = draw((H, s.k_out), s.w_std)
     out["b_out"] = draw((H,), s.w_std)
     out["dy"] = draw((s.batch, s.seq, H), s.dy_std)
+    if serial:
+        out["gamma1"] = out.pop("gamma")
+        out["beta1"] = out.pop("beta")
+        out["b_o"] = out.pop("b_out")
+        out["gamma2"] = draw((H,), s.gamma_std, 1.0)
+        out["beta2"] = draw((H,), s.beta_std)
+        out["b_down"] = draw((H,), s.w_std)
     return out
