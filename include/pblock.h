@@ -151,6 +151,53 @@ pb_status pblock_backward(const pb_config* cfg, const void* x,
                           float* db_in, float* dw_out, float* db_out,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------- serial block
+ * The standard pre-LN block that Eq. 2 replaces (Section 3.1, Eq. 1), for
+ * comparison and for models that keep it:
+ *
+ *     x1 = x + Attention(LN1(x)) W_o^T + b_o
+ *     y  = x1 + gelu(LN2(x1) W_up^T + b_up) W_down^T + b_down
+ *
+ * The second residual adds x1 (the paper's printed Eq. 1 writes x there; the
+ * block it describes, and the one this computes, carries x1).  Weights use
+ * the parallel block's packed layouts as slices: W_qkv = w_in rows 0..3A-1,
+ * W_up = rows 3A..N_in-1 (b_in likewise); W_o = w_out columns 0..A-1, W_down
+ * = columns A..K_out-1.  Two LayerNorms (ln1_*, ln2_*, activation dtype [H])
+ * and two output biases (b_o, b_down, activation dtype [H]); the same window
+ * rule, scaling, LayerNorm and GeLU as above.
+ *
+ * Stash regions, in this order, each at a 256-byte boundary
+ * (pblock_serial_saved_offsets, 10 entries):
+ *   h1 [T, H] act, z [T, N_in] act (Q | K | V | U), c [T, K_out] act (O | G),
+ *   mean1 [T] fp32, rstd1 [T] fp32, lse [batch, heads, seq] fp32,
+ *   x1 [T, H] act, h2 [T, H] act, mean2 [T] fp32, rstd2 [T] fp32.
+ *
+ * Workspace modes, ownership, asynchrony and errors are those of the
+ * parallel block's calls (pblock_serial_workspace_bytes takes the same
+ * PB_WS_* modes).  Gradients dln1_*, dln2_*, dw_in, db_in, dw_out, db_o,
+ * db_down are fp32, in the layouts of their parameters, and overwritten. */
+size_t pblock_serial_saved_bytes(const pb_config* cfg);
+pb_status pblock_serial_saved_offsets(const pb_config* cfg, size_t* offsets);
+size_t pblock_serial_workspace_bytes(const pb_config* cfg, int mode);
+pb_status pblock_serial_forward(const pb_config* cfg, const void* x,
+                                const void* ln1_gamma, const void* ln1_beta,
+                                const void* ln2_gamma, const void* ln2_beta,
+                                const void* w_in, const void* b_in,
+                                const void* w_out, const void* b_o,
+                                const void* b_down, void* y, void* saved,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+pb_status pblock_serial_backward(const pb_config* cfg, const void* x,
+                                 const void* ln1_gamma, const void* ln1_beta,
+                                 const void* ln2_gamma, const void* ln2_beta,
+                                 const void* w_in, const void* b_in,
+                                 const void* w_out, const void* b_o,
+                                 const void* b_down, const void* saved,
+                                 const void* dy, void* dx, float* dln1_gamma,
+                                 float* dln1_beta, float* dln2_gamma,
+                                 float* dln2_beta, float* dw_in, float* db_in,
+                                 float* dw_out, float* db_o, float* db_down,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Causal sliding-window attention alone (Section 3.1 SWA; the exact
  * FlashAttention-2 result of Section 3.3), for all heads of all batch rows.
  * q, k, v: element (b, s, head, e) at ptr[(b*seq + s)*ld + head*head_dim + e],

@@ -6,6 +6,8 @@
 #include <math.h>
 
 #include <algorithm>
+#include <array>
+#include <initializer_list>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -171,6 +173,82 @@ BwdLayout bwd_layout(const Dims& d) {
   L.part = take(part * 4);
   L.base = o;  // required; the tail-split region after it is optional
   L.split = take(split_bytes_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32));
+  L.total = o;
+  return L;
+}
+
+// ------------------------------------------------------------ serial block
+// Stash of the serial block: h1, Z (Q|K|V|U), C (O|G), mean1, rstd1, lse,
+// x1, h2, mean2, rstd2.
+struct SerialLayout {
+  size_t off[10];
+  size_t total;
+};
+SerialLayout serial_layout(const Dims& d) {
+  SerialLayout L;
+  size_t o = 0;
+  const size_t th = (size_t)(d.T * d.H) * d.esz;
+  const size_t sizes[10] = {th, (size_t)(d.T * d.N_in) * d.esz, (size_t)(d.T * d.K_out) * d.esz,
+                            (size_t)d.T * 4, (size_t)d.T * 4, (size_t)(d.B * d.heads * d.S) * 4,
+                            th, th, (size_t)d.T * 4, (size_t)d.T * 4};
+  for (int i = 0; i < 10; ++i) {
+    L.off[i] = o;
+    o = align256(o + sizes[i]);
+  }
+  L.total = o;
+  return L;
+}
+
+// Largest tail-split space among a list of GEMM shapes (M, N, K).
+size_t max_split_bytes(pb::Dt dt, std::initializer_list<std::array<int, 3>> shapes) {
+  size_t m = 0;
+  for (const auto& s : shapes)
+    m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, s[0], s[1], s[2])) * 4);
+  return m;
+}
+size_t serial_split_fwd(const Dims& d, pb::Dt dt) {
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, F = (int)d.F;
+  size_t m = max_split_bytes(dt, {{T, 3 * A, H}, {T, H, A}, {T, F, H}, {T, H, F}});
+  const pb::AttnShape a = attn_shape(d);
+  return std::max(m, pb::attn_fwd_partial_bytes(a, pb::attn_split_plan(dt, a)));
+}
+size_t serial_split_bwd(const Dims& d, pb::Dt dt) {
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, F = (int)d.F;
+  size_t m = max_split_bytes(dt, {{T, F, H}, {H, F, T}, {T, H, F}, {F, H, T}, {T, A, H},
+                                  {H, A, T}, {T, H, 3 * A}, {3 * A, H, T}});
+  const pb::AttnShape a = attn_shape(d);
+  return std::max(m, pb::attn_bwd_partial_bytes(a, pb::attn_split_plan(dt, a)));
+}
+
+// Backward workspace of the serial block: dO, dZ, dh (fp32, shared by both
+// LayerNorms), dx1, softmax row terms, LN row terms, LN partial column sums,
+// column-sum scratch, then the optional split region.
+struct SerialBwdLayout {
+  size_t d_o, dz, dh, dx1, delta, rowpart, pdg, pdb, pdy, part, split, base, total;
+};
+SerialBwdLayout serial_bwd_layout(const Dims& d) {
+  SerialBwdLayout L;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align256(o + bytes);
+    return at;
+  };
+  const int nblk = pb::ln_backward_chunks((int)d.T);
+  L.d_o = take((size_t)(d.T * d.A) * d.esz);
+  L.dz = take((size_t)(d.T * d.N_in) * d.esz);
+  L.dh = take((size_t)(d.T * d.H) * 4);
+  L.dx1 = take((size_t)(d.T * d.H) * d.esz);
+  L.delta = take((size_t)(d.B * d.heads * d.S) * 4);
+  L.rowpart = take((size_t)d.T * pb::ln_row_groups((int)d.H) * sizeof(float2));
+  L.pdg = take((size_t)nblk * d.H * 4);
+  L.pdb = take((size_t)nblk * d.H * 4);
+  L.pdy = take((size_t)nblk * d.H * 4);
+  size_t part = pb::colsum_partial_floats((int)d.T, (int)d.N_in);
+  part = std::max(part, pb::colsum_partial_floats(nblk, (int)d.H));
+  L.part = take(part * 4);
+  L.base = o;
+  L.split = take(serial_split_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32));
   L.total = o;
   return L;
 }
@@ -555,6 +633,281 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void
   a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
   pb::launch_attn_backward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, (float*)ws,
                            dq, dk, dv, ld_dqkv, (char*)ws + need, ws_bytes - need, stream);
+  return finish_launches();
+}
+
+size_t pblock_serial_saved_bytes(const pb_config* cfg) {
+  if (check_config(cfg) != PB_OK) return 0;
+  return serial_layout(dims_of(cfg)).total;
+}
+
+pb_status pblock_serial_saved_offsets(const pb_config* cfg, size_t* offsets) {
+  PB_CHECK(check_config(cfg));
+  if (!offsets) return fail(PB_ERR_INVALID_ARG, "offsets is NULL");
+  const SerialLayout L = serial_layout(dims_of(cfg));
+  for (int i = 0; i < 10; ++i) offsets[i] = L.off[i];
+  return PB_OK;
+}
+
+size_t pblock_serial_workspace_bytes(const pb_config* cfg, int mode) {
+  if (check_config(cfg) != PB_OK) return 0;
+  const Dims d = dims_of(cfg);
+  const size_t split = align256(serial_split_fwd(d, dt_of(cfg)));
+  switch (mode) {
+    case PB_WS_FORWARD_WITH_STASH: return serial_layout(d).total + split;
+    case PB_WS_BACKWARD: return serial_bwd_layout(d).total;
+    case PB_WS_FORWARD: return split;
+    default: return 0;
+  }
+}
+
+pb_status pblock_serial_forward(const pb_config* cfg, const void* x, const void* ln1_gamma,
+                                const void* ln1_beta, const void* ln2_gamma,
+                                const void* ln2_beta, const void* w_in, const void* b_in,
+                                const void* w_out, const void* b_o, const void* b_down, void* y,
+                                void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
+  PB_CHECK(check_config(cfg));
+  PB_CHECK(check_ptr(x, "x"));
+  PB_CHECK(check_ptr(ln1_gamma, "ln1_gamma"));
+  PB_CHECK(check_ptr(ln1_beta, "ln1_beta"));
+  PB_CHECK(check_ptr(ln2_gamma, "ln2_gamma"));
+  PB_CHECK(check_ptr(ln2_beta, "ln2_beta"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(b_in, "b_in"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(b_o, "b_o"));
+  PB_CHECK(check_ptr(b_down, "b_down"));
+  PB_CHECK(check_ptr(y, "y"));
+  const Dims d = dims_of(cfg);
+  const SerialLayout L = serial_layout(d);
+  const pb::Dt dt = dt_of(cfg);
+  void* stash = saved;
+  char* split_base = (char*)ws;
+  size_t split_bytes = ws ? ws_bytes : 0;
+  if (stash) {
+    PB_CHECK(check_ptr(stash, "saved"));
+    if (ws) PB_CHECK(check_ptr(ws, "ws"));
+  } else {
+    PB_CHECK(check_ptr(ws, "ws (needed when saved is NULL)"));
+    if (ws_bytes < L.total)
+      return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed to hold the stash", ws_bytes,
+                  L.total);
+    stash = ws;
+    split_base = (char*)ws + L.total;
+    split_bytes = ws_bytes - L.total;
+  }
+  float* split_ws = (float*)split_base;
+  const size_t split_f = split_bytes / 4;
+  const size_t e = d.esz;
+  char* sb = (char*)stash;
+  void* h1 = sb + L.off[0];
+  void* z = sb + L.off[1];
+  void* c = sb + L.off[2];
+  float* mean1 = (float*)(sb + L.off[3]);
+  float* rstd1 = (float*)(sb + L.off[4]);
+  float* lse = (float*)(sb + L.off[5]);
+  void* x1 = sb + L.off[6];
+  void* h2 = sb + L.off[7];
+  float* mean2 = (float*)(sb + L.off[8]);
+  float* rstd2 = (float*)(sb + L.off[9]);
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, F = (int)d.F, N_in = (int)d.N_in,
+            K_out = (int)d.K_out;
+
+  // x1 = x + Attention(LN1(x)) W_o^T + b_o
+  pb::launch_ln_forward(dt, x, ln1_gamma, ln1_beta, h1, mean1, rstd1, T, H, cfg->ln_eps, stream);
+  pb::EpiArgs eq;  // Q | K | V = h1 W_qkv^T + b_qkv -> Z[:, :3A] (no GeLU columns)
+  eq.out = z;
+  eq.ld_out = N_in;
+  eq.out2 = c;
+  eq.ld_out2 = K_out;
+  eq.bias = b_in;
+  eq.split = 3 * A;
+  eq.gelu_tanh = cfg->gelu_tanh;
+  pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h1, H, w_in, H, T, 3 * A, H, eq, split_ws,
+                  split_f, stream);
+  pb::launch_attn_forward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
+                          lse, split_base, split_bytes, stream);
+  pb::EpiArgs eo;
+  eo.out = x1;
+  eo.ld_out = H;
+  eo.bias = b_o;
+  eo.resid = x;
+  pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, c, K_out, w_out, K_out, T, H, A, eo,
+                  split_ws, split_f, stream);
+  // y = x1 + GeLU(LN2(x1) W_up^T + b_up) W_down^T + b_down
+  pb::launch_ln_forward(dt, x1, ln2_gamma, ln2_beta, h2, mean2, rstd2, T, H, cfg->ln_eps,
+                        stream);
+  pb::EpiArgs eu;  // U -> Z[:, 3A:], G = GeLU(U) -> C[:, A:]
+  eu.out = at(z, 3LL * A, e);
+  eu.ld_out = N_in;
+  eu.out2 = c;
+  eu.ld_out2 = K_out;
+  eu.bias = at(b_in, 3LL * A, e);
+  eu.split = 0;
+  eu.col2 = A;
+  eu.gelu_tanh = cfg->gelu_tanh;
+  pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h2, H, at(w_in, 3LL * A * H, e), H, T, F,
+                  H, eu, split_ws, split_f, stream);
+  pb::EpiArgs ed;
+  ed.out = y;
+  ed.ld_out = H;
+  ed.bias = b_down;
+  ed.resid = x1;
+  pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, at(c, A, e), K_out, at(w_out, A, e), K_out,
+                  T, H, F, ed, split_ws, split_f, stream);
+  return finish_launches();
+}
+
+pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void* ln1_gamma,
+                                 const void* ln1_beta, const void* ln2_gamma,
+                                 const void* ln2_beta, const void* w_in, const void* b_in,
+                                 const void* w_out, const void* b_o, const void* b_down,
+                                 const void* saved, const void* dy, void* dx,
+                                 float* dln1_gamma, float* dln1_beta, float* dln2_gamma,
+                                 float* dln2_beta, float* dw_in, float* db_in, float* dw_out,
+                                 float* db_o, float* db_down, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  PB_CHECK(check_config(cfg));
+  PB_CHECK(check_ptr(x, "x"));
+  PB_CHECK(check_ptr(ln1_gamma, "ln1_gamma"));
+  PB_CHECK(check_ptr(ln1_beta, "ln1_beta"));
+  PB_CHECK(check_ptr(ln2_gamma, "ln2_gamma"));
+  PB_CHECK(check_ptr(ln2_beta, "ln2_beta"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(b_in, "b_in"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(b_o, "b_o"));
+  PB_CHECK(check_ptr(b_down, "b_down"));
+  PB_CHECK(check_ptr(saved, "saved"));
+  PB_CHECK(check_ptr(dy, "dy"));
+  PB_CHECK(check_ptr(dx, "dx"));
+  PB_CHECK(check_ptr(dln1_gamma, "dln1_gamma"));
+  PB_CHECK(check_ptr(dln1_beta, "dln1_beta"));
+  PB_CHECK(check_ptr(dln2_gamma, "dln2_gamma"));
+  PB_CHECK(check_ptr(dln2_beta, "dln2_beta"));
+  PB_CHECK(check_ptr(dw_in, "dw_in"));
+  PB_CHECK(check_ptr(db_in, "db_in"));
+  PB_CHECK(check_ptr(dw_out, "dw_out"));
+  PB_CHECK(check_ptr(db_o, "db_o"));
+  PB_CHECK(check_ptr(db_down, "db_down"));
+  PB_CHECK(check_ptr(ws, "ws"));
+  const Dims d = dims_of(cfg);
+  const SerialBwdLayout W = serial_bwd_layout(d);
+  if (ws_bytes < W.base)
+    return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, W.base);
+  const SerialLayout L = serial_layout(d);
+  const pb::Dt dt = dt_of(cfg);
+  const size_t e = d.esz;
+  const char* sb = (const char*)saved;
+  const void* h1 = sb + L.off[0];
+  const void* z = sb + L.off[1];
+  const void* c = sb + L.off[2];
+  const float* mean1 = (const float*)(sb + L.off[3]);
+  const float* rstd1 = (const float*)(sb + L.off[4]);
+  const float* lse = (const float*)(sb + L.off[5]);
+  const void* x1 = sb + L.off[6];
+  const void* h2 = sb + L.off[7];
+  const float* mean2 = (const float*)(sb + L.off[8]);
+  const float* rstd2 = (const float*)(sb + L.off[9]);
+  char* wb = (char*)ws;
+  void* d_o = wb + W.d_o;
+  void* dz = wb + W.dz;
+  float* dh = (float*)(wb + W.dh);
+  void* dx1 = wb + W.dx1;
+  float* delta = (float*)(wb + W.delta);
+  float2* rowpart = (float2*)(wb + W.rowpart);
+  float* pdg = (float*)(wb + W.pdg);
+  float* pdb = (float*)(wb + W.pdb);
+  float* pdy = (float*)(wb + W.pdy);
+  float* part = (float*)(wb + W.part);
+  float* split_ws = (float*)(wb + W.split);
+  const size_t split_f = ws_bytes >= W.total ? (W.total - W.split) / 4 : 0;
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, F = (int)d.F, N_in = (int)d.N_in,
+            K_out = (int)d.K_out;
+  const int nblk = pb::ln_backward_chunks(T);
+  (void)ln1_beta;
+  (void)ln2_beta;
+  (void)b_in;
+  (void)b_o;
+  (void)b_down;
+
+  // MLP: dG = dy W_down, dU = dG * gelu'(U) -> dZ[:, 3A:]
+  pb::EpiArgs e1;
+  e1.out = dz;
+  e1.ld_out = N_in;
+  e1.out2 = dz;
+  e1.ld_out2 = N_in;
+  e1.aux = z;
+  e1.split = 0;
+  e1.col2 = 3 * A;
+  e1.gelu_tanh = cfg->gelu_tanh;
+  pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, at(w_out, A, e), K_out, T, F, H,
+                  e1, split_ws, split_f, stream);
+  // dh2 = dU W_up, with LN2's row terms
+  pb::EpiArgs e2;
+  e2.out = dh;
+  e2.ld_out = H;
+  e2.aux = x1;
+  e2.bias = ln2_gamma;
+  e2.mean = mean2;
+  e2.rstd = rstd2;
+  e2.rowpart = rowpart;
+  e2.rowpart_ld = pb::ln_row_groups(H);
+  pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, at(dz, 3LL * A, e), N_in,
+                  at(w_in, 3LL * A * H, e), H, T, H, F, e2, split_ws, split_f, stream);
+  // dx1 = dy + LN2'(dh2); dgamma2, dbeta2, and db_down = sum dy
+  pb::launch_ln_backward(dt, x1, mean2, rstd2, ln2_gamma, dh, rowpart, dy, dx1, pdg, pdb, pdy, T,
+                         H, stream);
+  pb::launch_colsum_f32(pdg, H, nblk, H, part, dln2_gamma, stream);
+  pb::launch_colsum_f32(pdb, H, nblk, H, part, dln2_beta, stream);
+  pb::launch_colsum_f32(pdy, H, nblk, H, part, db_down, stream);
+  // attention: dO = dx1 W_o, then dQ, dK, dV -> dZ[:, :3A]
+  pb::EpiArgs e3;
+  e3.out = d_o;
+  e3.ld_out = A;
+  e3.split = A;  // every column is dO
+  e3.gelu_tanh = cfg->gelu_tanh;
+  pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dx1, H, w_out, K_out, T, A, H, e3,
+                  split_ws, split_f, stream);
+  pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
+                           d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in,
+                           split_ws, split_f * 4, stream);
+  // dh1 = dQKV W_qkv, with LN1's row terms
+  pb::EpiArgs e4;
+  e4.out = dh;
+  e4.ld_out = H;
+  e4.aux = x;
+  e4.bias = ln1_gamma;
+  e4.mean = mean1;
+  e4.rstd = rstd1;
+  e4.rowpart = rowpart;
+  e4.rowpart_ld = pb::ln_row_groups(H);
+  pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, 3 * A, e4, split_ws,
+                  split_f, stream);
+  // dx = dx1 + LN1'(dh1); dgamma1, dbeta1, and db_o = sum dx1
+  pb::launch_ln_backward(dt, x, mean1, rstd1, ln1_gamma, dh, rowpart, dx1, dx, pdg, pdb, pdy, T,
+                         H, stream);
+  pb::launch_colsum_f32(pdg, H, nblk, H, part, dln1_gamma, stream);
+  pb::launch_colsum_f32(pdb, H, nblk, H, part, dln1_beta, stream);
+  pb::launch_colsum_f32(pdy, H, nblk, H, part, db_o, stream);
+  // bias gradients of the input projections: db_in = sum over tokens of dZ
+  pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+  // weight gradients (token contractions), last
+  pb::EpiArgs w;
+  w.ld_out = K_out;
+  w.out = at(dw_out, A, 4);  // dW_down = dy^T G
+  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, at(c, A, e), K_out, H, F, T, w,
+                  split_ws, split_f, stream);
+  w.out = dw_out;  // dW_o = dx1^T O
+  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dx1, H, c, K_out, H, A, T, w, split_ws,
+                  split_f, stream);
+  w.ld_out = H;
+  w.out = at(dw_in, 3LL * A * H, 4);  // dW_up = dU^T h2
+  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, at(dz, 3LL * A, e), N_in, h2, H, F, H, T,
+                  w, split_ws, split_f, stream);
+  w.out = dw_in;  // dW_qkv = dQKV^T h1
+  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h1, H, 3 * A, H, T, w, split_ws,
+                  split_f, stream);
   return finish_launches();
 }
 

@@ -24,13 +24,16 @@ ATTN_WS_FORWARD, ATTN_WS_BACKWARD_MIN, ATTN_WS_BACKWARD = 0, 1, 2
 STATUS = {0: "PB_OK", 1: "PB_ERR_INVALID_ARG", 2: "PB_ERR_UNSUPPORTED", 3: "PB_ERR_WORKSPACE",
           4: "PB_ERR_HIP"}
 SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
+SERIAL_SAVED_REGIONS = ("h1", "z", "c", "mean1", "rstd1", "lse", "x1", "h2", "mean2", "rstd2")
 
 # Every function the header declares (checked by the CPU tests).
 EXPORTS = (
     "pblock_validate", "pblock_saved_bytes", "pblock_saved_offsets", "pblock_workspace_bytes",
     "pblock_forward", "pblock_backward", "pblock_swattn_forward",
     "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_set_step_events",
-    "pblock_status_string", "pblock_last_error",
+    "pblock_status_string", "pblock_last_error", "pblock_serial_saved_bytes",
+    "pblock_serial_saved_offsets", "pblock_serial_workspace_bytes", "pblock_serial_forward",
+    "pblock_serial_backward",
 )
 
 # pb_step order of include/pblock.h
@@ -79,6 +82,11 @@ def load_library(path: str = LIB_PATH):
         "pblock_set_step_events": (c_int, [P, P]),
         "pblock_status_string": (ctypes.c_char_p, [c_int]),
         "pblock_last_error": (ctypes.c_char_p, []),
+        "pblock_serial_saved_bytes": (c_size_t, [cfgp]),
+        "pblock_serial_saved_offsets": (c_int, [cfgp, POINTER(c_size_t)]),
+        "pblock_serial_workspace_bytes": (c_size_t, [cfgp, c_int]),
+        "pblock_serial_forward": (c_int, [cfgp] + [P] * 13 + [c_size_t, P]),
+        "pblock_serial_backward": (c_int, [cfgp] + [P] * 23 + [c_size_t, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -197,6 +205,40 @@ def pblock_set_step_events(begin, end):
     _check(lib.pblock_set_step_events(b, e))
 
 
+def pblock_serial_saved_bytes(cfg: PbConfig) -> int:
+    return load_library().pblock_serial_saved_bytes(ctypes.byref(cfg))
+
+
+def pblock_serial_saved_offsets(cfg: PbConfig) -> dict:
+    arr = (c_size_t * len(SERIAL_SAVED_REGIONS))()
+    _check(load_library().pblock_serial_saved_offsets(ctypes.byref(cfg), arr))
+    return dict(zip(SERIAL_SAVED_REGIONS, list(arr)))
+
+
+def pblock_serial_workspace_bytes(cfg: PbConfig, mode: int) -> int:
+    """mode: WS_FORWARD, WS_FORWARD_WITH_STASH or WS_BACKWARD."""
+    return load_library().pblock_serial_workspace_bytes(ctypes.byref(cfg), int(mode))
+
+
+def pblock_serial_forward(cfg, x, ln1_gamma, ln1_beta, ln2_gamma, ln2_beta, w_in, b_in, w_out,
+                          b_o, b_down, y, saved=None, ws=None, stream=None):
+    _check(load_library().pblock_serial_forward(
+        ctypes.byref(cfg), _ptr(x), _ptr(ln1_gamma), _ptr(ln1_beta), _ptr(ln2_gamma),
+        _ptr(ln2_beta), _ptr(w_in), _ptr(b_in), _ptr(w_out), _ptr(b_o), _ptr(b_down), _ptr(y),
+        _ptr(saved), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def pblock_serial_backward(cfg, x, ln1_gamma, ln1_beta, ln2_gamma, ln2_beta, w_in, b_in, w_out,
+                           b_o, b_down, saved, dy, dx, dln1_gamma, dln1_beta, dln2_gamma,
+                           dln2_beta, dw_in, db_in, dw_out, db_o, db_down, ws, stream=None):
+    _check(load_library().pblock_serial_backward(
+        ctypes.byref(cfg), _ptr(x), _ptr(ln1_gamma), _ptr(ln1_beta), _ptr(ln2_gamma),
+        _ptr(ln2_beta), _ptr(w_in), _ptr(b_in), _ptr(w_out), _ptr(b_o), _ptr(b_down),
+        _ptr(saved), _ptr(dy), _ptr(dx), _ptr(dln1_gamma), _ptr(dln1_beta), _ptr(dln2_gamma),
+        _ptr(dln2_beta), _ptr(dw_in), _ptr(db_in), _ptr(dw_out), _ptr(db_o), _ptr(db_down),
+        _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
 def pblock_status_string(status: int) -> str:
     return load_library().pblock_status_string(status).decode()
 
@@ -258,18 +300,83 @@ class ParallelBlock:
 
     def saved_view(self, name: str):
         """A typed view of one stash region (h, z, c, mean, rstd, lse)."""
+        return _stash_view(self.cfg, self.saved, pblock_saved_offsets(self.cfg), name)
+
+
+def _stash_view(cfg, saved, offsets: dict, name: str):
+    import torch
+    T, H, A = cfg.batch * cfg.seq, cfg.hidden, cfg.heads * cfg.head_dim
+    act = torch.bfloat16 if cfg.dtype == PB_BF16 else torch.float32
+    f32 = torch.float32
+    shapes = {"z": ((T, 3 * A + cfg.ffn), act), "c": ((T, A + cfg.ffn), act),
+              "lse": ((cfg.batch, cfg.heads, cfg.seq), f32)}
+    for n in ("h", "h1", "h2", "x1"):
+        shapes[n] = ((T, H), act)
+    for n in ("mean", "rstd", "mean1", "rstd1", "mean2", "rstd2"):
+        shapes[n] = ((T,), f32)
+    shape, dt = shapes[name]
+    n = 1
+    for s_ in shape:
+        n *= s_
+    off = offsets[name]
+    nbytes = n * torch.empty((), dtype=dt).element_size()
+    return saved[off:off + nbytes].view(dt).view(shape)
+
+
+class SerialBlock:
+    """The standard pre-LN block's device buffers around the serial C calls.
+
+    ``tensors`` maps x, gamma1, beta1, gamma2, beta2, w_in, b_in, w_out, b_o,
+    b_down, dy to device tensors of the activation dtype (w_in and w_out in
+    the parallel block's packed layouts).  Buffers are allocated once here.
+    """
+
+    def __init__(self, cfg: PbConfig, tensors: dict, device="cuda"):
         import torch
-        cfg = self.cfg
-        off = pblock_saved_offsets(cfg)[name]
-        T, H, A = self.T, cfg.hidden, cfg.heads * cfg.head_dim
+        self.cfg = cfg
+        self.t = tensors
+        H = cfg.hidden
+        A = cfg.heads * cfg.head_dim
+        n_in, k_out = 3 * A + cfg.ffn, A + cfg.ffn
         act = torch.bfloat16 if cfg.dtype == PB_BF16 else torch.float32
-        shapes = {"h": ((T, H), act), "z": ((T, 3 * A + cfg.ffn), act),
-                  "c": ((T, A + cfg.ffn), act), "mean": ((T,), torch.float32),
-                  "rstd": ((T,), torch.float32),
-                  "lse": ((cfg.batch, cfg.heads, cfg.seq), torch.float32)}
-        shape, dt = shapes[name]
-        n = 1
-        for s_ in shape:
-            n *= s_
-        nbytes = n * torch.empty((), dtype=dt).element_size()
-        return self.saved[off:off + nbytes].view(dt).view(shape)
+        f32 = torch.float32
+        u8 = torch.uint8
+        self.y = torch.empty((cfg.batch, cfg.seq, H), dtype=act, device=device)
+        self.saved = torch.empty(pblock_serial_saved_bytes(cfg), dtype=u8, device=device)
+        self.ws = torch.empty(pblock_serial_workspace_bytes(cfg, WS_BACKWARD), dtype=u8,
+                              device=device)
+        nf = pblock_serial_workspace_bytes(cfg, WS_FORWARD)
+        self.ws_fwd = torch.empty(nf, dtype=u8, device=device) if nf else None
+        self.grads = dict(
+            dx=torch.empty((cfg.batch, cfg.seq, H), dtype=act, device=device),
+            dgamma1=torch.empty(H, dtype=f32, device=device),
+            dbeta1=torch.empty(H, dtype=f32, device=device),
+            dgamma2=torch.empty(H, dtype=f32, device=device),
+            dbeta2=torch.empty(H, dtype=f32, device=device),
+            dw_in=torch.empty((n_in, H), dtype=f32, device=device),
+            db_in=torch.empty(n_in, dtype=f32, device=device),
+            dw_out=torch.empty((H, k_out), dtype=f32, device=device),
+            db_o=torch.empty(H, dtype=f32, device=device),
+            db_down=torch.empty(H, dtype=f32, device=device),
+        )
+
+    def forward(self, stream=None):
+        t = self.t
+        pblock_serial_forward(self.cfg, t["x"], t["gamma1"], t["beta1"], t["gamma2"],
+                              t["beta2"], t["w_in"], t["b_in"], t["w_out"], t["b_o"],
+                              t["b_down"], self.y, self.saved, self.ws_fwd, stream)
+        return self.y
+
+    def backward(self, dy=None, stream=None):
+        t, g = self.t, self.grads
+        pblock_serial_backward(self.cfg, t["x"], t["gamma1"], t["beta1"], t["gamma2"],
+                               t["beta2"], t["w_in"], t["b_in"], t["w_out"], t["b_o"],
+                               t["b_down"], self.saved, t["dy"] if dy is None else dy, g["dx"],
+                               g["dgamma1"], g["dbeta1"], g["dgamma2"], g["dbeta2"], g["dw_in"],
+                               g["db_in"], g["dw_out"], g["db_o"], g["db_down"], self.ws,
+                               stream)
+        return g
+
+    def saved_view(self, name: str):
+        """A typed view of one stash region (names in SERIAL_SAVED_REGIONS)."""
+        return _stash_view(self.cfg, self.saved, pblock_serial_saved_offsets(self.cfg), name)

@@ -189,3 +189,70 @@ def test_swattn_workspace_modes():
         assert lib_ws(c, pb.ATTN_WS_FORWARD) == 0
         assert lib_ws(c, pb.ATTN_WS_BACKWARD) == lib_ws(c, pb.ATTN_WS_BACKWARD_MIN)
     assert lib_ws(small, 7) == 0
+
+
+def declared_arities():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    out = {}
+    for name, args in re.findall(r"\b(pblock_\w+)\s*\(([^;{]*?)\)\s*;", text):
+        a = args.strip()
+        out[name] = 0 if a in ("", "void") else a.count(",") + 1
+    return out
+
+
+def test_binding_argument_counts_match_the_header():
+    lib = pb.load_library()
+    ar = declared_arities()
+    assert sorted(ar) == sorted(pb.EXPORTS)
+    for name, n in ar.items():
+        assert len(getattr(lib, name).argtypes) == n, name
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_serial_saved_layout(name):
+    s = WORKLOADS[name]
+    c = pb.config_from_shape(s)
+    e = 2 if s.dtype == "bf16" else 4
+    T, H = s.tokens, s.hidden
+    sizes = [T * H * e, T * s.n_in * e, T * s.k_out * e, 4 * T, 4 * T,
+             4 * s.batch * s.heads * s.seq, T * H * e, T * H * e, 4 * T, 4 * T]
+    off, o = [], 0
+    for z in sizes:
+        off.append(o)
+        o = align(o + z)
+    assert pb.pblock_serial_saved_offsets(c) == dict(zip(pb.SERIAL_SAVED_REGIONS, off))
+    assert pb.pblock_serial_saved_bytes(c) == o
+    split = pb.pblock_serial_workspace_bytes(c, pb.WS_FORWARD)
+    assert split % 256 == 0
+    assert pb.pblock_serial_workspace_bytes(c, pb.WS_FORWARD_WITH_STASH) == o + split
+    # backward: dO, dZ, dh (fp32) and dx1 at least
+    assert pb.pblock_serial_workspace_bytes(c, pb.WS_BACKWARD) >= (
+        T * s.attn_width * e + T * s.n_in * e + 4 * T * H + T * H * e)
+    assert pb.pblock_serial_workspace_bytes(c, 3) == 0
+
+
+def test_serial_rejects_bad_arguments_before_launching():
+    lib = pb.load_library()
+    c = good_cfg()
+    # forward: no stash and a workspace too small for one
+    need = pb.pblock_serial_saved_bytes(c)
+    args = [FAKE] * 11  # x .. y
+    st = lib.pblock_serial_forward(ctypes.byref(c), *args, None, FAKE, need - 1, None)
+    assert st == 3 and "ws_bytes" in pb.pblock_last_error()
+    st = lib.pblock_serial_forward(ctypes.byref(c), *args, None, None, 0, None)
+    assert st == 1
+    bad = list(args)
+    bad[3] = FAKE + 4  # ln2_gamma misaligned
+    st = lib.pblock_serial_forward(ctypes.byref(c), *bad, FAKE, None, 0, None)
+    assert st == 1 and "ln2_gamma" in pb.pblock_last_error()
+    # backward: workspace below the required part, then a NULL gradient
+    bargs = [FAKE] * 22
+    st = lib.pblock_serial_backward(ctypes.byref(c), *bargs, FAKE, 1024, None)
+    assert st == 3
+    need = pb.pblock_serial_workspace_bytes(c, pb.WS_BACKWARD)
+    bargs[21] = None  # db_down
+    st = lib.pblock_serial_backward(ctypes.byref(c), *bargs, FAKE, need, None)
+    assert st == 1 and "db_down" in pb.pblock_last_error()
+    bad_cfg = good_cfg(head_dim=96)
+    assert pb.pblock_serial_saved_bytes(bad_cfg) == 0
+    assert pb.pblock_serial_workspace_bytes(bad_cfg, pb.WS_BACKWARD) == 0
