@@ -13,7 +13,10 @@ Prints one JSON line.  Besides the contract fields it carries:
                 inside the timed steps;
   steps         per-step times from a separate pass with events around every
                 step;
-  cpu_baseline  the fp64 CPU oracle timed on this host on one full step.
+  serial_block  the standard two-LayerNorm block on the same workload and
+                kernels (same model FLOPs), and the parallel block's speedup
+                over it;
+  cpu_baseline  the fp64 CPU oracle timed on this host on whole steps.
 
 Profiling helpers (see the commands recorded in profiles/):
   --copy-calibration   run a plain copy-like kernel of known size, for scaling
@@ -94,9 +97,15 @@ def source_fingerprint(step):
     return h.hexdigest()[:16]
 
 
-def gemm_steps(s):
+def gemm_steps(s, block="parallel"):
     """(M, N, K) of each GEMM step as launched."""
     T, H, n_in, k_out = s.tokens, s.hidden, s.n_in, s.k_out
+    if block == "serial":
+        A, F = s.attn_width, s.ffn
+        return {"qkv": (T, 3 * A, H), "o_proj": (T, H, A), "up": (T, F, H), "down": (T, H, F),
+                "dg": (T, F, H), "dh2": (T, H, F), "d_o": (T, A, H), "dh1": (T, H, 3 * A),
+                "dw_down": (H, F, T), "dw_o": (H, A, T), "dw_up": (F, H, T),
+                "dw_qkv": (3 * A, H, T)}
     return {"in_proj": (T, n_in, H), "out_proj": (T, H, k_out), "dc": (T, k_out, H),
             "dw_out": (H, k_out, T), "dh": (T, H, n_in), "dw_in": (n_in, H, T)}
 
@@ -105,7 +114,13 @@ def gemm_steps(s):
 # names: A K-contiguous, B K-contiguous, epilogue (pb::Epi value).
 GEMM_SIGNATURE = {"in_proj": "<true, true, (pb::Epi)1", "out_proj": "<true, true, (pb::Epi)2",
                   "dc": "<true, false, (pb::Epi)3", "dw_out": "<false, false, (pb::Epi)0",
-                  "dh": "<true, false, (pb::Epi)4", "dw_in": "<false, false, (pb::Epi)0"}
+                  "dh": "<true, false, (pb::Epi)4", "dw_in": "<false, false, (pb::Epi)0",
+                  "qkv": "<true, true, (pb::Epi)1", "o_proj": "<true, true, (pb::Epi)2",
+                  "up": "<true, true, (pb::Epi)1", "down": "<true, true, (pb::Epi)2",
+                  "dg": "<true, false, (pb::Epi)3", "dh2": "<true, false, (pb::Epi)4",
+                  "d_o": "<true, false, (pb::Epi)3", "dh1": "<true, false, (pb::Epi)4",
+                  "dw_down": "<false, false, (pb::Epi)0", "dw_o": "<false, false, (pb::Epi)0",
+                  "dw_up": "<false, false, (pb::Epi)0", "dw_qkv": "<false, false, (pb::Epi)0"}
 
 
 def demangle(name):
@@ -118,27 +133,45 @@ def demangle(name):
         return name
 
 
-def gemm_step_of(name, grid, s):
-    """Block step a GEMM launch belongs to ("" if none)."""
-    for st, mnk in gemm_steps(s).items():
-        if ("gemm_bf16" in name and GEMM_SIGNATURE[st] in name
-                and gemm_grid_threads(*mnk) == grid):
-            return st
-    return ""
+def gemm_step_of(name, grid, s, block="parallel"):
+    """Block step(s) a GEMM launch belongs to ("" if none; "a/b" when two
+    steps launch the same kernel on the same grid)."""
+    hits = [st for st, mnk in gemm_steps(s, block).items()
+            if "gemm_bf16" in name and GEMM_SIGNATURE[st] in name
+            and gemm_grid_threads(*mnk) == grid]
+    return "/".join(hits)
 
 
-def gemm_grid_threads(M, N, K):
-    """Work-items of a bf16 GEMM launch: 256 x 256 output tiles of 512 threads;
-    when the tiles leave a partial last wave over the 256 CUs, those tail tiles
-    are split along K (the plan the library uses with a full workspace)."""
+def split_plan(M, N, K):
+    """(n_full, tail, splits) of a bf16 GEMM with a full workspace, as the
+    library plans it: 256 x 256 tiles, one workgroup per CU on 256 CUs; a
+    partial last wave is split along K to fill the chip, and a grid of fewer
+    tiles than CUs is split along K when the estimate (waves x K-steps, plus
+    3 + 1/16 per partial tile for the reduction) wins."""
     tiles = -(-M // 256) * -(-N // 256)
     n_full = tiles // 256 * 256
     tail = tiles - n_full
-    if K % 64 == 0 and n_full and tail:
-        splits = min(256 // tail, K // 64)
-        if splits >= 2:
-            return (n_full + tail * splits) * 512
-    return tiles * 512
+    nk = K // 64
+    if K % 64 or tail == 0:
+        return tiles, 0, 1
+    if n_full:
+        splits = min(256 // tail, nk)
+    else:
+        def cost(sp):
+            c = -(-tiles * sp // 256) * -(-nk // sp)
+            return c if sp == 1 else c + 3 + tiles * sp / 16
+        splits = 1
+        for sp in range(2, min(16, nk) + 1):
+            if cost(sp) < cost(splits):
+                splits = sp
+    return (n_full, tail, splits) if splits >= 2 else (tiles, 0, 1)
+
+
+def gemm_grid_threads(M, N, K):
+    """Work-items of a bf16 GEMM launch: 512 threads per workgroup, one per
+    whole tile and one per K-slice of each split tile."""
+    n_full, tail, splits = split_plan(M, N, K)
+    return (n_full + tail * splits) * 512
 
 
 def traffic_path(step, workload):
@@ -211,7 +244,7 @@ def read_traffic(step, workload):
     return rec["traffic_bytes"]
 
 
-def trace_summary(d, workload):
+def trace_summary(d, workload, block="parallel"):
     """Markdown table of a kernel-trace run: one row per (kernel, grid)."""
     from paper_2402_15627_amd.inputs import WORKLOADS
     s = WORKLOADS[workload]
@@ -236,7 +269,7 @@ def trace_summary(d, workload):
             d = re.search(r"Li(\d+)E", short)
             short = m.group(1) + (f"<{d.group(1)}>" if d else "")
         short = re.sub(r"\(.*", "", short)
-        step = gemm_step_of(name, grid, s)
+        step = gemm_step_of(name, grid, s, block)
         rows.append((sum(v), short[:70], grid, step, len(v), sum(v) / len(v), min(v), max(v)))
     rows.sort(reverse=True)
     out = ["| kernel | grid (work-items) | block step | calls | avg us | min us | max us | "
@@ -272,6 +305,34 @@ def cpu_baseline(shape, inputs, min_seconds=10.0, max_steps=6):
                       f"matmul), same seeded inputs as the GPU run"}
 
 
+def time_serial(pb, shape, warmup, steps, parallel_ms, flops):
+    """The standard block (two LayerNorms, four projections; the same model
+    FLOPs) on the same workload and kernels, timed like the parallel block:
+    forward + backward, inputs resident, events around the whole loop."""
+    import torch
+    from paper_2402_15627_amd.inputs import make_inputs
+    act = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    dev = {k: torch.from_numpy(v).to(act).cuda()
+           for k, v in make_inputs(shape, seed=0, serial=True).items()}
+    blk = pb.SerialBlock(pb.config_from_shape(shape), dev)
+    for _ in range(warmup):
+        blk.forward()
+        blk.backward()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for _ in range(steps):
+        blk.forward()
+        blk.backward()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"ms_per_step": round(ms, 4), "value": round(flops / (ms * 1e-3) / 1e12, 2),
+            "unit": "TFLOP/s",
+            "parallel_speedup": round(ms / parallel_ms, 4) if parallel_ms else None}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,6 +341,10 @@ def main():
     ap.add_argument("--workload", default="175b_tp8_share")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
+    ap.add_argument("--block", choices=("parallel", "serial"), default="parallel",
+                    help="serial: time only the standard two-LayerNorm block (for profiling)")
+    ap.add_argument("--no-serial", action="store_true",
+                    help="skip timing the serial (two-LayerNorm) block for comparison")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run the counter calibration copy and exit")
     ap.add_argument("--traffic-summary", nargs=4, metavar="DIR",
@@ -291,7 +356,7 @@ def main():
     ap.add_argument("--command", default="", help="command line recorded with a summary")
     args = ap.parse_args()
     if args.trace_summary:
-        print(trace_summary(args.trace_summary, args.workload))
+        print(trace_summary(args.trace_summary, args.workload, args.block))
         return
     if args.traffic_summary:
         rec = traffic_summary(args.traffic_summary, args.workload, args.traffic_step)
@@ -329,6 +394,12 @@ def main():
 
     shape = WORKLOADS[args.workload]
     pb.load_library()
+    if args.block == "serial":
+        flops = model_flops(shape)
+        rec = time_serial(pb, shape, args.warmup, args.steps, None, flops)
+        print(json.dumps({"block": "serial", "workload": shape.name, "steps": args.steps,
+                          "warmup": args.warmup, **rec}), flush=True)
+        return
     inputs = make_inputs(shape, seed=0)
     act = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
     dev = {k: torch.from_numpy(v).to(act).cuda() for k, v in inputs.items()}
@@ -427,6 +498,8 @@ def main():
         "roofline": roof,
         "steps_breakdown": steps_out,
     }
+    if not args.no_serial:
+        out["serial_block"] = time_serial(pb, shape, args.warmup, K, ms, flops)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, inputs)
     print(json.dumps(out), flush=True)

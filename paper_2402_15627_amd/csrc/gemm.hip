@@ -716,13 +716,31 @@ SplitPlan gemm_split_plan(Dt dt, int M, int N, int K) {
   const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   SplitPlan none{tiles, 0, 1};
   if (dt != Dt::BF16 || K % kBK != 0) return none;
-  constexpr int kCUs = 256;  // MI355X
+  constexpr int kCUs = 256;  // MI355X; one workgroup per CU
+  const int nk = K / kBK;
   const int n_full = tiles / kCUs * kCUs;
   const int tail = tiles - n_full;
-  if (n_full == 0 || tail == 0) return none;
-  const int splits = std::min(kCUs / tail, K / kBK);
-  if (splits < 2) return none;
-  return SplitPlan{n_full, tail, splits};
+  if (tail == 0) return none;
+  if (n_full > 0) {
+    // the last, partial wave: split its tiles so that it fills the chip once
+    const int splits = std::min(kCUs / tail, nk);
+    if (splits < 2) return none;
+    return SplitPlan{n_full, tail, splits};
+  }
+  // Fewer tiles than CUs: split every tile along K when that is estimated
+  // to be faster.  Cost in K-tile steps of one workgroup: waves x K-tiles per
+  // slice, plus the reduction (a fixed launch cost and the fp32 partial
+  // tiles written and read back, about 1/16 of a step each).
+  auto cost = [&](int s) {
+    const int waves = (tiles * s + kCUs - 1) / kCUs;
+    const double c = (double)waves * ((nk + s - 1) / s);
+    return s == 1 ? c : c + 3.0 + tiles * s / 16.0;
+  };
+  int best = 1;
+  for (int s = 2; s <= std::min(16, nk); ++s)
+    if (cost(s) < cost(best)) best = s;
+  if (best < 2) return none;
+  return SplitPlan{0, tiles, best};
 }
 
 size_t gemm_split_floats(const SplitPlan& p) {

@@ -86,15 +86,38 @@ def test_saved_layout(name):
 
 
 def tail_split(M, N, K, bf16=True):
-    """The tail-split plan the library uses for an M x N x K GEMM: tiles of
-    256 x 256, 256 CUs; the last partial wave is split along K."""
+    """The split plan the library uses for an M x N x K GEMM: tiles of
+    256 x 256, 256 CUs; the last partial wave is split along K to fill the
+    chip, and a grid of fewer tiles than CUs is split along K when the
+    estimate (waves x K-steps, plus 3 + 1/16 per partial tile) wins."""
     tiles = -(-M // 256) * -(-N // 256)
     n_full = tiles // 256 * 256
     tail = tiles - n_full
-    if not bf16 or K % 64 or n_full == 0 or tail == 0:
+    if not bf16 or K % 64 or tail == 0:
         return 0
-    splits = min(256 // tail, K // 64)
+    nk = K // 64
+    if n_full:
+        splits = min(256 // tail, nk)
+    else:
+        def cost(s):
+            c = -(-tiles * s // 256) * -(-nk // s)
+            return c if s == 1 else c + 3 + tiles * s / 16
+        splits = 1
+        for s in range(2, min(16, nk) + 1):
+            if cost(s) < cost(splits):
+                splits = s
     return tail * splits * 65536 if splits >= 2 else 0
+
+
+def test_split_plan_examples():
+    """A few plans worked out by hand: a partial last wave of 80 tiles splits
+    3 ways; 48 tiles with K = 12288 split 5 ways (240 workgroups, one wave);
+    144 tiles split 3 ways (2 waves of a third of K each)."""
+    assert tail_split(2048, 10752, 12288) == 80 * 3 * 65536
+    assert tail_split(2048, 1536, 12288) == 48 * 5 * 65536
+    assert tail_split(2048, 4608, 12288) == 144 * 3 * 65536
+    assert tail_split(2048, 4608, 12288, bf16=False) == 0
+    assert tail_split(128, 256, 256) == 0  # one tile, four K-steps: not worth a reduction
 
 
 @pytest.mark.parametrize("name", sorted(WORKLOADS))

@@ -29,8 +29,10 @@ def test_gemm_grid_matches_the_split_plan():
     assert bench.gemm_grid_threads(*steps["out_proj"]) == (256 + 128 * 2) * 512
     # in_proj: 8 x 42 = 336 tiles -> 256 + 80 tail tiles split 3 ways
     assert bench.gemm_grid_threads(*steps["in_proj"]) == (256 + 80 * 3) * 512
-    # no whole wave: unsplit
-    assert bench.gemm_grid_threads(512, 512, 4096) == 4 * 512
+    # fewer tiles than CUs: 4 tiles, 64 K-steps -> 16 slices of 4 K-steps
+    assert bench.gemm_grid_threads(512, 512, 4096) == 4 * 16 * 512
+    # one tile, four K-steps: a reduction would cost more than it saves
+    assert bench.gemm_grid_threads(128, 256, 256) == 512
     # K not a multiple of 64: unsplit
     assert bench.gemm_grid_threads(2048, 12288 + 256, 1000) == 8 * 49 * 512
 
@@ -66,3 +68,21 @@ def test_committed_traffic_profile_parses():
     assert "rocprofv3 --pmc FETCH_SIZE" in text and "rocprofv3 --pmc WRITE_SIZE" in text
     rec = json.loads(text.split("```json\n")[1].split("\n```")[0])
     assert rec["traffic_bytes"] > 0 and rec["algorithmic_bytes"] > 0
+
+
+def test_serial_gemm_steps_are_labelled():
+    """Every GEMM of the serial block is found by kernel template and grid;
+    dW_down and dW_up (1152 tiles each, same template) share a label."""
+    s = WORKLOADS["175b_tp8_share"]
+    steps = bench.gemm_steps(s, "serial")
+    assert len(steps) == 12
+    sig = {k: bench.GEMM_SIGNATURE[k] for k in steps}
+    labels = set()
+    for st, mnk in steps.items():
+        name = f"void pb::(anonymous namespace)::gemm_bf16_dma_kernel{sig[st]}, true>()"
+        lab = bench.gemm_step_of(name, bench.gemm_grid_threads(*mnk), s, "serial")
+        assert st in lab.split("/"), (st, lab)
+        labels.add(lab)
+    assert "dw_down/dw_up" in labels
+    # 48 tiles of the dO GEMM, K = 12288: 5 slices each
+    assert bench.split_plan(*steps["d_o"]) == (0, 48, 5)
