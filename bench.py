@@ -13,6 +13,9 @@ Prints one JSON line.  Besides the contract fields it carries:
                 inside the timed steps;
   steps         per-step times from a separate pass with events around every
                 step;
+  lamb_step     one fused LAMB optimizer step over the block's parameters
+                (fp32 master weights and moments, the step's own gradients,
+                bf16 copy), against the HBM peak;
   serial_block  the standard two-LayerNorm block on the same workload and
                 kernels (same model FLOPs), and the parallel block's speedup
                 over it;
@@ -81,10 +84,11 @@ KERNEL_SOURCES = {
     "gemm": ["gemm.hip", "common.h", "kernels.h"],
     "attn": ["attn.hip", "common.h", "kernels.h"],
     "ln": ["ln.hip", "common.h", "kernels.h"],
+    "lamb": ["lamb.hip", "common.h", "kernels.h"],
 }
 STEP_SOURCE = {"in_proj": "gemm", "out_proj": "gemm", "dc": "gemm", "dw_out": "gemm", "dh": "gemm",
                "dw_in": "gemm", "attn_fwd": "attn", "attn_bwd": "attn", "ln_fwd": "ln",
-               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln"}
+               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln", "lamb": "lamb"}
 COPY_BYTES = 1 << 30  # read and written once by the calibration copy
 
 
@@ -228,6 +232,37 @@ def traffic_summary(dirs, workload, step):
     return rec
 
 
+def lamb_traffic_summary(dirs, workload):
+    """FETCH_SIZE / WRITE_SIZE per dispatch of the LAMB step's two streaming
+    kernels over the block's parameters, scaled by the calibration copy, next
+    to their algorithmic bytes."""
+    import numpy as np
+    from paper_2402_15627_amd.inputs import WORKLOADS, block_param_shapes
+    s = WORKLOADS[workload]
+    elements = sum(int(np.prod(sh)) for sh in block_param_shapes(s).values())
+    copy_pick = lambda r: "neg_kernel" in r["Kernel_Name"]  # noqa: E731
+    cfetch, _ = _per_dispatch(_counter_rows(dirs[2]), "FETCH_SIZE", copy_pick)
+    cwrite, _ = _per_dispatch(_counter_rows(dirs[3]), "WRITE_SIZE", copy_pick)
+    ff, wf = COPY_BYTES / 1024 / cfetch, COPY_BYTES / 1024 / cwrite
+    rec = {"step": "lamb", "workload": workload, "elements": elements, "copy_bytes": COPY_BYTES,
+           "copy_fetch_kib": round(cfetch, 1), "copy_write_kib": round(cwrite, 1),
+           "fetch_scale": round(ff, 4), "write_scale": round(wf, 4), "kernels": {}}
+    total = 0
+    for kern, (rd, wr) in {"lamb_moments": (16, 8), "lamb_apply": (12, 6)}.items():
+        pick = lambda r, k=kern: k in r["Kernel_Name"]  # noqa: E731
+        fetch, n1 = _per_dispatch(_counter_rows(dirs[0]), "FETCH_SIZE", pick)
+        write, n2 = _per_dispatch(_counter_rows(dirs[1]), "WRITE_SIZE", pick)
+        tb = int(fetch * 1024 * ff + write * 1024 * wf)
+        total += tb
+        rec["kernels"][kern] = {"dispatches": [n1, n2], "fetch_kib": round(fetch, 1),
+                                "write_kib": round(write, 1), "traffic_bytes": tb,
+                                "algorithmic_bytes": (rd + wr) * elements}
+    rec["traffic_bytes"] = total
+    rec["algorithmic_bytes"] = LAMB_BYTES_PER_ELEMENT * elements
+    rec["source_fingerprint"] = source_fingerprint("lamb")
+    return rec
+
+
 def read_traffic(step, workload):
     """Measured HBM bytes per launch from profiles/, if the sources still match."""
     try:
@@ -305,6 +340,59 @@ def cpu_baseline(shape, inputs, min_seconds=10.0, max_steps=6):
                       f"matmul), same seeded inputs as the GPU run"}
 
 
+LAMB_BYTES_PER_ELEMENT = 42  # moments pass 16 read + 8 written; update pass 12 read + 4 + 2 written
+
+
+def time_lamb(pb, shape, warmup, steps, grads=None):
+    """One LAMB step over the parallel block's six parameter tensors (fp32
+    master weights, moments and gradients; the bf16 model weights written as
+    the copy), timed with events around `steps` consecutive steps."""
+    import numpy as np
+    import torch
+    from paper_2402_15627_amd.inputs import block_param_shapes, make_lamb_state
+    shapes = block_param_shapes(shape)
+    st = {}
+    if grads is None:
+        st = make_lamb_state({n: (int(np.prod(sh)),) for n, sh in shapes.items()}, seed=0,
+                             w_std=shape.w_std)
+    bufs, ts = [], []
+    for n, sh in shapes.items():
+        numel = int(np.prod(sh))
+        if grads is None:
+            w, g, m, v = (torch.from_numpy(st[n][k]).cuda() for k in ("w", "g", "m", "v"))
+        else:
+            w = torch.randn(numel, device="cuda") * shape.w_std
+            g = grads[n].reshape(-1)
+            m = torch.zeros(numel, device="cuda")
+            v = torch.zeros(numel, device="cuda")
+        copy = torch.empty(numel, dtype=torch.bfloat16, device="cuda")
+        bufs.append((w, g, m, v, copy))
+        ts.append(pb.lamb_tensor(w, g, m, v, copy, 0.0 if n.startswith(("b_", "gamma", "beta"))
+                                 else 0.01))
+    ws = torch.empty(pb.pblock_lamb_workspace_bytes(ts), dtype=torch.uint8, device="cuda")
+    elements = sum(int(np.prod(sh)) for sh in shapes.values())
+
+    def step(t):
+        pb.pblock_lamb_step(pb.lamb_config(1e-3, step=t), ts, pb.PB_BF16, None, ws)
+
+    for i in range(warmup):
+        step(i + 1)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        step(warmup + i + 1)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    nbytes = LAMB_BYTES_PER_ELEMENT * elements
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"ms": round(ms, 4), "elements": elements, "bytes_per_step": nbytes,
+            "achieved_gbs": round(gbs, 1), "peak_gbs": PEAK_HBM_GBS,
+            "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": read_traffic("lamb", shape.name)}
+
+
 def time_serial(pb, shape, warmup, steps, parallel_ms, flops):
     """The standard block (two LayerNorms, four projections; the same model
     FLOPs) on the same workload and kernels, timed like the parallel block:
@@ -341,16 +429,20 @@ def main():
     ap.add_argument("--workload", default="175b_tp8_share")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
-    ap.add_argument("--block", choices=("parallel", "serial"), default="parallel",
-                    help="serial: time only the standard two-LayerNorm block (for profiling)")
+    ap.add_argument("--block", choices=("parallel", "serial", "lamb"), default="parallel",
+                    help="serial: time only the standard two-LayerNorm block; lamb: only the "
+                         "LAMB step over the block's parameters (for profiling)")
     ap.add_argument("--no-serial", action="store_true",
                     help="skip timing the serial (two-LayerNorm) block for comparison")
+    ap.add_argument("--no-lamb", action="store_true",
+                    help="skip timing the LAMB step over the block's parameters")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run the counter calibration copy and exit")
     ap.add_argument("--traffic-summary", nargs=4, metavar="DIR",
                     help="rocprofv3 --pmc output dirs: FETCH_SIZE and WRITE_SIZE of the bench, "
                          "then of --copy-calibration; writes profiles/<step>_<workload>_traffic.md")
-    ap.add_argument("--traffic-step", default="dw_in")
+    ap.add_argument("--traffic-step", default="dw_in",
+                    help="a GEMM step, or lamb (the LAMB step's two streaming kernels)")
     ap.add_argument("--trace-summary", metavar="DIR",
                     help="print a markdown table of a rocprofv3 --kernel-trace output dir")
     ap.add_argument("--command", default="", help="command line recorded with a summary")
@@ -359,12 +451,17 @@ def main():
         print(trace_summary(args.trace_summary, args.workload, args.block))
         return
     if args.traffic_summary:
-        rec = traffic_summary(args.traffic_summary, args.workload, args.traffic_step)
+        if args.traffic_step == "lamb":
+            rec = lamb_traffic_summary(args.traffic_summary, args.workload)
+            what = "the LAMB step's moments and update kernels"
+        else:
+            rec = traffic_summary(args.traffic_summary, args.workload, args.traffic_step)
+            what = f"the {args.traffic_step} GEMM"
         path = traffic_path(args.traffic_step, args.workload)
         with open(path, "w") as fh:
-            fh.write(f"# HBM traffic of the {args.traffic_step} GEMM, {args.workload}\n\n"
+            fh.write(f"# HBM traffic of {what}, {args.workload}\n\n"
                      "FETCH_SIZE and WRITE_SIZE (KiB per dispatch, rocprofv3 --pmc, one counter "
-                     "per run) of the launches with this step's grid, each scaled by "
+                     "per run) of the matching launches, each scaled by "
                      f"{COPY_BYTES} bytes over what the same counter reads for one dispatch of "
                      "the calibration copy (a read-once, write-once elementwise kernel).\n\n"
                      f"Commands (repository root on the GPU host):\n\n```\n{args.command}\n```\n\n"
@@ -394,6 +491,11 @@ def main():
 
     shape = WORKLOADS[args.workload]
     pb.load_library()
+    if args.block == "lamb":
+        rec = time_lamb(pb, shape, args.warmup, args.steps)
+        print(json.dumps({"block": "lamb", "workload": shape.name, "steps": args.steps,
+                          "warmup": args.warmup, **rec}), flush=True)
+        return
     if args.block == "serial":
         flops = model_flops(shape)
         rec = time_serial(pb, shape, args.warmup, args.steps, None, flops)
@@ -500,6 +602,11 @@ def main():
     }
     if not args.no_serial:
         out["serial_block"] = time_serial(pb, shape, args.warmup, K, ms, flops)
+    if not args.no_lamb:
+        names = ("w_in", "b_in", "w_out", "b_out", "gamma", "beta")
+        gmap = dict(zip(names, (blk.grads[k] for k in ("dw_in", "db_in", "dw_out", "db_out",
+                                                         "dgamma", "dbeta"))))
+        out["lamb_step"] = time_lamb(pb, shape, args.warmup, K, gmap)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, inputs)
     print(json.dumps(out), flush=True)

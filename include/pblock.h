@@ -235,6 +235,59 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
                                  void* dk, void* dv, int ld_dqkv, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------- LAMB step
+ * One step of the LAMB optimizer the paper trains with (Section 3.1, "LAMB
+ * optimizer"; the layer-wise method of You et al., 2020) over up to
+ * PB_LAMB_MAX_TENSORS tensors, each its own trust-ratio "layer".  For each
+ * tensor, with t = cfg->step:
+ *
+ *   g  = grad_scale * grad
+ *   m  = beta1 m + (1 - beta1) g,   v = beta2 v + (1 - beta2) g^2
+ *   u  = (m / c1) / (sqrt(v / c2) + eps) + weight_decay * w
+ *        c1 = 1 - beta1^t, c2 = 1 - beta2^t (1 and 1 when bias_correction = 0)
+ *   r  = ||w|| / ||u|| over the whole tensor (1 if either norm is 0)
+ *   w  = w - lr * r * u
+ *
+ * param, exp_avg (m) and exp_avg_sq (v) are fp32 and updated in place; grad
+ * is fp32 (as pblock_backward writes it).  param_copy, when not NULL,
+ * receives the updated weights in copy_dtype (bf16: round to nearest even),
+ * e.g. the block's bf16 parameters.  Every pointer is device memory, 16-byte
+ * aligned; the five arrays of a tensor must not overlap.  trust_ratio, when
+ * not NULL, is a device array of n_tensors floats that receives r.
+ * Tensors with numel = 0 are allowed (nothing is touched).  More tensors:
+ * call again; tensors are independent, so the result is the same.
+ *
+ * ws must hold pblock_lamb_workspace_bytes(n_tensors, tensors) bytes (per-
+ * chunk partial norms and the ratios).  Asynchronous on the stream; the
+ * result does not depend on timing (fixed reduction order, no atomics).
+ * Errors: PB_ERR_INVALID_ARG for a bad config (lr or grad_scale not finite,
+ * beta outside [0, 1), eps <= 0, step < 1, negative or non-finite decay,
+ * n_tensors outside 1..16), a NULL or misaligned pointer, or too many
+ * elements; PB_ERR_WORKSPACE for a small ws. */
+#define PB_LAMB_MAX_TENSORS 16
+typedef struct {
+  float lr;
+  float beta1, beta2;
+  float eps;
+  float grad_scale;
+  int step;            /* t >= 1 */
+  int bias_correction; /* 0 or 1 */
+} pb_lamb_config;
+typedef struct {
+  float* param;        /* [numel] fp32 master weights */
+  const float* grad;   /* [numel] fp32 */
+  float* exp_avg;      /* [numel] fp32 */
+  float* exp_avg_sq;   /* [numel] fp32 */
+  void* param_copy;    /* NULL or [numel] in copy_dtype */
+  size_t numel;
+  float weight_decay;  /* lambda of this tensor (0 for biases and norms, say) */
+} pb_lamb_tensor;
+size_t pblock_lamb_workspace_bytes(int n_tensors, const pb_lamb_tensor* tensors);
+pb_status pblock_lamb_step(const pb_lamb_config* cfg, int n_tensors,
+                           const pb_lamb_tensor* tensors, pb_dtype copy_dtype,
+                           float* trust_ratio, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
 /* Steps of the forward and backward passes, for pblock_set_step_events. */
 typedef enum {
   PB_STEP_LN_FWD = 0, /* LayerNorm of x                                     */

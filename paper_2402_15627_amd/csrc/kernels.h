@@ -36,6 +36,38 @@ void launch_colsum(Dt dt, const void* src, int ld, int rows, int cols, float* pa
 void launch_colsum_f32(const float* src, int ld, int rows, int cols, float* part, float* out,
                        hipStream_t s);
 
+// -------------------------------------------------------------- LAMB step
+// One LAMB step over up to kLambMaxTensors fp32 tensors, each with its own
+// trust ratio.  Elements are processed in chunks of kLambChunk per
+// workgroup.  Tensor i owns chunks [chunk0[i], chunk_end[i]); chunk0[i] is a
+// multiple of kLambGroup (chunks up to the next boundary are padding) and
+// chunk0[n] is the padded total.
+constexpr int kLambMaxTensors = 16;
+constexpr int kLambChunk = 1024;
+constexpr int kLambGroup = 256;
+struct LambTable {
+  float* w[kLambMaxTensors];
+  const float* g[kLambMaxTensors];
+  float* m[kLambMaxTensors];
+  float* v[kLambMaxTensors];
+  void* copy[kLambMaxTensors];  // nullptr: no copy of this tensor
+  long long numel[kLambMaxTensors];
+  float wd[kLambMaxTensors];
+  int chunk0[kLambMaxTensors + 1];
+  int chunk_end[kLambMaxTensors];
+  int n;
+};
+struct LambScalars {
+  float lr, beta1, beta2, eps, grad_scale;
+  float c1, c2;  // 1 / (1 - beta^t), or 1 without bias correction
+};
+int lamb_chunks(long long numel);
+int lamb_padded_chunks(long long numel);  // rounded up to a multiple of kLambGroup
+// partial: chunk0[n] float2; group: chunk0[n] / kLambGroup double2; ratio:
+// n floats (all workspace); ratio_out: n floats or nullptr.
+void launch_lamb(const LambTable& t, const LambScalars& sc, Dt copy_dt, float2* partial,
+                 double2* group, float* ratio, float* ratio_out, hipStream_t s);
+
 // ------------------------------------------------------------------ GEMMs
 // C[m, n] = sum_k A(m, k) B(k, n), fp32 accumulation.
 // A(m, k) is A[m * lda + k] when a_kcontig, else A[k * lda + m]; B(k, n) is

@@ -5,6 +5,8 @@
 
 #include <math.h>
 
+#include <cmath>
+
 #include <algorithm>
 #include <array>
 #include <initializer_list>
@@ -908,6 +910,95 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   w.out = dw_in;  // dW_qkv = dQKV^T h1
   pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h1, H, 3 * A, H, T, w, split_ws,
                   split_f, stream);
+  return finish_launches();
+}
+
+// ---------------------------------------------------------------- LAMB step
+static_assert(PB_LAMB_MAX_TENSORS == pb::kLambMaxTensors, "tensor limit");
+
+size_t pblock_lamb_workspace_bytes(int n_tensors, const pb_lamb_tensor* tensors) {
+  if (n_tensors < 1 || n_tensors > PB_LAMB_MAX_TENSORS || !tensors) return 0;
+  long long chunks = 0;
+  for (int i = 0; i < n_tensors; ++i) chunks += pb::lamb_padded_chunks((long long)tensors[i].numel);
+  if (chunks > INT32_MAX) return 0;
+  return align256((size_t)chunks * sizeof(float2)) +
+         align256((size_t)(chunks / pb::kLambGroup) * sizeof(double2)) +
+         align256((size_t)n_tensors * 4);
+}
+
+pb_status pblock_lamb_step(const pb_lamb_config* cfg, int n_tensors,
+                           const pb_lamb_tensor* tensors, pb_dtype copy_dtype,
+                           float* trust_ratio, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!cfg) return fail(PB_ERR_INVALID_ARG, "cfg is NULL");
+  if (!std::isfinite(cfg->lr)) return fail(PB_ERR_INVALID_ARG, "lr is not finite");
+  if (!(cfg->beta1 >= 0.f && cfg->beta1 < 1.f) || !(cfg->beta2 >= 0.f && cfg->beta2 < 1.f))
+    return fail(PB_ERR_INVALID_ARG, "beta1=%g, beta2=%g: each must be in [0, 1)",
+                (double)cfg->beta1, (double)cfg->beta2);
+  if (!(cfg->eps > 0.f) || !std::isfinite(cfg->eps))
+    return fail(PB_ERR_INVALID_ARG, "eps=%g must be positive and finite", (double)cfg->eps);
+  if (!std::isfinite(cfg->grad_scale)) return fail(PB_ERR_INVALID_ARG, "grad_scale is not finite");
+  if (cfg->step < 1) return fail(PB_ERR_INVALID_ARG, "step=%d must be >= 1", cfg->step);
+  if (cfg->bias_correction != 0 && cfg->bias_correction != 1)
+    return fail(PB_ERR_INVALID_ARG, "bias_correction must be 0 or 1");
+  if (copy_dtype != PB_BF16 && copy_dtype != PB_F32)
+    return fail(PB_ERR_INVALID_ARG, "copy_dtype=%d", (int)copy_dtype);
+  if (n_tensors < 1 || n_tensors > PB_LAMB_MAX_TENSORS)
+    return fail(PB_ERR_INVALID_ARG, "n_tensors=%d must be in 1..%d", n_tensors,
+                PB_LAMB_MAX_TENSORS);
+  if (!tensors) return fail(PB_ERR_INVALID_ARG, "tensors is NULL");
+  pb::LambTable t{};
+  t.n = n_tensors;
+  long long chunks = 0;
+  for (int i = 0; i < n_tensors; ++i) {
+    const pb_lamb_tensor& x = tensors[i];
+    if (!(x.weight_decay >= 0.f) || !std::isfinite(x.weight_decay))
+      return fail(PB_ERR_INVALID_ARG, "tensor %d: weight_decay=%g", i, (double)x.weight_decay);
+    if (x.numel > 0) {
+      const char* names[4] = {"param", "grad", "exp_avg", "exp_avg_sq"};
+      const void* ptrs[4] = {x.param, x.grad, x.exp_avg, x.exp_avg_sq};
+      for (int k = 0; k < 4; ++k)
+        if (!ptrs[k] || (uintptr_t)ptrs[k] % 16)
+          return fail(PB_ERR_INVALID_ARG, "tensor %d: %s is NULL or not 16-byte aligned", i,
+                      names[k]);
+      if (x.param_copy && (uintptr_t)x.param_copy % 16)
+        return fail(PB_ERR_INVALID_ARG, "tensor %d: param_copy is not 16-byte aligned", i);
+    }
+    t.w[i] = x.param;
+    t.g[i] = x.grad;
+    t.m[i] = x.exp_avg;
+    t.v[i] = x.exp_avg_sq;
+    t.copy[i] = x.numel > 0 ? x.param_copy : nullptr;
+    t.numel[i] = (long long)x.numel;
+    t.wd[i] = x.weight_decay;
+    t.chunk0[i] = (int)chunks;
+    t.chunk_end[i] = (int)std::min<long long>(chunks + pb::lamb_chunks((long long)x.numel),
+                                              INT32_MAX);
+    chunks += pb::lamb_padded_chunks((long long)x.numel);
+    if (chunks > INT32_MAX) return fail(PB_ERR_INVALID_ARG, "too many elements in one call");
+  }
+  t.chunk0[n_tensors] = (int)chunks;
+  if (trust_ratio && (uintptr_t)trust_ratio % 4)
+    return fail(PB_ERR_INVALID_ARG, "trust_ratio is not 4-byte aligned");
+  const size_t need = pblock_lamb_workspace_bytes(n_tensors, tensors);
+  if (!ws || (uintptr_t)ws % 256)
+    return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
+  if (ws_bytes < need) return fail(PB_ERR_WORKSPACE, "ws_bytes=%zu < %zu needed", ws_bytes, need);
+  pb::LambScalars sc;
+  sc.lr = cfg->lr;
+  sc.beta1 = cfg->beta1;
+  sc.beta2 = cfg->beta2;
+  sc.eps = cfg->eps;
+  sc.grad_scale = cfg->grad_scale;
+  sc.c1 = cfg->bias_correction ? (float)(1.0 / (1.0 - pow((double)cfg->beta1, cfg->step))) : 1.f;
+  sc.c2 = cfg->bias_correction ? (float)(1.0 / (1.0 - pow((double)cfg->beta2, cfg->step))) : 1.f;
+  char* wsb = (char*)ws;
+  float2* partial = (float2*)wsb;
+  wsb += align256((size_t)chunks * sizeof(float2));
+  double2* group = (double2*)wsb;
+  wsb += align256((size_t)(chunks / pb::kLambGroup) * sizeof(double2));
+  float* ratio = (float*)wsb;
+  pb::launch_lamb(t, sc, copy_dtype == PB_BF16 ? pb::Dt::BF16 : pb::Dt::F32, partial, group,
+                  ratio, trust_ratio, stream);
   return finish_launches();
 }
 

@@ -157,3 +157,37 @@ def make_inputs(s: BlockShape, seed: int = 0, serial: bool = False) -> dict[str,
         out["beta2"] = draw((H,), s.beta_std)
         out["b_down"] = draw((H,), s.w_std)
     return out
+
+
+def block_param_shapes(s: BlockShape) -> dict[str, tuple]:
+    """Parameter shapes of the parallel block, in the library's packed layout."""
+    H = s.hidden
+    return {"w_in": (s.n_in, H), "b_in": (s.n_in,), "w_out": (H, s.k_out), "b_out": (H,),
+            "gamma": (H,), "beta": (H,)}
+
+
+def make_lamb_state(shapes: dict, seed: int = 0, w_std: float = 0.02,
+                    g_std: float = 1e-3) -> dict[str, dict[str, np.ndarray]]:
+    """Seeded optimizer state for a LAMB step: per tensor, fp32 master
+    weights w with standard deviation w_std around 0 (around 1 for
+    gamma-like tensors, named "gamma*"), gradient g with standard deviation
+    g_std, first moment m with g_std / 3, and second moment v = (g_std z)^2
+    for a unit-variance z (non-negative, of the size a running average of
+    g^2 has).  The draws are uniform with the stated standard deviation
+    (uniform draws keep the full-size state, ~10^9 values, quick to make);
+    tensors are drawn in the order given, each w, g, m, v in turn, from
+    numpy.random.default_rng(seed)."""
+    rng = np.random.default_rng(seed)
+    half = np.float32(np.sqrt(3.0))  # a uniform draw on [-sqrt 3, sqrt 3] has unit variance
+    out = {}
+    for name, shape in shapes.items():
+        def draw(std, mean=0.0):
+            z = rng.random(size=shape, dtype=np.float32)
+            z = (2.0 * z - 1.0) * half
+            return (np.float32(mean) + np.float32(std) * z).astype(np.float32)
+        w = draw(w_std, 1.0 if name.startswith("gamma") else 0.0)
+        g = draw(g_std)
+        m = draw(g_std / 3)
+        v = np.square(draw(g_std))
+        out[name] = {"w": w, "g": g, "m": m, "v": v}
+    return out

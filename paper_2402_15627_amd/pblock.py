@@ -33,8 +33,9 @@ EXPORTS = (
     "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_set_step_events",
     "pblock_status_string", "pblock_last_error", "pblock_serial_saved_bytes",
     "pblock_serial_saved_offsets", "pblock_serial_workspace_bytes", "pblock_serial_forward",
-    "pblock_serial_backward",
+    "pblock_serial_backward", "pblock_lamb_workspace_bytes", "pblock_lamb_step",
 )
+LAMB_MAX_TENSORS = 16
 
 # pb_step order of include/pblock.h
 STEPS = ("ln_fwd", "in_proj", "attn_fwd", "out_proj", "dc", "dw_out", "db_out", "attn_bwd", "dh",
@@ -45,6 +46,19 @@ class PbConfig(ctypes.Structure):
     _fields_ = [("batch", c_int), ("seq", c_int), ("hidden", c_int), ("heads", c_int),
                 ("head_dim", c_int), ("ffn", c_int), ("window", c_int), ("ln_eps", c_float),
                 ("gelu_tanh", c_int), ("dtype", c_int)]
+
+
+class LambConfig(ctypes.Structure):
+    """pb_lamb_config."""
+    _fields_ = [("lr", c_float), ("beta1", c_float), ("beta2", c_float), ("eps", c_float),
+                ("grad_scale", c_float), ("step", c_int), ("bias_correction", c_int)]
+
+
+class LambTensor(ctypes.Structure):
+    """pb_lamb_tensor (device addresses as integers)."""
+    _fields_ = [("param", c_void_p), ("grad", c_void_p), ("exp_avg", c_void_p),
+                ("exp_avg_sq", c_void_p), ("param_copy", c_void_p), ("numel", c_size_t),
+                ("weight_decay", c_float)]
 
 
 class PblockError(RuntimeError):
@@ -87,6 +101,9 @@ def load_library(path: str = LIB_PATH):
         "pblock_serial_workspace_bytes": (c_size_t, [cfgp, c_int]),
         "pblock_serial_forward": (c_int, [cfgp] + [P] * 13 + [c_size_t, P]),
         "pblock_serial_backward": (c_int, [cfgp] + [P] * 23 + [c_size_t, P]),
+        "pblock_lamb_workspace_bytes": (c_size_t, [c_int, POINTER(LambTensor)]),
+        "pblock_lamb_step": (c_int, [POINTER(LambConfig), c_int, POINTER(LambTensor), c_int, P, P,
+                                     c_size_t, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -237,6 +254,35 @@ def pblock_serial_backward(cfg, x, ln1_gamma, ln1_beta, ln2_gamma, ln2_beta, w_i
         _ptr(saved), _ptr(dy), _ptr(dx), _ptr(dln1_gamma), _ptr(dln1_beta), _ptr(dln2_gamma),
         _ptr(dln2_beta), _ptr(dw_in), _ptr(db_in), _ptr(dw_out), _ptr(db_o), _ptr(db_down),
         _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def lamb_config(lr, beta1=0.9, beta2=0.999, eps=1e-6, step=1, bias_correction=True,
+                grad_scale=1.0) -> LambConfig:
+    return LambConfig(lr, beta1, beta2, eps, grad_scale, int(step), int(bool(bias_correction)))
+
+
+def lamb_tensor(param, grad, exp_avg, exp_avg_sq, param_copy=None, weight_decay=0.0):
+    """A pb_lamb_tensor from torch tensors (fp32 param, grad and moments of
+    equal size; an optional copy of the same size)."""
+    return LambTensor(_ptr(param), _ptr(grad), _ptr(exp_avg), _ptr(exp_avg_sq),
+                      _ptr(param_copy), param.numel(), weight_decay)
+
+
+def _lamb_array(tensors):
+    arr = (LambTensor * len(tensors))(*tensors)
+    return arr
+
+
+def pblock_lamb_workspace_bytes(tensors) -> int:
+    """tensors: a sequence of LambTensor."""
+    return load_library().pblock_lamb_workspace_bytes(len(tensors), _lamb_array(tensors))
+
+
+def pblock_lamb_step(cfg: LambConfig, tensors, copy_dtype=PB_BF16, trust_ratio=None, ws=None,
+                     stream=None):
+    _check(load_library().pblock_lamb_step(
+        ctypes.byref(cfg), len(tensors), _lamb_array(tensors), int(copy_dtype),
+        _ptr(trust_ratio), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
 def pblock_status_string(status: int) -> str:

@@ -279,3 +279,35 @@ def test_serial_rejects_bad_arguments_before_launching():
     bad_cfg = good_cfg(head_dim=96)
     assert pb.pblock_serial_saved_bytes(bad_cfg) == 0
     assert pb.pblock_serial_workspace_bytes(bad_cfg, pb.WS_BACKWARD) == 0
+
+
+def test_lamb_workspace_and_validation():
+    T = pb.LambTensor
+    ts = [T(FAKE, FAKE, FAKE, FAKE, None, 8192 * 3 + 5, 0.01), T(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0.0)]
+    # chunks of 1024 elements, each tensor's chunks padded to a group of 256:
+    # 256 float2 partials, one double2 group sum, two ratios
+    assert pb.pblock_lamb_workspace_bytes(ts) == align(256 * 8) + align(16) + align(2 * 4)
+    assert pb.pblock_lamb_workspace_bytes([]) == 0
+    assert pb.pblock_lamb_workspace_bytes([ts[0]] * 17) == 0
+    lib = pb.load_library()
+    good = pb.lamb_config(1e-3, step=1)
+
+    def call(cfg=good, tensors=ts, copy=pb.PB_BF16, ws=FAKE, nbytes=1 << 20):
+        arr = (pb.LambTensor * len(tensors))(*tensors)
+        return lib.pblock_lamb_step(ctypes.byref(cfg), len(tensors), arr, copy, None, ws, nbytes,
+                                    None)
+
+    assert call(nbytes=64) == 3 and "ws_bytes" in pb.pblock_last_error()
+    for bad in (pb.lamb_config(1e-3, beta1=1.0), pb.lamb_config(1e-3, eps=0.0),
+                pb.lamb_config(1e-3, step=0), pb.lamb_config(float("nan")),
+                pb.lamb_config(1e-3, beta2=-0.1)):
+        assert call(cfg=bad) == 1
+    assert call(copy=5) == 1
+    assert call(tensors=[T(FAKE, None, FAKE, FAKE, None, 16, 0.0)]) == 1
+    assert "grad" in pb.pblock_last_error()
+    assert call(tensors=[T(FAKE, FAKE, FAKE + 8, FAKE, None, 16, 0.0)]) == 1
+    assert call(tensors=[T(FAKE, FAKE, FAKE, FAKE, FAKE + 2, 16, 0.0)]) == 1
+    assert call(tensors=[T(FAKE, FAKE, FAKE, FAKE, None, 16, -1.0)]) == 1
+    # empty tensors need no pointers
+    assert pb.pblock_lamb_workspace_bytes([T(None, None, None, None, None, 0, 0.0)]) == align(4)
+    assert call(ws=FAKE + 16) == 1
