@@ -92,7 +92,7 @@ typedef struct {
   int seq;       /* >= 1                                                    */
   int hidden;    /* H >= 8, multiple of 8, <= 32768                         */
   int heads;     /* >= 1                                                    */
-  int head_dim;  /* 64 or 128                                               */
+  int head_dim;  /* 64, 96 or 128                                           */
   int ffn;       /* F >= 8, multiple of 8                                   */
   int window;    /* >= 1; keys seen per query, itself included              */
   float ln_eps;  /* > 0, e.g. 1e-5                                          */

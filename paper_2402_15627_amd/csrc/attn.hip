@@ -70,10 +70,17 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 // per row, one 256-byte bank period) f is a 4-bit rotation of r that makes
 // both access patterns conflict-free: a 16-byte read by 16 consecutive rows
 // at one chunk, and a transposing read of 8 consecutive rows x 4 aligned
-// chunks.  D = 64 uses an injective 3-bit variant.
+// chunks.  D = 64 uses an injective 3-bit variant.  D = 96 (12 chunks, rows
+// 192 bytes apart): row r starts at bank group 12 r mod 16 = 4 (3 r mod 4),
+// so r mod 4 already spreads rows over the four quarters of the bank period;
+// f(r) = (r / 4) mod 4 on the low two chunk bits (which keeps c below 12)
+// spreads them within a quarter.  16 rows at one chunk then hit 16 distinct
+// bank groups, and so do 4 consecutive rows x 4 aligned chunks.
 template <int D>
 PB_DEV int rowswz(int r) {
+  static_assert(D == 64 || D == 96 || D == 128, "head_dim");
   if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else if constexpr (D == 96) return (r >> 2) & 3;
   else return ((r & 1) << 2) | ((r >> 1) & 3);
 }
 template <int D>
@@ -107,16 +114,26 @@ PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" :
 // [rows_valid, ld] token-major matrix, by LDS-DMA (each lane's 16 bytes land
 // at the piece's LDS base + 16 * lane).  Rows past rows_valid are read from
 // the last valid row: finite values that the window mask always zeroes.
+// The tile is cut into 1 KB pieces (one DMA instruction each); with NW
+// dividing their number each wave moves a contiguous run, else piece i goes
+// to wave i mod NW.  dma_pieces is the number a wave issues.
+template <int D, int TL, int NW>
+__host__ __device__ constexpr int dma_pieces(int wave) {
+  constexpr int NP = TL * 2 * D / 1024;
+  return NP % NW == 0 ? NP / NW : (NP - wave + NW - 1) / NW;
+}
 template <int D, int TL, int NW>
 PB_DEV void dma_tile(const bf16* __restrict__ base, int ld, int row0, int rows_valid,
                      uint32_t lds_tile, int wave, int lane) {
   constexpr int RB = 2 * D;
   constexpr int BYTES = TL * RB;
-  constexpr int PER_WAVE = BYTES / NW;
-  static_assert(PER_WAVE % 1024 == 0, "each wave moves whole 1 KB pieces");
+  constexpr int NP = BYTES / 1024;
+  static_assert(BYTES % 1024 == 0, "tiles are whole 1 KB pieces");
 #pragma unroll
-  for (int i = 0; i < PER_WAVE / 1024; ++i) {
-    const int piece = wave * PER_WAVE + i * 1024;
+  for (int i = 0; i < (NP + NW - 1) / NW; ++i) {
+    const int pc = NP % NW == 0 ? wave * (NP / NW) + i : i * NW + wave;
+    if (NP % NW != 0 && pc >= NP) break;  // wave-uniform
+    const int piece = pc * 1024;
     const int p = piece + 16 * lane;
     const int row = p / RB, slot = (p / 16) % (RB / 16);
     const int c = chunk_at<D>(row, slot);
@@ -498,8 +515,7 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   // lse and 32 delta values (one 4-byte DMA by wave 0; rows past the end are
   // read from the last row: finite values that the mask always zeroes).
   // DMA instructions per wave per stage: dma_tile moves 1 KB pieces.
-  constexpr int kPiecesQ = TB / kWavesK / 1024;
-  const int per_stage = 2 * kPiecesQ + (wave == 0 ? 1 : 0);
+  const int per_stage = 2 * dma_pieces<D, TL, kWavesK>(wave) + (wave == 0 ? 1 : 0);
   const int nt = t_end - t_begin;
   auto issue_stage = [&](int i) {
     const int s = i % NS;
@@ -978,6 +994,7 @@ void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k
                          int ld_qkv, void* o, int ld_o, float* lse, void* part,
                          size_t part_bytes, hipStream_t s) {
   if (a.head_dim == 64) fwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, part, part_bytes, s);
+  else if (a.head_dim == 96) fwd_d<96>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, part, part_bytes, s);
   else fwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, lse, part, part_bytes, s);
 }
 
@@ -987,6 +1004,9 @@ void launch_attn_backward(Dt dt, const AttnShape& a, const void* q, const void* 
                           void* part, size_t part_bytes, hipStream_t s) {
   if (a.head_dim == 64)
     bwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
+              part_bytes, s);
+  else if (a.head_dim == 96)
+    bwd_d<96>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
               part_bytes, s);
   else
     bwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,

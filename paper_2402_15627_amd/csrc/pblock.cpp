@@ -83,8 +83,8 @@ pb_status check_config(const pb_config* c) {
                 c->hidden);
   if (c->ffn < 8 || c->ffn % 8)
     return fail(PB_ERR_INVALID_ARG, "ffn=%d must be a positive multiple of 8", c->ffn);
-  if (c->head_dim != 64 && c->head_dim != 128)
-    return fail(PB_ERR_UNSUPPORTED, "head_dim=%d: kernels exist for 64 and 128", c->head_dim);
+  if (c->head_dim != 64 && c->head_dim != 96 && c->head_dim != 128)
+    return fail(PB_ERR_UNSUPPORTED, "head_dim=%d: kernels exist for 64, 96 and 128", c->head_dim);
   if (!(c->ln_eps > 0.f) || !isfinite(c->ln_eps))
     return fail(PB_ERR_INVALID_ARG, "ln_eps must be finite and > 0");
   if (c->gelu_tanh != 0 && c->gelu_tanh != 1)
@@ -288,8 +288,8 @@ pb_status check_attn_config(const pb_config* c) {
     return fail(PB_ERR_INVALID_ARG, "dtype %d is neither PB_BF16 nor PB_F32", (int)c->dtype);
   if (c->batch < 1 || c->seq < 1 || c->heads < 1 || c->window < 1)
     return fail(PB_ERR_INVALID_ARG, "batch, seq, heads and window must be >= 1");
-  if (c->head_dim != 64 && c->head_dim != 128)
-    return fail(PB_ERR_UNSUPPORTED, "head_dim=%d: kernels exist for 64 and 128", c->head_dim);
+  if (c->head_dim != 64 && c->head_dim != 96 && c->head_dim != 128)
+    return fail(PB_ERR_UNSUPPORTED, "head_dim=%d: kernels exist for 64, 96 and 128", c->head_dim);
   if (c->heads > 65535 || c->batch > 65535)
     return fail(PB_ERR_UNSUPPORTED, "heads and batch must be <= 65535 (grid limits)");
   if ((long long)c->batch * c->seq * c->heads > kMaxInt)

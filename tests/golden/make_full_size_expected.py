@@ -24,7 +24,8 @@ sys.path.insert(0, ROOT)
 from oracle import pblock_oracle as orc  # noqa: E402
 from paper_2402_15627_amd.inputs import WORKLOADS, make_inputs  # noqa: E402
 
-FULL_SIZE = ("13b_shape", "175b_tp8_share", "175b_tp8_share_w512", "long_seq_8k", "175b_full")
+FULL_SIZE = ("13b_shape", "175b_tp8_share", "175b_tp8_share_w512", "long_seq_8k", "175b_full",
+             "175b_tp8_share_d96")
 
 
 def sample_rows(s):

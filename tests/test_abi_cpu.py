@@ -42,7 +42,7 @@ def good_cfg(**kw):
 
 @pytest.mark.parametrize("field,value,status", [
     ("hidden", 12, 1), ("hidden", 0, 1), ("ffn", 20, 1), ("batch", 0, 1),
-    ("seq", 0, 1), ("heads", 0, 1), ("window", 0, 1), ("head_dim", 96, 2), ("head_dim", 32, 2),
+    ("seq", 0, 1), ("heads", 0, 1), ("window", 0, 1), ("head_dim", 80, 2), ("head_dim", 32, 2),
     ("hidden", 40960, 2), ("gelu_tanh", 2, 1), ("dtype", 7, 1), ("ln_eps", 0.0, 1),
     ("ln_eps", float("nan"), 1),
 ])
@@ -276,7 +276,7 @@ def test_serial_rejects_bad_arguments_before_launching():
     bargs[21] = None  # db_down
     st = lib.pblock_serial_backward(ctypes.byref(c), *bargs, FAKE, need, None)
     assert st == 1 and "db_down" in pb.pblock_last_error()
-    bad_cfg = good_cfg(head_dim=96)
+    bad_cfg = good_cfg(head_dim=80)
     assert pb.pblock_serial_saved_bytes(bad_cfg) == 0
     assert pb.pblock_serial_workspace_bytes(bad_cfg, pb.WS_BACKWARD) == 0
 

@@ -38,6 +38,13 @@ CASES = [
     shape("bf16_d128_ragged_erf", batch=3, seq=161, hidden=392, heads=3, head_dim=128, ffn=200,
           window=129, gelu_tanh=False),
     shape("bf16_seq1", batch=4, seq=1, hidden=64, heads=1, head_dim=64, ffn=64, window=8),
+    # head_dim 96 (Table 1's 175B heads): 12-chunk rows, 6 K-steps, 3 output blocks
+    shape("bf16_d96_ragged", batch=2, seq=203, hidden=384, heads=3, head_dim=96, ffn=232,
+          window=71),
+    shape("bf16_d96_full_erf", batch=1, seq=300, hidden=192, heads=2, head_dim=96, ffn=128,
+          window=4096, gelu_tanh=False),
+    shape("f32_d96", batch=1, seq=77, hidden=96, heads=1, head_dim=96, ffn=64, window=20,
+          dtype="f32"),
     shape("bf16_w_edge_tiles", batch=1, seq=512, hidden=256, heads=2, head_dim=128, ffn=256,
           window=64),
     # in-projection: 3 x 86 = 258 output tiles, ragged in M and N: 256 whole
@@ -148,7 +155,7 @@ def test_repeat_runs_are_bitwise_identical():
 
 
 @pytest.mark.parametrize("W", [1, 5, 64, 65, 200, 10000])
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d", [64, 96, 128])
 def test_swattn_entry_points_match_oracle(W, d):
     """pblock_swattn_forward / _backward on q, k, v with padded rows, with the
     split workspace (B * heads is small, so long blocks are split) and
