@@ -102,6 +102,8 @@ WORKLOADS: dict[str, BlockShape] = {
         # Table 1's literal 175B heads (128 x 96): one of 8 ranks holds 16
         BlockShape("175b_tp8_share_d96", 1, 2048, 12288, 16, 96, 6144, 2048, "bf16",
                    w_std=0.006),
+        BlockShape("175b_full_d96", 1, 2048, 12288, 128, 96, 49152, 2048, "bf16",
+                   w_std=0.006),
     ]
 }
 

@@ -25,7 +25,7 @@ from oracle import pblock_oracle as orc  # noqa: E402
 from paper_2402_15627_amd.inputs import WORKLOADS, make_inputs  # noqa: E402
 
 FULL_SIZE = ("13b_shape", "175b_tp8_share", "175b_tp8_share_w512", "long_seq_8k", "175b_full",
-             "175b_tp8_share_d96")
+             "175b_tp8_share_d96", "175b_full_d96")
 
 
 def sample_rows(s):

@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
 HERE = os.path.dirname(os.path.abspath(__file__))
 GOLDEN = os.path.join(HERE, "golden")
 FULL = ["13b_shape", "175b_tp8_share", "175b_tp8_share_w512", "long_seq_8k", "175b_full",
-        "175b_tp8_share_d96"]
+        "175b_tp8_share_d96", "175b_full_d96"]
 
 
 def _say(msg):
