@@ -13,6 +13,9 @@ Prints one JSON line.  Besides the contract fields it carries:
                 inside the timed steps;
   steps         per-step times from a separate pass with events around every
                 step;
+  ag_in_proj    the in-projection pipelined with the all-gather of its input
+                over 8 ranks (one GPU: shards copied from local buffers),
+                against the GEMM alone and copies followed by one GEMM;
   lamb_step     one fused LAMB optimizer step over the block's parameters
                 (fp32 master weights and moments, the step's own gradients,
                 bf16 copy), against the HBM peak;
@@ -393,6 +396,56 @@ def time_lamb(pb, shape, warmup, steps, grads=None):
             "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": read_traffic("lamb", shape.name)}
 
 
+def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
+    """The in-projection pipelined with the all-gather of its input over tp
+    ranks (shards copied on comm streams, GEMM launches over groups of
+    shards as they land), against the GEMM alone and the copies followed by
+    one GEMM.  Each variant is timed with events on the compute stream."""
+    import torch
+    T, H = shape.tokens, shape.hidden
+    cfg = pb.config_from_shape(shape)
+    act = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    src = (torch.randn(T, H, device="cuda")).to(act)
+    h = torch.empty_like(src)
+    z = torch.empty(T, shape.n_in, dtype=act, device="cuda")
+    c = torch.empty(T, shape.k_out, dtype=act, device="cuda")
+    rows = T // tp
+    stream = torch.cuda.Stream()
+    comm = [torch.cuda.Stream() for _ in range(n_comm)]
+    out = {}
+
+    def timed(per, in_place):
+        nws = pb.pblock_ag_in_proj_workspace_bytes(cfg, tp, per)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
+        if in_place:
+            h.copy_(src)
+            shards = [h[j * rows:(j + 1) * rows] for j in range(tp)]
+        else:
+            shards = [src[j * rows:(j + 1) * rows] for j in range(tp)]
+        torch.cuda.synchronize()
+
+        def call():
+            pb.pblock_ag_in_proj(cfg, tp, 0, shards, h, dev["w_in"], dev["b_in"], z, c, per, ws,
+                                 stream, comm)
+        for _ in range(warmup):
+            call()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return round(e0.elapsed_time(e1) / steps, 4)
+
+    out["gemm_only_ms"] = timed(tp, True)
+    out["copies_then_gemm_ms"] = timed(tp, False)
+    for per in (1, 2, 4):
+        out[f"pipelined_{per}_shards_per_launch_ms"] = timed(per, False)
+    return {"tp": tp, "n_comm": n_comm, "shard_bytes": rows * H * src.element_size(), **out}
+
+
 def time_serial(pb, shape, warmup, steps, parallel_ms, flops):
     """The standard block (two LayerNorms, four projections; the same model
     FLOPs) on the same workload and kernels, timed like the parallel block:
@@ -434,6 +487,8 @@ def main():
                          "LAMB step over the block's parameters (for profiling)")
     ap.add_argument("--no-serial", action="store_true",
                     help="skip timing the serial (two-LayerNorm) block for comparison")
+    ap.add_argument("--no-ag", action="store_true",
+                    help="skip timing the in-projection pipelined with the all-gather")
     ap.add_argument("--no-lamb", action="store_true",
                     help="skip timing the LAMB step over the block's parameters")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -602,6 +657,8 @@ def main():
     }
     if not args.no_serial:
         out["serial_block"] = time_serial(pb, shape, args.warmup, K, ms, flops)
+    if not args.no_ag:
+        out["ag_in_proj"] = time_ag(pb, shape, dev, 2, 5)
     if not args.no_lamb:
         names = ("w_in", "b_in", "w_out", "b_out", "gamma", "beta")
         gmap = dict(zip(names, (blk.grads[k] for k in ("dw_in", "db_in", "dw_out", "db_out",

@@ -235,6 +235,44 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
                                  void* dk, void* dv, int ld_dqkv, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------- in-projection + all-gather
+ * Section 3.2 ("Overlapping in tensor/sequence parallelism", Fig. 3):
+ * under sequence parallelism the LayerNorm output h is sharded along the
+ * tokens over tp ranks and all-gathered before the column-parallel
+ * in-projection; the paper breaks that GEMM into chunks and pipelines them
+ * with the communication.  Here the shards are copied into h on the comm
+ * streams in ring order from `rank` (rank, rank + 1, ...; the k-th on
+ * comm_streams[k % n_comm]), and the in-projection runs on `stream` in
+ * launches of shards_per_launch shards each, every launch waiting (by
+ * event) only for its own shards.  shards_per_launch = tp is the
+ * unpipelined order: all copies, then one GEMM.
+ *
+ * shards[j]: rank j's rows of h, [T / tp, H] in the activation dtype (on
+ *   one GPU, buffers in local memory; across GPUs, peer memory opened by IPC
+ *   handles).  A shard already in place (shards[j] == h + j (T / tp) H) is
+ *   not copied.  h: [T, H], the gathered LN output.
+ * z [T, N_in], c [T, K_out]: written as pblock_forward writes the stash's
+ *   Z and the G half of C (bias, and GeLU of the MLP-up columns); the
+ *   result does not depend on tp, rank or the launch grouping beyond the
+ *   rounding of K-split tiles.
+ * Requirements: T % tp == 0, 1 <= tp <= 64, 0 <= rank < tp,
+ *   1 <= shards_per_launch <= tp, 1 <= n_comm <= 8, comm streams distinct
+ *   from each other and from `stream`.
+ * ws: optional GEMM split region of pblock_ag_in_proj_workspace_bytes(cfg,
+ *   tp, shards_per_launch) bytes (NULL/0 runs every launch unsplit).
+ * The copies start after the work already on `stream`; later work on
+ *   `stream` follows every copy and GEMM.  The library keeps 65 HIP events
+ *   per device for this call (created on first use): calls on one device
+ *   must not run concurrently from several host threads. */
+size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp,
+                                         int shards_per_launch);
+pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
+                            const void* const* shards, void* h,
+                            const void* w_in, const void* b_in, void* z,
+                            void* c, int shards_per_launch, void* ws,
+                            size_t ws_bytes, hipStream_t stream, int n_comm,
+                            const hipStream_t* comm_streams);
+
 /* ------------------------------------------------------------- LAMB step
  * One step of the LAMB optimizer the paper trains with (Section 3.1, "LAMB
  * optimizer"; the layer-wise method of You et al., 2020) over up to

@@ -913,6 +913,143 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   return finish_launches();
 }
 
+// -------------------------------------------- in-projection + all-gather
+namespace {
+constexpr int kAgMaxComm = 8;
+constexpr int kAgMaxTp = 64;
+constexpr int kAgMaxDevices = 64;
+// Events of the fused call, per device, created on first use.
+struct AgEvents {
+  bool ready = false;
+  hipEvent_t start;
+  hipEvent_t landed[kAgMaxTp];
+};
+AgEvents g_ag[kAgMaxDevices];
+
+// Largest GEMM split region over the launches of one call: row ranges of
+// m whole shards, m = 1 .. per_launch.
+size_t ag_split_bytes(const pb_config* cfg, int tp, int per_launch) {
+  const Dims d = dims_of(cfg);
+  const int rows = (int)(d.T / tp);
+  size_t m = 0;
+  for (int k = 1; k <= per_launch; ++k)
+    m = std::max(m, pb::gemm_split_floats(
+                        pb::gemm_split_plan(dt_of(cfg), rows * k, (int)d.N_in, (int)d.H)) *
+                        4);
+  return align256(m);
+}
+}  // namespace
+
+size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
+  if (check_config(cfg) != PB_OK || tp < 1 || tp > kAgMaxTp || shards_per_launch < 1 ||
+      shards_per_launch > tp || dims_of(cfg).T % tp)
+    return 0;
+  return ag_split_bytes(cfg, tp, shards_per_launch);
+}
+
+pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* const* shards,
+                            void* h, const void* w_in, const void* b_in, void* z, void* c,
+                            int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
+                            int n_comm, const hipStream_t* comm_streams) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  if (tp < 1 || tp > kAgMaxTp) return fail(PB_ERR_INVALID_ARG, "tp=%d must be in 1..64", tp);
+  if (rank < 0 || rank >= tp) return fail(PB_ERR_INVALID_ARG, "rank=%d not in 0..tp-1", rank);
+  if (d.T % tp) return fail(PB_ERR_INVALID_ARG, "tokens=%lld not divisible by tp=%d", d.T, tp);
+  if (shards_per_launch < 1 || shards_per_launch > tp)
+    return fail(PB_ERR_INVALID_ARG, "shards_per_launch=%d must be in 1..tp", shards_per_launch);
+  if (n_comm < 1 || n_comm > kAgMaxComm)
+    return fail(PB_ERR_INVALID_ARG, "n_comm=%d must be in 1..%d", n_comm, kAgMaxComm);
+  if (!comm_streams) return fail(PB_ERR_INVALID_ARG, "comm_streams is NULL");
+  for (int i = 0; i < n_comm; ++i) {
+    if (comm_streams[i] == stream)
+      return fail(PB_ERR_INVALID_ARG, "comm_streams[%d] equals stream", i);
+    for (int k = 0; k < i; ++k)
+      if (comm_streams[k] == comm_streams[i])
+        return fail(PB_ERR_INVALID_ARG, "comm_streams[%d] repeats comm_streams[%d]", i, k);
+  }
+  if (!shards) return fail(PB_ERR_INVALID_ARG, "shards is NULL");
+  for (int j = 0; j < tp; ++j) {
+    if (!shards[j] || (uintptr_t)shards[j] % 16)
+      return fail(PB_ERR_INVALID_ARG, "shards[%d] is NULL or not 16-byte aligned", j);
+  }
+  PB_CHECK(check_ptr(h, "h"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(b_in, "b_in"));
+  PB_CHECK(check_ptr(z, "z"));
+  PB_CHECK(check_ptr(c, "c"));
+  if (ws_bytes && (!ws || (uintptr_t)ws % 256))
+    return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kAgMaxDevices)
+    return fail(PB_ERR_HIP, "hipGetDevice failed");
+  AgEvents& ev = g_ag[dev];
+  if (!ev.ready) {
+    if (hipEventCreateWithFlags(&ev.start, hipEventDisableTiming) != hipSuccess)
+      return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
+    for (int i = 0; i < kAgMaxTp; ++i)
+      if (hipEventCreateWithFlags(&ev.landed[i], hipEventDisableTiming) != hipSuccess)
+        return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
+    ev.ready = true;
+  }
+  auto ok = [](hipError_t e) { return e == hipSuccess; };
+
+  const pb::Dt dt = dt_of(cfg);
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  const int rows = T / tp;
+  const size_t e = d.esz;
+  const size_t shard_bytes = (size_t)rows * H * e;
+  // the copies start after the work already on `stream` (which may produce
+  // the local shard)
+  if (!ok(hipEventRecord(ev.start, stream))) return fail(PB_ERR_HIP, "hipEventRecord failed");
+  for (int i = 0; i < n_comm; ++i)
+    if (!ok(hipStreamWaitEvent(comm_streams[i], ev.start, 0)))
+      return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+  // shards in ring order from this rank, round-robin over the comm streams
+  for (int k = 0; k < tp; ++k) {
+    const int j = (rank + k) % tp;
+    hipStream_t cs = comm_streams[k % n_comm];
+    char* dst = (char*)h + (size_t)j * shard_bytes;
+    if (shards[j] != dst &&
+        !ok(hipMemcpyAsync(dst, shards[j], shard_bytes, hipMemcpyDeviceToDeviceNoCU, cs)))
+      return fail(PB_ERR_HIP, "hipMemcpyAsync of shard %d failed", j);
+    if (!ok(hipEventRecord(ev.landed[k], cs))) return fail(PB_ERR_HIP, "hipEventRecord failed");
+  }
+  // the in-projection over groups of shards_per_launch shards in arrival
+  // order, each launch on `stream` once its shards have landed (a group that
+  // wraps past the last rank is two row ranges)
+  float* split_ws = (float*)ws;
+  const size_t split_f = ws_bytes / 4;
+  auto gemm_rows = [&](int j0, int nsh) {
+    const int r0 = j0 * rows, m = nsh * rows;
+    pb::EpiArgs e1;
+    e1.out = at(z, (long long)r0 * N_in, e);
+    e1.ld_out = N_in;
+    e1.out2 = at(c, (long long)r0 * K_out, e);
+    e1.ld_out2 = K_out;
+    e1.bias = b_in;
+    e1.split = 3 * A;
+    e1.col2 = A;
+    e1.gelu_tanh = cfg->gelu_tanh;
+    pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, at(h, (long long)r0 * H, e), H, w_in, H,
+                    m, N_in, H, e1, split_ws, split_f, stream);
+  };
+  for (int k0 = 0; k0 < tp; k0 += shards_per_launch) {
+    const int k1 = std::min(tp, k0 + shards_per_launch);
+    for (int k = k0; k < k1; ++k)
+      if (!ok(hipStreamWaitEvent(stream, ev.landed[k], 0)))
+        return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+    const int j0 = (rank + k0) % tp, n = k1 - k0;
+    if (j0 + n <= tp) {
+      gemm_rows(j0, n);
+    } else {
+      gemm_rows(j0, tp - j0);
+      gemm_rows(0, j0 + n - tp);
+    }
+  }
+  return finish_launches();
+}
+
 // ---------------------------------------------------------------- LAMB step
 static_assert(PB_LAMB_MAX_TENSORS == pb::kLambMaxTensors, "tensor limit");
 

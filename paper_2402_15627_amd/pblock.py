@@ -34,6 +34,7 @@ EXPORTS = (
     "pblock_status_string", "pblock_last_error", "pblock_serial_saved_bytes",
     "pblock_serial_saved_offsets", "pblock_serial_workspace_bytes", "pblock_serial_forward",
     "pblock_serial_backward", "pblock_lamb_workspace_bytes", "pblock_lamb_step",
+    "pblock_ag_in_proj_workspace_bytes", "pblock_ag_in_proj",
 )
 LAMB_MAX_TENSORS = 16
 
@@ -102,6 +103,9 @@ def load_library(path: str = LIB_PATH):
         "pblock_serial_forward": (c_int, [cfgp] + [P] * 13 + [c_size_t, P]),
         "pblock_serial_backward": (c_int, [cfgp] + [P] * 23 + [c_size_t, P]),
         "pblock_lamb_workspace_bytes": (c_size_t, [c_int, POINTER(LambTensor)]),
+        "pblock_ag_in_proj_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
+        "pblock_ag_in_proj": (c_int, [cfgp, c_int, c_int, POINTER(c_void_p), P, P, P, P, P, c_int,
+                                      P, c_size_t, P, c_int, POINTER(c_void_p)]),
         "pblock_lamb_step": (c_int, [POINTER(LambConfig), c_int, POINTER(LambTensor), c_int, P, P,
                                      c_size_t, P]),
     }
@@ -283,6 +287,24 @@ def pblock_lamb_step(cfg: LambConfig, tensors, copy_dtype=PB_BF16, trust_ratio=N
     _check(load_library().pblock_lamb_step(
         ctypes.byref(cfg), len(tensors), _lamb_array(tensors), int(copy_dtype),
         _ptr(trust_ratio), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def pblock_ag_in_proj_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch: int) -> int:
+    return load_library().pblock_ag_in_proj_workspace_bytes(ctypes.byref(cfg), int(tp),
+                                                            int(shards_per_launch))
+
+
+def pblock_ag_in_proj(cfg, tp, rank, shards, h, w_in, b_in, z, c, shards_per_launch, ws, stream,
+                      comm_streams):
+    """shards: tp tensors (or addresses), rank j's rows of h; comm_streams: a
+    non-empty sequence of streams other than `stream` (torch streams or raw
+    handles)."""
+    arr = (c_void_p * len(shards))(*[_ptr(t) for t in shards])
+    cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
+    _check(load_library().pblock_ag_in_proj(
+        ctypes.byref(cfg), int(tp), int(rank), arr, _ptr(h), _ptr(w_in), _ptr(b_in), _ptr(z),
+        _ptr(c), int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream),
+        len(comm_streams), cs))
 
 
 def pblock_status_string(status: int) -> str:

@@ -311,3 +311,28 @@ def test_lamb_workspace_and_validation():
     # empty tensors need no pointers
     assert pb.pblock_lamb_workspace_bytes([T(None, None, None, None, None, 0, 0.0)]) == align(4)
     assert call(ws=FAKE + 16) == 1
+
+
+def test_ag_in_proj_rejects_bad_arguments_before_launching():
+    lib = pb.load_library()
+    c = good_cfg()  # 13B shape: T = 2048, H = 5120
+
+    def call(cfg=c, tp=8, rank=0, per=1, stream=FAKE, comm=(FAKE + 256,), ws=FAKE,
+             nbytes=1 << 20):
+        shards = (ctypes.c_void_p * tp)(*([FAKE] * tp)) if tp > 0 else None
+        cs = (ctypes.c_void_p * max(len(comm), 1))(*comm) if comm else None
+        return lib.pblock_ag_in_proj(ctypes.byref(cfg), tp, rank, shards, FAKE, FAKE, FAKE, FAKE,
+                                     FAKE, per, ws, nbytes, stream, len(comm), cs)
+
+    assert call(tp=3) == 1 and "divisible" in pb.pblock_last_error()
+    assert call(tp=65) == 1
+    assert call(rank=8) == 1 and call(rank=-1) == 1
+    assert call(per=0) == 1 and call(per=9) == 1
+    assert call(comm=(FAKE,)) == 1  # comm stream equal to the compute stream
+    assert call(comm=(FAKE + 256, FAKE + 256)) == 1  # repeated
+    assert call(comm=()) == 1
+    assert call(ws=FAKE + 16) == 1
+    assert call(cfg=good_cfg(head_dim=80)) == 2
+    assert pb.pblock_ag_in_proj_workspace_bytes(c, 8, 1) % 256 == 0
+    assert pb.pblock_ag_in_proj_workspace_bytes(c, 8, 9) == 0
+    assert pb.pblock_ag_in_proj_workspace_bytes(c, 3, 1) == 0
