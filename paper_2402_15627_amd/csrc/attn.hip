@@ -458,12 +458,12 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(const T* __restrict__ O
 // tiles: half the registers of one wave doing both, and no repeated work.
 // The transposed operands are read from the natural Q and dO tiles.
 template <int D>
-__global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
+PB_DEV void dkdv_body(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV, int ld_d,
     int S, int H, int W, float scale, int cs, int nc, float* __restrict__ pdk,
-    float* __restrict__ pdv) {
+    float* __restrict__ pdv, int bx) {
   constexpr int TL = kTLdkv;
   constexpr int NB = kBlockK;
   constexpr int TB = TL * 2 * D;
@@ -477,8 +477,8 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
   auto g_off = [&](int s) { return s * STAGE + TB; };
   auto l_off = [&](int s) { return s * STAGE + 2 * TB; };
 
-  const int chunk = (int)blockIdx.x % nc;
-  const int k0 = ((int)blockIdx.x / nc) * NB;
+  const int chunk = bx % nc;
+  const int k0 = (bx / nc) * NB;
   const int ntot = kblock_tiles(k0, S, W);
   const int t_begin = chunk * cs;
   if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
@@ -625,11 +625,11 @@ __global__ __launch_bounds__(64 * kWavesK) void attn_dkdv_bf16(
 // dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T (K^T read from the natural K
 // tile).
 template <int D>
-__global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2))) void attn_dq_bf16(
+PB_DEV void dq_body(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dQ, int ld_d, int S, int H, int W,
-    float scale, int cs, int nc, float* __restrict__ pdq) {
+    float scale, int cs, int nc, float* __restrict__ pdq, int bx) {
   constexpr int TL = kTL;
   constexpr int NB = kBlockQ;
   constexpr int TB = TL * 2 * D;
@@ -639,8 +639,8 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
   auto v_off = [&](int s) { return (2 * s + 1) * TB; };
 
   const int nqb = (S + NB - 1) / NB;
-  const int chunk = (int)blockIdx.x % nc;
-  const int q0 = (nqb - 1 - (int)blockIdx.x / nc) * NB;
+  const int chunk = bx % nc;
+  const int q0 = (nqb - 1 - bx / nc) * NB;
   const int ntot = qblock_tiles(q0, S, W);
   const int t_begin = chunk * cs;
   if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
@@ -754,6 +754,29 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
         store4(dqr + 32 * db + 8 * j + 4 * fh, a);
       }
   }
+}
+
+// Both backward kernels in one launch: workgroups 0 .. nxk - 1 of the x grid
+// are dK/dV blocks, the rest dQ blocks.  They are independent given delta;
+// sharing a launch lets the short dQ blocks fill the CUs that the dK/dV
+// blocks leave idle (both grids alone are too small for the chip at few
+// heads), instead of running one after the other.
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_bwd_bf16(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
+    const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
+    const float* __restrict__ delta, bf16* __restrict__ dQ, bf16* __restrict__ dK,
+    bf16* __restrict__ dV, int ld_d, int S, int H, int W, float scale, int kv_cs, int kv_nc,
+    int nxk, int q_cs, int q_nc, float* __restrict__ pdk, float* __restrict__ pdv,
+    float* __restrict__ pdq) {
+  static_assert(64 * kWavesK == 256 && 64 * kWavesQ == 256, "one block size for both roles");
+  const int bx = (int)blockIdx.x;
+  if (bx < nxk)
+    dkdv_body<D>(Q, K, V, ld, dO, ld_o, lse, delta, dK, dV, ld_d, S, H, W, scale, kv_cs, kv_nc,
+                 pdk, pdv, bx);
+  else
+    dq_body<D>(Q, K, V, ld, dO, ld_o, lse, delta, dQ, ld_d, S, H, W, scale, q_cs, q_nc, pdq,
+               bx - nxk);
 }
 
 // ============================================================ fp32 path
@@ -919,25 +942,24 @@ void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
       p.fwd_chunk = p.kv_chunk = kUnsplit;
       p.fwd_n = p.kv_n = 1;
     }
-    // dK/dV partials, then (after their merge) dQ partials, in the same space
+    // dK, dV and dQ partials side by side (the two roles run concurrently)
     float* pdk = (float*)part;
     float* pdv = pdk ? pdk + part_floats(a, p.kv_n) : nullptr;
-    dim3 gk((a.seq + kBlockK - 1) / kBlockK * p.kv_n, a.heads, a.batch);
-    attn_dkdv_bf16<D><<<gk, 64 * kWavesK, dkdv_lds<D>(), s>>>(
+    float* pdq = pdk ? pdv + part_floats(a, p.kv_n) : nullptr;
+    const int nxk = (a.seq + kBlockK - 1) / kBlockK * p.kv_n;
+    const int nxq = (a.seq + kBlockQ - 1) / kBlockQ * p.fwd_n;
+    dim3 g(nxk + nxq, a.heads, a.batch);
+    attn_bwd_bf16<D><<<g, 256, std::max(dkdv_lds<D>(), dq_lds<D>()), s>>>(
         (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (const bf16*)d_o, ld_do, lse, delta,
-        (bf16*)dk, (bf16*)dv, ld_d, a.seq, a.heads, a.window, scale, p.kv_chunk, p.kv_n, pdk,
-        pdv);
+        (bf16*)dq, (bf16*)dk, (bf16*)dv, ld_d, a.seq, a.heads, a.window, scale, p.kv_chunk,
+        p.kv_n, nxk, p.fwd_chunk, p.fwd_n, pdk, pdv, pdq);
     if (p.kv_n > 1)
       attn_sum_combine<D, true><<<combine_grid(a), 256, 0, s>>>(
           pdk, pdv, p.kv_chunk, (bf16*)dk, (bf16*)dv, ld_d, a.batch, a.seq, a.heads, a.window);
-    dim3 gq((a.seq + kBlockQ - 1) / kBlockQ * p.fwd_n, a.heads, a.batch);
-    attn_dq_bf16<D><<<gq, 64 * kWavesQ, dq_lds<D>(), s>>>(
-        (const bf16*)q, (const bf16*)k, (const bf16*)v, ld, (const bf16*)d_o, ld_do, lse, delta,
-        (bf16*)dq, ld_d, a.seq, a.heads, a.window, scale, p.fwd_chunk, p.fwd_n, (float*)part);
     if (p.fwd_n > 1)
       attn_sum_combine<D, false><<<combine_grid(a), 256, 0, s>>>(
-          (const float*)part, nullptr, p.fwd_chunk, (bf16*)dq, nullptr, ld_d, a.batch, a.seq,
-          a.heads, a.window);
+          pdq, nullptr, p.fwd_chunk, (bf16*)dq, nullptr, ld_d, a.batch, a.seq, a.heads,
+          a.window);
   } else {
     attn_delta_kernel<float><<<(nrows + 255) / 256, 256, 0, s>>>(
         (const float*)o, ld_o, (const float*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
@@ -987,7 +1009,7 @@ size_t attn_fwd_partial_bytes(const AttnShape& a, const AttnSplit& p) {
 }
 
 size_t attn_bwd_partial_bytes(const AttnShape& a, const AttnSplit& p) {
-  return std::max(2 * part_floats(a, p.kv_n) * 4, part_floats(a, p.fwd_n) * 4);
+  return (2 * part_floats(a, p.kv_n) + part_floats(a, p.fwd_n)) * 4;
 }
 
 void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
