@@ -630,9 +630,11 @@ def main():
     steps_out = {}
     for n in names:
         k, a = work[n]
-        rate = a / (step_ms[n] * 1e-3) / (1e12 if k == "mfma" else 1e9)
+        # a step whose work is done inside another one (db_out: summed with
+        # the LN backward's column sums) records ~0 ms and reports no rate
+        rate = a / (step_ms[n] * 1e-3) / (1e12 if k == "mfma" else 1e9) if step_ms[n] > 2e-3 else None
         steps_out[n] = {"ms": round(step_ms[n], 4),
-                        ("tflops" if k == "mfma" else "gbs"): round(rate, 1)}
+                        ("tflops" if k == "mfma" else "gbs"): None if rate is None else round(rate, 1)}
 
     out = {
         "metric": METRIC,

@@ -334,12 +334,13 @@ typedef enum {
   PB_STEP_OUT_PROJ,   /* y = x + C W_out^T + b_out                          */
   PB_STEP_DC,         /* dC = dy W_out; dU = dC_mlp * gelu'(U)              */
   PB_STEP_DW_OUT,     /* dW_out = dy^T C                                    */
-  PB_STEP_DB_OUT,     /* db_out = sum over tokens of dy                     */
+  PB_STEP_DB_OUT,     /* empty: db_out is summed with dgamma and dbeta in
+                         the LN backward step's column sums              */
   PB_STEP_ATTN_BWD,   /* dQ, dK, dV                                         */
   PB_STEP_DH,         /* dh = dZ W_in                                       */
   PB_STEP_DW_IN,      /* dW_in = dZ^T h                                     */
   PB_STEP_DB_IN,      /* db_in = sum over tokens of dZ                      */
-  PB_STEP_LN_BWD,     /* dx = dy + LN backward; dgamma, dbeta               */
+  PB_STEP_LN_BWD,     /* dx = dy + LN backward; dgamma, dbeta, db_out       */
   PB_STEP_COUNT
 } pb_step;
 

@@ -35,6 +35,11 @@ void launch_colsum(Dt dt, const void* src, int ld, int rows, int cols, float* pa
                    hipStream_t s);
 void launch_colsum_f32(const float* src, int ld, int rows, int cols, float* part, float* out,
                        hipStream_t s);
+// Three fp32 [rows, cols] arrays at once (same ld; cols a multiple of 4), in
+// one launch and without a partial buffer: for the few hundred rows of the
+// LayerNorm backward's per-chunk partial sums.
+void launch_colsum3_f32(const float* a, const float* b, const float* c, int ld, int rows,
+                        int cols, float* out_a, float* out_b, float* out_c, hipStream_t s);
 
 // -------------------------------------------------------------- LAMB step
 // One LAMB step over up to kLambMaxTensors fp32 tensors, each with its own

@@ -203,13 +203,35 @@ __global__ __launch_bounds__(kColThreads) void colsum_stage1(const T* __restrict
   }
 }
 
-__global__ __launch_bounds__(256) void colsum_stage2(const float* __restrict__ part, int chunks,
-                                                     int cols, float* __restrict__ out) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= cols) return;
-  float t = 0.f;
-  for (int i = 0; i < chunks; ++i) t += part[(size_t)i * cols + c];
-  out[c] = t;
+// Column sums of up to three fp32 [rows, cols] arrays (cols a multiple of
+// 4), blockIdx.y picking the array: a workgroup covers 64 columns as 16
+// column quads x 16 row groups; each thread adds rows g, g + 16, ... of its
+// four columns, and the 16 group sums are added in a fixed order.  Many
+// short, independent row walks keep enough loads in flight for the few
+// hundred rows these arrays have.
+struct Colsum3 {
+  const float* src[3];
+  float* out[3];
+};
+__global__ __launch_bounds__(256) void colsum_rows_f32(Colsum3 a, int ld, int rows, int cols) {
+  __shared__ f32x4 red[16][16];
+  const float* __restrict__ src = a.src[blockIdx.y];
+  const int q = threadIdx.x & 15, g = threadIdx.x >> 4;
+  const int c = (blockIdx.x * 16 + q) * 4;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (c < cols) {
+#pragma unroll 8
+    for (int r = g; r < rows; r += 16)
+      acc += *reinterpret_cast<const f32x4*>(src + (size_t)r * ld + c);
+  }
+  red[g][q] = acc;
+  __syncthreads();
+  if (g == 0 && c < cols) {
+    f32x4 t = red[0][q];
+#pragma unroll
+    for (int i = 1; i < 16; ++i) t += red[i][q];
+    *reinterpret_cast<f32x4*>(a.out[blockIdx.y] + c) = t;
+  }
 }
 
 template <typename T>
@@ -219,7 +241,8 @@ void colsum_impl(const T* src, int ld, int rows, int cols, float* part, float* o
   const int rpc = (rows + chunks - 1) / chunks;
   dim3 g1((cols + kColWidth - 1) / kColWidth, chunks);
   colsum_stage1<T><<<g1, kColThreads, 0, s>>>(src, ld, rows, cols, rpc, part);
-  colsum_stage2<<<(cols + 255) / 256, 256, 0, s>>>(part, chunks, cols, out);
+  Colsum3 a{{part, nullptr, nullptr}, {out, nullptr, nullptr}};
+  colsum_rows_f32<<<dim3((cols + 63) / 64, 1), 256, 0, s>>>(a, cols, chunks, cols);
 }
 
 template <typename T, int NV>
@@ -288,6 +311,12 @@ void launch_colsum(Dt dt, const void* src, int ld, int rows, int cols, float* pa
 void launch_colsum_f32(const float* src, int ld, int rows, int cols, float* part, float* out,
                        hipStream_t s) {
   colsum_impl<float>(src, ld, rows, cols, part, out, s);
+}
+
+void launch_colsum3_f32(const float* a, const float* b, const float* c, int ld, int rows,
+                        int cols, float* out_a, float* out_b, float* out_c, hipStream_t s) {
+  Colsum3 args{{a, b, c}, {out_a, out_b, out_c}};
+  colsum_rows_f32<<<dim3((cols + 63) / 64, 3), 256, 0, s>>>(args, ld, rows, cols);
 }
 
 }  // namespace pb

@@ -529,14 +529,13 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     StepScope sc(PB_STEP_LN_BWD, stream);
     pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, rowpart, dy, dx, pdg, pdb, pdy, T, H,
                            stream);
-    const int nblk = pb::ln_backward_chunks(T);
-    pb::launch_colsum_f32(pdg, H, nblk, H, part, dgamma, stream);
-    pb::launch_colsum_f32(pdb, H, nblk, H, part, dbeta, stream);
+    // dgamma, dbeta and db_out (= sum over tokens of dy) from the LN
+    // backward's per-chunk partial sums, in one launch
+    pb::launch_colsum3_f32(pdg, pdb, pdy, H, pb::ln_backward_chunks(T), H, dgamma, dbeta, db_out,
+                           stream);
   }
   {
-    // db_out = sum over tokens of dy, from the LN backward's partial sums
-    StepScope sc(PB_STEP_DB_OUT, stream);
-    pb::launch_colsum_f32(pdy, H, pb::ln_backward_chunks(T), H, part, db_out, stream);
+    StepScope sc(PB_STEP_DB_OUT, stream);  // now inside the LN backward's column sums
   }
   // db_in = sum over tokens of dZ
   {
@@ -860,9 +859,7 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   // dx1 = dy + LN2'(dh2); dgamma2, dbeta2, and db_down = sum dy
   pb::launch_ln_backward(dt, x1, mean2, rstd2, ln2_gamma, dh, rowpart, dy, dx1, pdg, pdb, pdy, T,
                          H, stream);
-  pb::launch_colsum_f32(pdg, H, nblk, H, part, dln2_gamma, stream);
-  pb::launch_colsum_f32(pdb, H, nblk, H, part, dln2_beta, stream);
-  pb::launch_colsum_f32(pdy, H, nblk, H, part, db_down, stream);
+  pb::launch_colsum3_f32(pdg, pdb, pdy, H, nblk, H, dln2_gamma, dln2_beta, db_down, stream);
   // attention: dO = dx1 W_o, then dQ, dK, dV -> dZ[:, :3A]
   pb::EpiArgs e3;
   e3.out = d_o;
@@ -889,9 +886,7 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   // dx = dx1 + LN1'(dh1); dgamma1, dbeta1, and db_o = sum dx1
   pb::launch_ln_backward(dt, x, mean1, rstd1, ln1_gamma, dh, rowpart, dx1, dx, pdg, pdb, pdy, T,
                          H, stream);
-  pb::launch_colsum_f32(pdg, H, nblk, H, part, dln1_gamma, stream);
-  pb::launch_colsum_f32(pdb, H, nblk, H, part, dln1_beta, stream);
-  pb::launch_colsum_f32(pdy, H, nblk, H, part, db_o, stream);
+  pb::launch_colsum3_f32(pdg, pdb, pdy, H, nblk, H, dln1_gamma, dln1_beta, db_o, stream);
   // bias gradients of the input projections: db_in = sum over tokens of dZ
   pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
   // weight gradients (token contractions), last
