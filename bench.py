@@ -73,12 +73,14 @@ def step_work(s):
         "out_proj": ("mfma", 2 * T * k_out * H),
         "dc": ("mfma", 2 * T * H * k_out),
         "dw_out": ("mfma", 2 * H * k_out * T),
-        "db_out": ("hbm", T * H * e + 4 * H),
+        # db_out is summed with dgamma and dbeta in the LN backward's column
+        # sums; its step is empty
+        "db_out": ("hbm", 0),
         "attn_bwd": ("mfma", 8 * s.batch * A * P),
         "dh": ("mfma", 2 * T * n_in * H),
         "dw_in": ("mfma", 2 * n_in * H * T),
         "db_in": ("hbm", T * n_in * e + 4 * n_in),
-        "ln_bwd": ("hbm", 3 * T * H * e + 4 * T * H + 8 * T + 8 * H),
+        "ln_bwd": ("hbm", 3 * T * H * e + 4 * T * H + 8 * T + 12 * H),
     }
 
 
@@ -631,8 +633,8 @@ def main():
     for n in names:
         k, a = work[n]
         # a step whose work is done inside another one (db_out: summed with
-        # the LN backward's column sums) records ~0 ms and reports no rate
-        rate = a / (step_ms[n] * 1e-3) / (1e12 if k == "mfma" else 1e9) if step_ms[n] > 2e-3 else None
+        # the LN backward's column sums) reports no rate
+        rate = a / (step_ms[n] * 1e-3) / (1e12 if k == "mfma" else 1e9) if a else None
         steps_out[n] = {"ms": round(step_ms[n], 4),
                         ("tflops" if k == "mfma" else "gbs"): None if rate is None else round(rate, 1)}
 
