@@ -284,6 +284,18 @@ def read_traffic(step, workload):
     return rec["traffic_bytes"]
 
 
+def short_kernel_name(name):
+    """Readable kernel name: template arguments spelled out, epilogues named."""
+    short = re.sub(r"^void ", "", name).replace("pb::(anonymous namespace)::", "")
+    for i, e in enumerate(("StoreF32", "BiasGelu", "BiasResid", "DgeluSplit", "LnGrad")):
+        short = short.replace(f"(pb::Epi){i}", e)
+    m = re.match(r"_ZN2pb12_GLOBAL__N_1\d+(\w+?)I", short)  # names c++filt leaves
+    if m:
+        d = re.search(r"Li(\d+)E", short)
+        short = m.group(1) + (f"<{d.group(1)}>" if d else "")
+    return re.sub(r"\(.*", "", short)[:70]
+
+
 def trace_summary(d, workload, block="parallel"):
     """Markdown table of a kernel-trace run: one row per (kernel, grid)."""
     from paper_2402_15627_amd.inputs import WORKLOADS
@@ -301,16 +313,9 @@ def trace_summary(d, workload, block="parallel"):
     total = sum(sum(v) for v in groups.values())
     rows = []
     for (name, grid), v in groups.items():
-        short = re.sub(r"^void ", "", name).replace("pb::(anonymous namespace)::", "")
-        for i, e in enumerate(("StoreF32", "BiasGelu", "BiasResid", "DgeluSplit", "LnGrad")):
-            short = short.replace(f"(pb::Epi){i}", e)
-        m = re.match(r"_ZN2pb12_GLOBAL__N_1\d+(\w+?)I", short)  # names c++filt leaves
-        if m:
-            d = re.search(r"Li(\d+)E", short)
-            short = m.group(1) + (f"<{d.group(1)}>" if d else "")
-        short = re.sub(r"\(.*", "", short)
         step = gemm_step_of(name, grid, s, block)
-        rows.append((sum(v), short[:70], grid, step, len(v), sum(v) / len(v), min(v), max(v)))
+        rows.append((sum(v), short_kernel_name(name), grid, step, len(v), sum(v) / len(v), min(v),
+                     max(v)))
     rows.sort(reverse=True)
     out = ["| kernel | grid (work-items) | block step | calls | avg us | min us | max us | "
            "% of GPU time |", "|---|---:|---|---:|---:|---:|---:|---:|"]
@@ -346,6 +351,83 @@ def cpu_baseline(shape, inputs, min_seconds=10.0, max_steps=6):
 
 
 LAMB_BYTES_PER_ELEMENT = 42  # moments pass 16 read + 8 written; update pass 12 read + 4 + 2 written
+
+
+def device_info():
+    """Name, compute units and the driver's maximum shader clock of device 0."""
+    import torch
+    p = torch.cuda.get_device_properties(0)
+    rec = {"name": p.name, "compute_units": p.multi_processor_count,
+           "arch": getattr(p, "gcnArchName", None)}
+    try:
+        import ctypes
+        hip = ctypes.CDLL("libamdhip64.so")
+        v = ctypes.c_int()
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), 5, 0) == 0:  # hipDeviceAttributeClockRate (kHz)
+            rec["max_clock_mhz"] = v.value // 1000
+    except OSError:
+        pass
+    return rec
+
+
+def measured_sclk_mhz(step, seconds=2.0):
+    """Median shader clock (MHz) that rocm-smi reports while steps run back to
+    back for a few seconds (the chip lowers its clock under sustained matrix
+    load); None when rocm-smi is not available."""
+    import shutil
+    import subprocess
+    import threading
+    import torch
+    exe = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
+    if not os.path.exists(exe):
+        return None
+    samples = []
+    stop = threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            try:
+                out = subprocess.run([exe, "--showclocks", "--json"], capture_output=True,
+                                     text=True, timeout=20).stdout
+                for card in json.loads(out).values():
+                    for k, v in card.items():
+                        if k.lower().startswith("sclk"):
+                            m = re.search(r"(\d+)\s*mhz", str(v), re.I)
+                            if m:
+                                samples.append(int(m.group(1)))
+            except (OSError, ValueError, subprocess.SubprocessError, AttributeError):
+                pass
+
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    t0 = time.time()
+    while time.time() - t0 < seconds:
+        for _ in range(20):
+            step()
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=30)
+    return sorted(samples)[len(samples) // 2] if samples else None
+
+
+def mfma_summary(d, workload):
+    """Markdown table of a rocprofv3 --pmc MfmaUtil run: per kernel and grid."""
+    from paper_2402_15627_amd.inputs import WORKLOADS
+    s = WORKLOADS[workload]
+    rows = _counter_rows(d)
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != "MfmaUtil":
+            continue
+        key = (demangle(r["Kernel_Name"]), int(r["Grid_Size"]))
+        per.setdefault(key, {})[r["Dispatch_Id"]] = float(r["Counter_Value"])
+    out = ["| kernel | grid (work-items) | block step | dispatches | MFMA busy % |",
+           "|---|---:|---|---:|---:|"]
+    for (name, grid), v in sorted(per.items(), key=lambda kv: -sum(kv[1].values()) / len(kv[1])):
+        vals = list(v.values())
+        out.append(f"| `{short_kernel_name(name)}` | {grid} | {gemm_step_of(name, grid, s)} | {len(vals)} | "
+                   f"{sum(vals) / len(vals):.1f} |")
+    return "\n".join(out)
 
 
 def time_lamb(pb, shape, warmup, steps, grads=None):
@@ -502,10 +584,15 @@ def main():
                     help="a GEMM step, or lamb (the LAMB step's two streaming kernels)")
     ap.add_argument("--trace-summary", metavar="DIR",
                     help="print a markdown table of a rocprofv3 --kernel-trace output dir")
+    ap.add_argument("--mfma-summary", metavar="DIR",
+                    help="print a markdown table of a rocprofv3 --pmc MfmaUtil output dir")
     ap.add_argument("--command", default="", help="command line recorded with a summary")
     args = ap.parse_args()
     if args.trace_summary:
         print(trace_summary(args.trace_summary, args.workload, args.block))
+        return
+    if args.mfma_summary:
+        print(mfma_summary(args.mfma_summary, args.workload))
         return
     if args.traffic_summary:
         if args.traffic_step == "lamb":
@@ -614,6 +701,18 @@ def main():
     ms = t_start.elapsed_time(t_end) / K
     dom_ms = sum(db[i].elapsed_time(de[i]) for i in range(K)) / K
 
+    # Per-step spread: a separate pass with events around every whole step.
+    sb = [new_event() for _ in range(K)]
+    se = [new_event() for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        sb[i].record()
+        step()
+        se[i].record()
+    torch.cuda.synchronize()
+    per_step = sorted(sb[i].elapsed_time(se[i]) for i in range(K))
+    sclk = measured_sclk_mhz(step)
+
     value = flops / (ms * 1e-3) / 1e12
     kind, amount = work[dominant]
     if kind == "mfma":
@@ -657,6 +756,12 @@ def main():
                    "ffn": shape.ffn, "window": shape.window, "flops_per_step": flops,
                    "parallelism": "none: one GPU holding one tensor-parallel rank's share"},
         "roofline": roof,
+        "step_ms": {"min": round(per_step[0], 4), "median": round(per_step[K // 2], 4),
+                    "max": round(per_step[-1], 4)},
+        "device": device_info(),
+        "clock": {"sclk_mhz_median": sclk,
+                  "pct_of_peak_at_measured_clock":
+                      round(100 * value / (PEAK_BF16_TFLOPS * sclk / 2400.0), 2) if sclk else None},
         "steps_breakdown": steps_out,
     }
     if not args.no_serial:
