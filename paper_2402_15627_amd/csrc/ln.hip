@@ -13,6 +13,24 @@
 namespace pb {
 namespace {
 
+// Eight elements of data read once and not again soon (x in the forward;
+// x, dh and dy in the backward): non-temporal loads keep them from pushing
+// out of the caches what the next kernels reuse (h for the in-projection,
+// dZ for the column sums and dW_in).  Measured: LN forward 34 -> 27 us,
+// db_in 20 -> 15 us at the 175B share.
+template <typename T> PB_DEV void load8_stream(const T* p, float* v);
+template <> PB_DEV void load8_stream<bf16>(const bf16* p, float* v) {
+  const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { v[2 * i] = lo_bf(w[i]); v[2 * i + 1] = hi_bf(w[i]); }
+}
+template <> PB_DEV void load8_stream<float>(const float* p, float* v) {
+  const f32x4 a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  const f32x4 b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { v[i] = a[i]; v[4 + i] = b[i]; }
+}
+
 constexpr int kLnThreads = 512;
 constexpr int kLnWaves = kLnThreads / 64;
 
@@ -47,7 +65,7 @@ __global__ __launch_bounds__(kLnThreads) void ln_fwd_kernel(const T* __restrict_
   for (int j = 0; j < NV; ++j) {
     const int c = (threadIdx.x + j * kLnThreads) * 8;
     if (c < H) {
-      load8(xr + c, v[j]);
+      load8_stream(xr + c, v[j]);
 #pragma unroll
       for (int e = 0; e < 8; ++e) s += v[j][e];
     }
@@ -139,9 +157,9 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
   for (int rr = 0; rr < nr; ++rr) {
     const size_t off = (size_t)(r0 + rr) * H + c;
     float xv[8], d[8], yv[8], o[8];
-    load8(x + off, xv);
-    load8(dh + off, d);
-    load8(dy + off, yv);
+    load8_stream(x + off, xv);
+    load8_stream(dh + off, d);
+    load8_stream(dy + off, yv);
     const float mu = mean[r0 + rr], rs = rstd[r0 + rr];
     const float m1 = stat[rr][0], m2 = stat[rr][1];
 #pragma unroll
