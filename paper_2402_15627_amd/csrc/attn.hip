@@ -937,7 +937,7 @@ void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
   if (dt == Dt::BF16) {
     attn_delta_kernel<bf16><<<(nrows + 255) / 256, 256, 0, s>>>(
         (const bf16*)o, ld_o, (const bf16*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
-    AttnSplit p = attn_split_plan(dt, a);
+    AttnSplit p = attn_bwd_split_plan(dt, a);
     if (!part || part_bytes < attn_bwd_partial_bytes(a, p)) {
       p.fwd_chunk = p.kv_chunk = kUnsplit;
       p.fwd_n = p.kv_n = 1;
@@ -1000,6 +1000,15 @@ AttnSplit attn_split_plan(Dt dt, const AttnShape& a) {
   };
   choose(kBlockQ, kWavesQ, false, p.fwd_chunk, p.fwd_n);
   choose(kBlockK, kWavesK, true, p.kv_chunk, p.kv_n);
+  return p;
+}
+
+AttnSplit attn_bwd_split_plan(Dt dt, const AttnShape& a) {
+  AttnSplit p = attn_split_plan(dt, a);
+  // both roles share one launch: split only when together they are too few
+  const long long blocks = (long long)((a.seq + kBlockK - 1) / kBlockK +
+                                       (a.seq + kBlockQ - 1) / kBlockQ) * a.heads * a.batch;
+  if (blocks * kWavesK >= kSplitBelow) p = AttnSplit{kUnsplit, 1, kUnsplit, 1};
   return p;
 }
 

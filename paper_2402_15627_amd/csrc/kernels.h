@@ -142,6 +142,9 @@ struct AttnSplit {
   int kv_chunk, kv_n;    // dK/dV: query tiles of 32
 };
 AttnSplit attn_split_plan(Dt dt, const AttnShape& a);
+// The backward's plan: both backward roles run in one launch, so it splits
+// only when their blocks together are too few for the chip.
+AttnSplit attn_bwd_split_plan(Dt dt, const AttnShape& a);
 // Bytes of partial results the split forward / backward needs (0: unsplit).
 size_t attn_fwd_partial_bytes(const AttnShape& a, const AttnSplit& p);
 size_t attn_bwd_partial_bytes(const AttnShape& a, const AttnSplit& p);

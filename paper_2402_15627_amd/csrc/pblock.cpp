@@ -144,7 +144,7 @@ size_t split_bytes_bwd(const Dims& d, pb::Dt dt) {
   m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, T, H, N_in)));
   m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, N_in, H, T)));
   const pb::AttnShape a = attn_shape(d);
-  return std::max(m * 4, pb::attn_bwd_partial_bytes(a, pb::attn_split_plan(dt, a)));
+  return std::max(m * 4, pb::attn_bwd_partial_bytes(a, pb::attn_bwd_split_plan(dt, a)));
 }
 
 struct BwdLayout {
@@ -219,7 +219,7 @@ size_t serial_split_bwd(const Dims& d, pb::Dt dt) {
   size_t m = max_split_bytes(dt, {{T, F, H}, {H, F, T}, {T, H, F}, {F, H, T}, {T, A, H},
                                   {H, A, T}, {T, H, 3 * A}, {3 * A, H, T}});
   const pb::AttnShape a = attn_shape(d);
-  return std::max(m, pb::attn_bwd_partial_bytes(a, pb::attn_split_plan(dt, a)));
+  return std::max(m, pb::attn_bwd_partial_bytes(a, pb::attn_bwd_split_plan(dt, a)));
 }
 
 // Backward workspace of the serial block: dO, dZ, dh (fp32, shared by both
@@ -599,7 +599,8 @@ size_t pblock_swattn_workspace_bytes(const pb_config* cfg, int mode) {
     case PB_ATTN_WS_FORWARD: return pb::attn_fwd_partial_bytes(a, p);
     case PB_ATTN_WS_BACKWARD_MIN: return swattn_delta_bytes(cfg);
     case PB_ATTN_WS_BACKWARD:
-      return swattn_delta_bytes(cfg) + align256(pb::attn_bwd_partial_bytes(a, p));
+      return swattn_delta_bytes(cfg) +
+             align256(pb::attn_bwd_partial_bytes(a, pb::attn_bwd_split_plan(dt_of(cfg), a)));
     default: return 0;
   }
 }

@@ -196,22 +196,25 @@ def test_status_strings():
 
 
 def test_swattn_workspace_modes():
-    """The split workspace is planned only when batch * heads * (seq / 64)
-    blocks are too few to fill the GPU; the backward's minimum is one fp32
-    row term per query."""
+    """The split workspace is planned only when the blocks are too few to fill
+    the GPU: the forward's batch * heads * (seq / 128) blocks, the backward's
+    dK/dV and dQ blocks together (they share one launch).  The backward's
+    minimum is one fp32 row term per query."""
     lib_ws = pb.pblock_swattn_workspace_bytes
-    small = pb.make_config(1, 2048, 1536, 12, 128, 64, 2048, "bf16")
+    share = pb.make_config(1, 2048, 1536, 12, 128, 64, 2048, "bf16")  # 576 bwd blocks
+    tiny = pb.make_config(1, 2048, 512, 4, 128, 64, 2048, "bf16")     # 192 bwd blocks
     big = pb.make_config(1, 8192, 5120, 40, 128, 64, 1024, "bf16")
     f32 = pb.make_config(1, 2048, 1536, 12, 128, 64, 2048, "f32")
-    for c in (small, big, f32):
+    for c in (share, tiny, big, f32):
         assert lib_ws(c, pb.ATTN_WS_BACKWARD_MIN) == -(-c.batch * c.heads * c.seq * 4 // 256) * 256
         assert lib_ws(c, pb.ATTN_WS_BACKWARD) >= lib_ws(c, pb.ATTN_WS_BACKWARD_MIN)
-    assert lib_ws(small, pb.ATTN_WS_FORWARD) > 0
-    assert lib_ws(small, pb.ATTN_WS_BACKWARD) > lib_ws(small, pb.ATTN_WS_BACKWARD_MIN)
+    assert lib_ws(share, pb.ATTN_WS_FORWARD) > 0  # 192 forward blocks
+    assert lib_ws(share, pb.ATTN_WS_BACKWARD) == lib_ws(share, pb.ATTN_WS_BACKWARD_MIN)
+    assert lib_ws(tiny, pb.ATTN_WS_BACKWARD) > lib_ws(tiny, pb.ATTN_WS_BACKWARD_MIN)
     for c in (big, f32):
         assert lib_ws(c, pb.ATTN_WS_FORWARD) == 0
         assert lib_ws(c, pb.ATTN_WS_BACKWARD) == lib_ws(c, pb.ATTN_WS_BACKWARD_MIN)
-    assert lib_ws(small, 7) == 0
+    assert lib_ws(share, 7) == 0
 
 
 def declared_arities():
