@@ -349,7 +349,7 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kDK = 64;                     // K-tile of the DMA path
 constexpr int kStages = 2;
-constexpr int kDTile = kBM * kDK * 2;       // one operand tile: 16 KB
+constexpr int kDTile = kBM * kDK * 2;       // one operand tile: 32 KB
 constexpr int kPieces = kDTile / kThreads / 16;  // 1 KB DMA pieces per operand per wave: 4
 constexpr int kDmaPerStage = 2 * kPieces;   // DMA instructions per wave per stage
 static_assert(kBM == kBN && kPieces * 1024 * (kThreads / 64) == kDTile, "tile split over waves");
@@ -538,14 +538,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     // this wave, and after the barrier for all.
     wait_dma<0>();
     block_barrier();
-    // the next tile's first fragments (past the last tile: a stale stage,
-    // unused), and the loads of tile t + 2 spread over k-steps 2 and 3
-    read_frags(t + 1, 0);
+    // the loads of tile t + 2 spread over k-steps 2 and 3, each half issued
+    // ahead of that k-step's fragment reads (about 0.5% faster than after
+    // them), and the next tile's first fragments (past the last tile: a
+    // stale stage, unused)
     if (t + 2 < nt) issue_half(t + 2, 0);
+    read_frags(t + 1, 0);
     mma(2);
     __builtin_amdgcn_sched_barrier(0);
-    read_frags(t + 1, 1);
     if (t + 2 < nt) issue_half(t + 2, 1);
+    read_frags(t + 1, 1);
     mma(3);
     __builtin_amdgcn_sched_barrier(0);
   }
