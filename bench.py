@@ -381,13 +381,22 @@ def measured_sclk_mhz(step, seconds=2.0):
     exe = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
     if not os.path.exists(exe):
         return None
+    # Under rocprofv3 every child process loads the profiler's library, which
+    # initialises the GPU, so a launcher that re-execs (rocm-smi's
+    # "#!/usr/bin/env python3" line) is a forbidden exec: take no samples
+    # there.  Elsewhere the script is started by this interpreter directly.
+    if any(k.startswith("ROCPROF_") for k in os.environ):
+        return None
+    with open(exe, "rb") as f:
+        head = f.readline()
+    cmd = [sys.executable, exe] if head.startswith(b"#!") and b"python" in head else [exe]
     samples = []
     stop = threading.Event()
 
     def sampler():
         while not stop.is_set():
             try:
-                out = subprocess.run([exe, "--showclocks", "--json"], capture_output=True,
+                out = subprocess.run(cmd + ["--showclocks", "--json"], capture_output=True,
                                      text=True, timeout=20).stdout
                 for card in json.loads(out).values():
                     for k, v in card.items():
