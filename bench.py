@@ -16,6 +16,10 @@ Prints one JSON line.  Besides the contract fields it carries:
   ag_in_proj    the in-projection pipelined with the all-gather of its input
                 over 8 ranks (one GPU: shards copied from local buffers),
                 against the GEMM alone and copies followed by one GEMM;
+  rs_out_proj   the out-projection's partial sums pipelined with their
+                reduce-scatter over 8 ranks (chunks copied into local
+                buffers), against the GEMM alone and one GEMM followed by the
+                copies, and the receiving side's sum;
   lamb_step     one fused LAMB optimizer step over the block's parameters
                 (fp32 master weights and moments, the step's own gradients,
                 bf16 copy), against the HBM peak;
@@ -539,6 +543,59 @@ def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     return {"tp": tp, "n_comm": n_comm, "shard_bytes": rows * H * src.element_size(), **out}
 
 
+def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
+    """The out-projection's partial sums pipelined with their reduce-scatter
+    over tp ranks (row chunks sent on comm streams as their GEMM launch
+    finishes), against the GEMM alone and one GEMM followed by the copies;
+    and the receiving side's sum of tp chunks.  Events on the compute
+    stream."""
+    import torch
+    T, H = shape.tokens, shape.hidden
+    cfg = pb.config_from_shape(shape)
+    act = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    c = torch.randn(T, shape.k_out, device="cuda").to(act)
+    partial = torch.empty(T, H, dtype=act, device="cuda")
+    rows = T // tp
+    recv = torch.empty(tp, rows, H, dtype=act, device="cuda")
+    stream = torch.cuda.Stream()
+    comm = [torch.cuda.Stream() for _ in range(n_comm)]
+    out = {}
+
+    def timed(call):
+        for _ in range(warmup):
+            call()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return round(e0.elapsed_time(e1) / steps, 4)
+
+    def send(per, in_place):
+        nws = pb.pblock_rs_out_proj_workspace_bytes(cfg, tp, per)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
+        dst = ([partial[j * rows:(j + 1) * rows] for j in range(tp)] if in_place
+               else [recv[j] for j in range(tp)])
+        return lambda: pb.pblock_rs_out_proj(cfg, tp, 0, c, dev["w_out"], partial, dst, per, ws,
+                                             stream, comm)
+
+    out["gemm_only_ms"] = timed(send(tp, True))
+    out["gemm_then_copies_ms"] = timed(send(tp, False))
+    for per in (1, 2, 4):
+        out[f"pipelined_{per}_shards_per_launch_ms"] = timed(send(per, False))
+    y = torch.empty(rows, H, dtype=act, device="cuda")
+    parts = [recv[q] for q in range(tp)]
+    ms = timed(lambda: pb.pblock_rs_reduce(cfg, tp, parts, dev["x"].reshape(T, H)[:rows], dev["b_out"], y,
+                                           stream))
+    nbytes = (tp + 2) * rows * H * partial.element_size()
+    out["reduce_ms"] = ms
+    out["reduce_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
+    return {"tp": tp, "n_comm": n_comm, "chunk_bytes": rows * H * partial.element_size(), **out}
+
+
 def time_serial(pb, shape, warmup, steps, parallel_ms, flops):
     """The standard block (two LayerNorms, four projections; the same model
     FLOPs) on the same workload and kernels, timed like the parallel block:
@@ -581,7 +638,7 @@ def main():
     ap.add_argument("--no-serial", action="store_true",
                     help="skip timing the serial (two-LayerNorm) block for comparison")
     ap.add_argument("--no-ag", action="store_true",
-                    help="skip timing the in-projection pipelined with the all-gather")
+                    help="skip timing the all-gather and reduce-scatter pipelines")
     ap.add_argument("--no-lamb", action="store_true",
                     help="skip timing the LAMB step over the block's parameters")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -777,6 +834,7 @@ def main():
         out["serial_block"] = time_serial(pb, shape, args.warmup, K, ms, flops)
     if not args.no_ag:
         out["ag_in_proj"] = time_ag(pb, shape, dev, 2, 5)
+        out["rs_out_proj"] = time_rs(pb, shape, dev, 2, 5)
     if not args.no_lamb:
         names = ("w_in", "b_in", "w_out", "b_out", "gamma", "beta")
         gmap = dict(zip(names, (blk.grads[k] for k in ("dw_in", "db_in", "dw_out", "db_out",

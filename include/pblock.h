@@ -273,6 +273,52 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
                             size_t ws_bytes, hipStream_t stream, int n_comm,
                             const hipStream_t* comm_streams);
 
+/* --------------------------------------- out-projection + reduce-scatter
+ * Section 3.2 ("Overlapping in tensor/sequence parallelism", Fig. 3), the
+ * other half of the pattern above: after the row-parallel out-projection
+ * every rank holds a partial sum P_r = C_r W_out,r^T of every token row
+ * (C_r, W_out,r: its own columns of the out-projection input and weight),
+ * and a reduce-scatter leaves rank j with the sum over ranks of its own
+ * rows.  The paper pipelines that GEMM in chunks with the communication.
+ *
+ * pblock_rs_out_proj (the sending side of rank `rank`) computes P_r on
+ * `stream` in row chunks of T / tp rows, in ring order from rank + 1 (this
+ * rank's own chunk last), shards_per_launch chunks per launch; each chunk
+ * j is copied to dst[j] on comm_streams[k % n_comm] (k its position in that
+ * order) as soon as its launch has finished.  shards_per_launch = tp is the
+ * unpipelined order: one GEMM, then all copies.
+ *   c [T, K_out], w_out [H, K_out]: as in pblock_forward, in the activation
+ *     dtype; cfg describes this rank's share (A, F its own widths).
+ *   partial [T, H]: P_r in the activation dtype (rounded from the fp32
+ *     accumulation).  dst[j]: [T / tp, H], where rank j receives this
+ *     rank's chunk (on one GPU, local buffers; across GPUs, peer memory
+ *     opened by IPC handles).  A chunk already in place (dst[j] == partial
+ *     + j (T / tp) H) is not copied.
+ *   Requirements as for pblock_ag_in_proj; ws: optional GEMM split region
+ *   of pblock_rs_out_proj_workspace_bytes(cfg, tp, shards_per_launch)
+ *   bytes (NULL/0 runs every launch unsplit).  Later work on `stream`
+ *   follows every GEMM and copy.  The library keeps 128 HIP events per
+ *   device for this call (created on first use): calls on one device must
+ *   not run concurrently from several host threads.
+ *
+ * pblock_rs_reduce (the receiving side of one rank): y_shard = x_shard +
+ * b_out + sum over q = 0 .. tp-1 of parts[q], summed in fp32 in the order
+ * of q and rounded once; parts[q], x_shard, y_shard: [T / tp, H] in the
+ * activation dtype, 16-byte aligned; b_out: [H].  With parts[q] the chunk
+ * rank q sent here, y_shard is this rank's rows of the block output of
+ * Eq. 2 (the out-projection of all ranks, the bias and the residual). */
+size_t pblock_rs_out_proj_workspace_bytes(const pb_config* cfg, int tp,
+                                          int shards_per_launch);
+pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank,
+                             const void* c, const void* w_out, void* partial,
+                             void* const* dst, int shards_per_launch, void* ws,
+                             size_t ws_bytes, hipStream_t stream, int n_comm,
+                             const hipStream_t* comm_streams);
+pb_status pblock_rs_reduce(const pb_config* cfg, int tp,
+                           const void* const* parts, const void* x_shard,
+                           const void* b_out, void* y_shard,
+                           hipStream_t stream);
+
 /* ------------------------------------------------------------- LAMB step
  * One step of the LAMB optimizer the paper trains with (Section 3.1, "LAMB
  * optimizer"; the layer-wise method of You et al., 2020) over up to

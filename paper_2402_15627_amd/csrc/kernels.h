@@ -73,6 +73,17 @@ int lamb_padded_chunks(long long numel);  // rounded up to a multiple of kLambGr
 void launch_lamb(const LambTable& t, const LambScalars& sc, Dt copy_dt, float2* partial,
                  double2* group, float* ratio, float* ratio_out, hipStream_t s);
 
+// ------------------------------------------------------ reduce-scatter sum
+// y = x + bias + sum over q < n of parts[q], row-major [rows, H] (H a
+// multiple of 8), summed in fp32 in the order of q.
+constexpr int kRsMaxParts = 64;
+struct RsParts {
+  const void* p[kRsMaxParts];
+  int n;
+};
+void launch_rs_reduce(Dt dt, const RsParts& parts, const void* x, const void* bias, void* y,
+                      int rows, int H, hipStream_t s);
+
 // ------------------------------------------------------------------ GEMMs
 // C[m, n] = sum_k A(m, k) B(k, n), fp32 accumulation.
 // A(m, k) is A[m * lda + k] when a_kcontig, else A[k * lda + m]; B(k, n) is

@@ -934,6 +934,25 @@ size_t ag_split_bytes(const pb_config* cfg, int tp, int per_launch) {
                         4);
   return align256(m);
 }
+pb_status check_tp_streams(int tp, int rank, long long T, int per_launch, int n_comm,
+                           const hipStream_t* comm_streams, hipStream_t stream) {
+  if (tp < 1 || tp > kAgMaxTp) return fail(PB_ERR_INVALID_ARG, "tp=%d must be in 1..64", tp);
+  if (rank < 0 || rank >= tp) return fail(PB_ERR_INVALID_ARG, "rank=%d not in 0..tp-1", rank);
+  if (T % tp) return fail(PB_ERR_INVALID_ARG, "tokens=%lld not divisible by tp=%d", T, tp);
+  if (per_launch < 1 || per_launch > tp)
+    return fail(PB_ERR_INVALID_ARG, "shards_per_launch=%d must be in 1..tp", per_launch);
+  if (n_comm < 1 || n_comm > kAgMaxComm)
+    return fail(PB_ERR_INVALID_ARG, "n_comm=%d must be in 1..%d", n_comm, kAgMaxComm);
+  if (!comm_streams) return fail(PB_ERR_INVALID_ARG, "comm_streams is NULL");
+  for (int i = 0; i < n_comm; ++i) {
+    if (comm_streams[i] == stream)
+      return fail(PB_ERR_INVALID_ARG, "comm_streams[%d] equals stream", i);
+    for (int k = 0; k < i; ++k)
+      if (comm_streams[k] == comm_streams[i])
+        return fail(PB_ERR_INVALID_ARG, "comm_streams[%d] repeats comm_streams[%d]", i, k);
+  }
+  return PB_OK;
+}
 }  // namespace
 
 size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
@@ -949,21 +968,7 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
                             int n_comm, const hipStream_t* comm_streams) {
   PB_CHECK(check_config(cfg));
   const Dims d = dims_of(cfg);
-  if (tp < 1 || tp > kAgMaxTp) return fail(PB_ERR_INVALID_ARG, "tp=%d must be in 1..64", tp);
-  if (rank < 0 || rank >= tp) return fail(PB_ERR_INVALID_ARG, "rank=%d not in 0..tp-1", rank);
-  if (d.T % tp) return fail(PB_ERR_INVALID_ARG, "tokens=%lld not divisible by tp=%d", d.T, tp);
-  if (shards_per_launch < 1 || shards_per_launch > tp)
-    return fail(PB_ERR_INVALID_ARG, "shards_per_launch=%d must be in 1..tp", shards_per_launch);
-  if (n_comm < 1 || n_comm > kAgMaxComm)
-    return fail(PB_ERR_INVALID_ARG, "n_comm=%d must be in 1..%d", n_comm, kAgMaxComm);
-  if (!comm_streams) return fail(PB_ERR_INVALID_ARG, "comm_streams is NULL");
-  for (int i = 0; i < n_comm; ++i) {
-    if (comm_streams[i] == stream)
-      return fail(PB_ERR_INVALID_ARG, "comm_streams[%d] equals stream", i);
-    for (int k = 0; k < i; ++k)
-      if (comm_streams[k] == comm_streams[i])
-        return fail(PB_ERR_INVALID_ARG, "comm_streams[%d] repeats comm_streams[%d]", i, k);
-  }
+  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
   if (!shards) return fail(PB_ERR_INVALID_ARG, "shards is NULL");
   for (int j = 0; j < tp; ++j) {
     if (!shards[j] || (uintptr_t)shards[j] % 16)
@@ -1043,6 +1048,142 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
       gemm_rows(0, j0 + n - tp);
     }
   }
+  return finish_launches();
+}
+
+// --------------------------------------- out-projection + reduce-scatter
+namespace {
+// Events of the fused call, per device, created on first use.
+struct RsEvents {
+  bool ready = false;
+  hipEvent_t computed[kAgMaxTp];  // per launch group, on `stream`
+  hipEvent_t sent[kAgMaxTp];      // per chunk, on its comm stream
+};
+RsEvents g_rs[kAgMaxDevices];
+
+size_t rs_split_bytes(const pb_config* cfg, int tp, int per_launch) {
+  const Dims d = dims_of(cfg);
+  const int rows = (int)(d.T / tp);
+  size_t m = 0;
+  for (int k = 1; k <= per_launch; ++k)
+    m = std::max(m, pb::gemm_split_floats(
+                        pb::gemm_split_plan(dt_of(cfg), rows * k, (int)d.H, (int)d.K_out)) *
+                        4);
+  return align256(m);
+}
+
+}  // namespace
+
+size_t pblock_rs_out_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
+  if (check_config(cfg) != PB_OK || tp < 1 || tp > kAgMaxTp || shards_per_launch < 1 ||
+      shards_per_launch > tp || dims_of(cfg).T % tp)
+    return 0;
+  return rs_split_bytes(cfg, tp, shards_per_launch);
+}
+
+pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank, const void* c,
+                             const void* w_out, void* partial, void* const* dst,
+                             int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
+                             int n_comm, const hipStream_t* comm_streams) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
+  if (!dst) return fail(PB_ERR_INVALID_ARG, "dst is NULL");
+  for (int j = 0; j < tp; ++j) {
+    if (!dst[j] || (uintptr_t)dst[j] % 16)
+      return fail(PB_ERR_INVALID_ARG, "dst[%d] is NULL or not 16-byte aligned", j);
+  }
+  PB_CHECK(check_ptr(c, "c"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(partial, "partial"));
+  if (ws_bytes && (!ws || (uintptr_t)ws % 256))
+    return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kAgMaxDevices)
+    return fail(PB_ERR_HIP, "hipGetDevice failed");
+  RsEvents& ev = g_rs[dev];
+  if (!ev.ready) {
+    for (int i = 0; i < kAgMaxTp; ++i)
+      if (hipEventCreateWithFlags(&ev.computed[i], hipEventDisableTiming) != hipSuccess ||
+          hipEventCreateWithFlags(&ev.sent[i], hipEventDisableTiming) != hipSuccess)
+        return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
+    ev.ready = true;
+  }
+  auto ok = [](hipError_t e) { return e == hipSuccess; };
+
+  const pb::Dt dt = dt_of(cfg);
+  const int H = (int)d.H, K_out = (int)d.K_out;
+  const int rows = (int)(d.T / tp);
+  const size_t e = d.esz;
+  const size_t chunk_bytes = (size_t)rows * H * e;
+  float* split_ws = (float*)ws;
+  const size_t split_f = ws_bytes / 4;
+  // P = C W_out^T over a row range, stored in the activation type
+  auto gemm_rows = [&](int j0, int nsh) {
+    const int r0 = j0 * rows, m = nsh * rows;
+    pb::EpiArgs ep;
+    ep.out = at(partial, (long long)r0 * H, e);
+    ep.ld_out = H;
+    ep.split = H;  // every column is a plain store
+    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, true, at(c, (long long)r0 * K_out, e), K_out,
+                    w_out, K_out, m, H, K_out, ep, split_ws, split_f, stream);
+  };
+  // chunks in ring order from rank + 1, so this rank's own rows come last;
+  // each group of shards_per_launch chunks is one launch (two row ranges
+  // when it wraps past the last rank), and each chunk is sent on its comm
+  // stream as soon as its launch has finished
+  int group = 0;
+  for (int k0 = 0; k0 < tp; k0 += shards_per_launch, ++group) {
+    const int k1 = std::min(tp, k0 + shards_per_launch);
+    const int j0 = (rank + 1 + k0) % tp, n = k1 - k0;
+    if (j0 + n <= tp) {
+      gemm_rows(j0, n);
+    } else {
+      gemm_rows(j0, tp - j0);
+      gemm_rows(0, j0 + n - tp);
+    }
+    if (!ok(hipEventRecord(ev.computed[group], stream)))
+      return fail(PB_ERR_HIP, "hipEventRecord failed");
+    for (int k = k0; k < k1; ++k) {
+      const int j = (rank + 1 + k) % tp;
+      hipStream_t cs = comm_streams[k % n_comm];
+      if (!ok(hipStreamWaitEvent(cs, ev.computed[group], 0)))
+        return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+      const char* src = (const char*)partial + (size_t)j * chunk_bytes;
+      if (dst[j] != src &&
+          !ok(hipMemcpyAsync(dst[j], src, chunk_bytes, hipMemcpyDeviceToDeviceNoCU, cs)))
+        return fail(PB_ERR_HIP, "hipMemcpyAsync of chunk %d failed", j);
+      if (!ok(hipEventRecord(ev.sent[k], cs))) return fail(PB_ERR_HIP, "hipEventRecord failed");
+    }
+  }
+  // later work on `stream` follows every send
+  for (int k = 0; k < tp; ++k)
+    if (!ok(hipStreamWaitEvent(stream, ev.sent[k], 0)))
+      return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+  return finish_launches();
+}
+
+pb_status pblock_rs_reduce(const pb_config* cfg, int tp, const void* const* parts,
+                           const void* x_shard, const void* b_out, void* y_shard,
+                           hipStream_t stream) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  if (tp < 1 || tp > pb::kRsMaxParts)
+    return fail(PB_ERR_INVALID_ARG, "tp=%d must be in 1..%d", tp, pb::kRsMaxParts);
+  if (d.T % tp) return fail(PB_ERR_INVALID_ARG, "tokens=%lld not divisible by tp=%d", d.T, tp);
+  if (!parts) return fail(PB_ERR_INVALID_ARG, "parts is NULL");
+  pb::RsParts rp{};
+  rp.n = tp;
+  for (int q = 0; q < tp; ++q) {
+    if (!parts[q] || (uintptr_t)parts[q] % 16)
+      return fail(PB_ERR_INVALID_ARG, "parts[%d] is NULL or not 16-byte aligned", q);
+    rp.p[q] = parts[q];
+  }
+  PB_CHECK(check_ptr(x_shard, "x_shard"));
+  PB_CHECK(check_ptr(b_out, "b_out"));
+  PB_CHECK(check_ptr(y_shard, "y_shard"));
+  pb::launch_rs_reduce(dt_of(cfg), rp, x_shard, b_out, y_shard, (int)(d.T / tp), (int)d.H,
+                       stream);
   return finish_launches();
 }
 

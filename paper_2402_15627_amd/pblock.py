@@ -35,6 +35,7 @@ EXPORTS = (
     "pblock_serial_saved_offsets", "pblock_serial_workspace_bytes", "pblock_serial_forward",
     "pblock_serial_backward", "pblock_lamb_workspace_bytes", "pblock_lamb_step",
     "pblock_ag_in_proj_workspace_bytes", "pblock_ag_in_proj",
+    "pblock_rs_out_proj_workspace_bytes", "pblock_rs_out_proj", "pblock_rs_reduce",
 )
 LAMB_MAX_TENSORS = 16
 
@@ -106,6 +107,10 @@ def load_library(path: str = LIB_PATH):
         "pblock_ag_in_proj_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
         "pblock_ag_in_proj": (c_int, [cfgp, c_int, c_int, POINTER(c_void_p), P, P, P, P, P, c_int,
                                       P, c_size_t, P, c_int, POINTER(c_void_p)]),
+        "pblock_rs_out_proj_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
+        "pblock_rs_out_proj": (c_int, [cfgp, c_int, c_int, P, P, P, POINTER(c_void_p), c_int, P,
+                                       c_size_t, P, c_int, POINTER(c_void_p)]),
+        "pblock_rs_reduce": (c_int, [cfgp, c_int, POINTER(c_void_p), P, P, P, P]),
         "pblock_lamb_step": (c_int, [POINTER(LambConfig), c_int, POINTER(LambTensor), c_int, P, P,
                                      c_size_t, P]),
     }
@@ -299,12 +304,42 @@ def pblock_ag_in_proj(cfg, tp, rank, shards, h, w_in, b_in, z, c, shards_per_lau
     """shards: tp tensors (or addresses), rank j's rows of h; comm_streams: a
     non-empty sequence of streams other than `stream` (torch streams or raw
     handles)."""
+    if len(shards) != tp:
+        raise ValueError(f"{len(shards)} shards for tp={tp}")
     arr = (c_void_p * len(shards))(*[_ptr(t) for t in shards])
     cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
     _check(load_library().pblock_ag_in_proj(
         ctypes.byref(cfg), int(tp), int(rank), arr, _ptr(h), _ptr(w_in), _ptr(b_in), _ptr(z),
         _ptr(c), int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream),
         len(comm_streams), cs))
+
+
+def pblock_rs_out_proj_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch: int) -> int:
+    return load_library().pblock_rs_out_proj_workspace_bytes(ctypes.byref(cfg), int(tp),
+                                                             int(shards_per_launch))
+
+
+def pblock_rs_out_proj(cfg, tp, rank, c, w_out, partial, dst, shards_per_launch, ws, stream,
+                       comm_streams):
+    """dst: tp tensors (or addresses), where rank j receives this rank's
+    chunk j; comm_streams as for pblock_ag_in_proj."""
+    if len(dst) != tp:
+        raise ValueError(f"{len(dst)} destinations for tp={tp}")
+    arr = (c_void_p * len(dst))(*[_ptr(t) for t in dst])
+    cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
+    _check(load_library().pblock_rs_out_proj(
+        ctypes.byref(cfg), int(tp), int(rank), _ptr(c), _ptr(w_out), _ptr(partial), arr,
+        int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream), len(comm_streams), cs))
+
+
+def pblock_rs_reduce(cfg, tp, parts, x_shard, b_out, y_shard, stream=None):
+    """parts: tp tensors (or addresses), the chunks this rank received, in
+    rank order."""
+    if len(parts) != tp:
+        raise ValueError(f"{len(parts)} parts for tp={tp}")
+    arr = (c_void_p * len(parts))(*[_ptr(t) for t in parts])
+    _check(load_library().pblock_rs_reduce(ctypes.byref(cfg), int(tp), arr, _ptr(x_shard),
+                                           _ptr(b_out), _ptr(y_shard), _stream(stream)))
 
 
 def pblock_status_string(status: int) -> str:

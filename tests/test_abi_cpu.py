@@ -339,3 +339,44 @@ def test_ag_in_proj_rejects_bad_arguments_before_launching():
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 8, 1) % 256 == 0
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 8, 9) == 0
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 3, 1) == 0
+
+
+def test_rs_out_proj_and_reduce_reject_bad_arguments_before_launching():
+    lib = pb.load_library()
+    c = good_cfg()  # 13B shape: T = 2048, H = 5120
+
+    def call(cfg=c, tp=8, rank=0, per=1, stream=FAKE, comm=(FAKE + 256,), ws=FAKE,
+             nbytes=1 << 20, dst=None):
+        d = (ctypes.c_void_p * tp)(*(dst or [FAKE] * tp)) if tp > 0 else None
+        cs = (ctypes.c_void_p * max(len(comm), 1))(*comm) if comm else None
+        return lib.pblock_rs_out_proj(ctypes.byref(cfg), tp, rank, FAKE, FAKE, FAKE, d, per, ws,
+                                      nbytes, stream, len(comm), cs)
+
+    assert call(tp=3) == 1 and "divisible" in pb.pblock_last_error()
+    assert call(tp=65) == 1
+    assert call(rank=8) == 1 and call(rank=-1) == 1
+    assert call(per=0) == 1 and call(per=9) == 1
+    assert call(comm=(FAKE,)) == 1
+    assert call(comm=(FAKE + 256, FAKE + 256)) == 1
+    assert call(comm=()) == 1
+    assert call(ws=FAKE + 16) == 1
+    assert call(dst=[FAKE] * 7 + [FAKE + 8]) == 1 and "dst[7]" in pb.pblock_last_error()
+    assert call(dst=[FAKE] * 3 + [None] * 5) == 1 and "dst[3]" in pb.pblock_last_error()
+    assert call(cfg=good_cfg(head_dim=80)) == 2
+    assert pb.pblock_rs_out_proj_workspace_bytes(c, 8, 1) % 256 == 0
+    assert pb.pblock_rs_out_proj_workspace_bytes(c, 8, 9) == 0
+    assert pb.pblock_rs_out_proj_workspace_bytes(c, 3, 1) == 0
+    # the python wrappers refuse a list of the wrong length
+    with pytest.raises(ValueError):
+        pb.pblock_rs_out_proj(c, 8, 0, FAKE, FAKE, FAKE, [FAKE] * 7, 1, None, FAKE, [FAKE + 256])
+    with pytest.raises(ValueError):
+        pb.pblock_rs_reduce(c, 8, [FAKE] * 9, FAKE, FAKE, FAKE)
+
+    def reduce(cfg=c, tp=8, parts=None, x=FAKE, b=FAKE, y=FAKE):
+        arr = (ctypes.c_void_p * tp)(*(parts or [FAKE] * tp)) if tp > 0 else None
+        return lib.pblock_rs_reduce(ctypes.byref(cfg), tp, arr, x, b, y, FAKE)
+
+    assert reduce(tp=3) == 1
+    assert reduce(tp=0) == 1 and reduce(tp=65) == 1
+    assert reduce(parts=[FAKE] * 7 + [FAKE + 4]) == 1 and "parts[7]" in pb.pblock_last_error()
+    assert reduce(y=None) == 1 and reduce(b=FAKE + 2) == 1
