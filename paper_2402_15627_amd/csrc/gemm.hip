@@ -408,6 +408,44 @@ PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, in
   }
 }
 
+// fp32 store of a wave's 64 x 128 block of the tile, staged through the
+// wave's 16 KB of LDS so that every store instruction writes whole lines: per
+// 32-row half, the lanes write their accumulators row-major (the 16-byte
+// chunk index XOR-ed by the row), then read back two 512-byte rows per
+// instruction.  Stored straight from the accumulator layout, each
+// instruction writes 32-byte pieces of 32 rows; the whole-line form makes the
+// weight-gradient GEMMs 3-8% faster, and non-temporal whole-line stores
+// another 1-3% (measured also for the K-slice partials, which the reduction
+// launch reads right after).  acc[i][j][4 jj + e] is row mw + 32 i + fr, column nw + 32 j +
+// 8 jj + 4 fh + e.  All LDS reads of the main loop must be finished (block
+// barrier) before the first call.
+constexpr int kEpiWaveLds = 32 * kWTN * 4;  // one half: 16 KB
+static_assert(kEpiWaveLds * kWavesM * kWavesN <= 4 * kTileBytes, "epilogue staging fits");
+PB_DEV void wave_store_f32_lds(float* __restrict__ out, int ld, const f32x16 (&acc)[kTM][kTN],
+                               int mw, int nw, int M, int N, int fr, int fh, int lane,
+                               unsigned char* buf) {
+#pragma unroll
+  for (int i = 0; i < kTM; ++i) {
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int c = 8 * j + 2 * jj + fh;
+        *reinterpret_cast<f32x4*>(buf + fr * (kWTN * 4) + ((c ^ fr) & 31) * 16) =
+            f32x4{acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
+                  acc[i][j][4 * jj + 3]};
+      }
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const int r = 2 * t + (lane >> 5), c = lane & 31;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(buf + r * (kWTN * 4) + ((c ^ r) & 31) * 16);
+      const int m = mw + 32 * i + r, n = nw + 4 * c;
+      if (m < M && n < N)
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(out + (size_t)m * ld + n));
+    }
+  }
+}
+
 // Work items: the first n_full workgroups compute whole tiles (logical ids
 // 0 .. n_full - 1); the remaining tail * splits workgroups each compute one
 // K-slice of one of the last `tail` tiles and store its fp32 partial tile
@@ -552,21 +590,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  if (slice >= 0) {
-    // partial tile of one K-slice, stored whole (bounds are applied on reduce)
-    float* pt = part + ((size_t)(lid - n_full) * splits + slice) * (kBM * kBN);
-#pragma unroll
-    for (int i = 0; i < kTM; ++i) {
-      const int ml = wm + 32 * i + fr;
-#pragma unroll
-      for (int j = 0; j < kTN; ++j)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const int nl = wn + 32 * j + 8 * jj + 4 * fh;
-          *reinterpret_cast<f32x4*>(pt + ml * kBN + nl) =
-              f32x4{acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
-                    acc[i][j][4 * jj + 3]};
-        }
+  if (slice >= 0 || EPI == Epi::StoreF32) {
+    block_barrier();  // every wave is done with the main loop's LDS
+    unsigned char* buf = smem + wave * kEpiWaveLds;
+    if (slice >= 0) {
+      // partial tile of one K-slice, stored whole (bounds are applied on reduce)
+      float* pt = part + ((size_t)(lid - n_full) * splits + slice) * (kBM * kBN);
+      wave_store_f32_lds(pt, kBN, acc, wm, wn, kBM, kBN, fr, fh, lane, buf);
+    } else {
+      wave_store_f32_lds((float*)ep.out, ep.ld_out, acc, m0 + wm, n0 + wn, M, N, fr, fh, lane,
+                         buf);
     }
     return;
   }
