@@ -408,40 +408,156 @@ PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, in
   }
 }
 
-// fp32 store of a wave's 64 x 128 block of the tile, staged through the
-// wave's 16 KB of LDS so that every store instruction writes whole lines: per
-// 32-row half, the lanes write their accumulators row-major (the 16-byte
-// chunk index XOR-ed by the row), then read back two 512-byte rows per
-// instruction.  Stored straight from the accumulator layout, each
-// instruction writes 32-byte pieces of 32 rows; the whole-line form makes the
-// weight-gradient GEMMs 3-8% faster, and non-temporal whole-line stores
-// another 1-3% (measured also for the K-slice partials, which the reduction
-// launch reads right after).  acc[i][j][4 jj + e] is row mw + 32 i + fr, column nw + 32 j +
-// 8 jj + 4 fh + e.  All LDS reads of the main loop must be finished (block
-// barrier) before the first call.
+// The epilogue of a wave's 64 x 128 block of the tile, staged through the
+// wave's 16 KB of LDS so that every global access of the epilogue covers
+// whole lines.  Per 32-row half, the lanes write their accumulators row-major
+// (the 16-byte chunk index XOR-ed by the row), read them back as four
+// consecutive columns of one row per lane (two rows per instruction), and
+// apply the epilogue to those four columns: fp32 results go out as 512
+// contiguous bytes of a row per 32 lanes, bf16 results and the bias,
+// residual and GeLU inputs as 256.  Applied straight from the accumulator
+// layout, each access would cover 8 to 32 bytes of 32 different rows.
+// Weight gradients and K-slice partials (part_tile; ld kBN, no epilogue) are
+// written with non-temporal stores.  For LnGrad each 16-lane group holds one
+// row's 64-column group and sums its row terms across the group.
+// acc[i][j][4 jj + e] is row mw + 32 i + fr, column nw + 32 j + 8 jj + 4 fh +
+// e.  All LDS reads of the main loop must be finished (block barrier) first.
 constexpr int kEpiWaveLds = 32 * kWTN * 4;  // one half: 16 KB
 static_assert(kEpiWaveLds * kWavesM * kWavesN <= 4 * kTileBytes, "epilogue staging fits");
-PB_DEV void wave_store_f32_lds(float* __restrict__ out, int ld, const f32x16 (&acc)[kTM][kTN],
-                               int mw, int nw, int M, int N, int fr, int fh, int lane,
-                               unsigned char* buf) {
+template <Epi EPI, bool GT>
+PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
+                              const f32x16 (&acc)[kTM][kTN], int mw, int nw, int M, int N, int fr,
+                              int fh, int lane, unsigned char* buf) {
+  const int c = lane & 31, hi = lane >> 5;
+  const int n = nw + 4 * c;  // this lane's four columns, the same in every row
+  const int ncl = min(n, N - 4);
+  // inputs that depend only on the column, loaded once
+  float b4[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (EPI == Epi::BiasGelu || EPI == Epi::BiasResid || EPI == Epi::LnGrad)
+    if (!part_tile) load4<bf16>((const bf16*)ep.bias + ncl, b4);
+  const bool dg_aux = EPI == Epi::DgeluSplit && ep.split < N;  // any GeLU' column at all
 #pragma unroll
   for (int i = 0; i < kTM; ++i) {
 #pragma unroll
     for (int j = 0; j < kTN; ++j)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int c = 8 * j + 2 * jj + fh;
-        *reinterpret_cast<f32x4*>(buf + fr * (kWTN * 4) + ((c ^ fr) & 31) * 16) =
+        const int cw = 8 * j + 2 * jj + fh;
+        *reinterpret_cast<f32x4*>(buf + fr * (kWTN * 4) + ((cw ^ fr) & 31) * 16) =
             f32x4{acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
                   acc[i][j][4 * jj + 3]};
       }
+    const int m0h = mw + 32 * i;  // first row of this half
+    // Per-row inputs of the half, all issued before any result is stored (a
+    // wait for a load also waits for every earlier store): the residual,
+    // GeLU input or LayerNorm input of this lane's four columns in each of
+    // its 16 rows, at clamped addresses; LayerNorm statistics one row per
+    // lane, broadcast below.
+    u32x2 in2[16];
+    float mu_l = 0.f, rs_l = 0.f;
+    if (!part_tile) {
+      if constexpr (EPI == Epi::BiasResid || EPI == Epi::LnGrad) {
+        const bf16* src = (const bf16*)(EPI == Epi::BiasResid ? ep.resid : ep.aux);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+          const int mc = min(m0h + 2 * t + hi, M - 1);
+          in2[t] = *reinterpret_cast<const u32x2*>(src + (size_t)mc * ep.ld_out + ncl);
+        }
+      }
+      if constexpr (EPI == Epi::DgeluSplit) {
+        if (dg_aux) {
+          const int col = max(ncl - ep.split, 0) + ep.col2;
+#pragma unroll
+          for (int t = 0; t < 16; ++t) {
+            const int mc = min(m0h + 2 * t + hi, M - 1);
+            in2[t] = *reinterpret_cast<const u32x2*>((const bf16*)ep.aux +
+                                                     (size_t)mc * ep.ld_out2 + col);
+          }
+        }
+      }
+      if constexpr (EPI == Epi::LnGrad) {
+        const int mr = min(m0h + c, M - 1);
+        mu_l = ep.mean[mr];
+        rs_l = ep.rstd[mr];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
-      const int r = 2 * t + (lane >> 5), c = lane & 31;
+      const int r = 2 * t + hi;
       const f32x4 v = *reinterpret_cast<const f32x4*>(buf + r * (kWTN * 4) + ((c ^ r) & 31) * 16);
-      const int m = mw + 32 * i + r, n = nw + 4 * c;
-      if (m < M && n < N)
-        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(out + (size_t)m * ld + n));
+      const int m = m0h + r;
+      const bool ok = m < M && n < N;
+      if (part_tile) {
+        if (ok)
+          __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(part_tile + m * kBN + n));
+        continue;
+      }
+      float o[4];
+      if constexpr (EPI == Epi::StoreF32) {
+        if (ok)
+          __builtin_nontemporal_store(
+              v, reinterpret_cast<f32x4*>((float*)ep.out + (size_t)m * ep.ld_out + n));
+      } else if constexpr (EPI == Epi::BiasGelu) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = v[e] + b4[e];
+        if (ok) {
+          store4((bf16*)ep.out + (size_t)m * ep.ld_out + n, o);
+          if (n >= ep.split) {
+            float g[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) g[e] = gelu<GT>(o[e]);
+            store4((bf16*)ep.out2 + (size_t)m * ep.ld_out2 + (n - ep.split) + ep.col2, g);
+          }
+        }
+      } else if constexpr (EPI == Epi::BiasResid) {
+        const float rr[4] = {lo_bf(in2[t][0]), hi_bf(in2[t][0]), lo_bf(in2[t][1]),
+                             hi_bf(in2[t][1])};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = v[e] + b4[e] + rr[e];
+        if (ok) store4((bf16*)ep.out + (size_t)m * ep.ld_out + n, o);
+      } else if constexpr (EPI == Epi::DgeluSplit) {
+        if (n < ep.split) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = v[e];
+          if (ok) store4((bf16*)ep.out + (size_t)m * ep.ld_out + n, o);
+        } else {
+          const float u[4] = {lo_bf(in2[t][0]), hi_bf(in2[t][0]), lo_bf(in2[t][1]),
+                              hi_bf(in2[t][1])};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = v[e] * gelu_grad<GT>(u[e]);
+          if (ok)
+            store4((bf16*)ep.out2 + (size_t)m * ep.ld_out2 + (n - ep.split) + ep.col2, o);
+        }
+      } else {  // LnGrad: dh, and the row terms of this lane's 64-column group
+        const float xv[4] = {lo_bf(in2[t][0]), hi_bf(in2[t][0]), lo_bf(in2[t][1]),
+                             hi_bf(in2[t][1])};
+        const float mu_a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mu_l), 2 * t));
+        const float mu_b =
+            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mu_l), 2 * t + 1));
+        const float rs_a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rs_l), 2 * t));
+        const float rs_b =
+            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rs_l), 2 * t + 1));
+        const float mu = hi ? mu_b : mu_a, rs = hi ? rs_b : rs_a;
+        float s1 = 0.f, s2 = 0.f;
+        if (ok) {
+          const float dh[4] = {v[0], v[1], v[2], v[3]};
+          store4((float*)ep.out + (size_t)m * ep.ld_out + n, dh);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float g = b4[e] * v[e];
+            s1 += g;
+            s2 += g * ((xv[e] - mu) * rs);
+          }
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) {
+          s1 += __shfl_xor(s1, off, 64);
+          s2 += __shfl_xor(s2, off, 64);
+        }
+        if ((c & 15) == 0 && ok)  // n is the group's first column
+          ep.rowpart[(size_t)m * ep.rowpart_ld + n / 64] = make_float2(s1, s2);
+      }
     }
   }
 }
@@ -590,20 +706,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  if (slice >= 0 || EPI == Epi::StoreF32) {
-    block_barrier();  // every wave is done with the main loop's LDS
-    unsigned char* buf = smem + wave * kEpiWaveLds;
-    if (slice >= 0) {
-      // partial tile of one K-slice, stored whole (bounds are applied on reduce)
-      float* pt = part + ((size_t)(lid - n_full) * splits + slice) * (kBM * kBN);
-      wave_store_f32_lds(pt, kBN, acc, wm, wn, kBM, kBN, fr, fh, lane, buf);
-    } else {
-      wave_store_f32_lds((float*)ep.out, ep.ld_out, acc, m0 + wm, n0 + wn, M, N, fr, fh, lane,
-                         buf);
-    }
-    return;
+  block_barrier();  // every wave is done with the main loop's LDS
+  unsigned char* buf = smem + wave * kEpiWaveLds;
+  if (slice >= 0) {
+    // partial tile of one K-slice, stored whole (bounds are applied on reduce)
+    float* pt = part + ((size_t)(lid - n_full) * splits + slice) * (kBM * kBN);
+    wave_epilogue_lds<EPI, GT>(ep, pt, acc, wm, wn, kBM, kBN, fr, fh, lane, buf);
+  } else {
+    wave_epilogue_lds<EPI, GT>(ep, nullptr, acc, m0 + wm, n0 + wn, M, N, fr, fh, lane, buf);
   }
-  wave_epilogue<EPI, GT>(ep, acc, m0 + wm, n0 + wn, M, N, fr, fh);
 }
 
 // Sum of the K-slice partials of each tail tile, in slice order (so the
