@@ -417,8 +417,9 @@ PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, in
 // contiguous bytes of a row per 32 lanes, bf16 results and the bias,
 // residual and GeLU inputs as 256.  Applied straight from the accumulator
 // layout, each access would cover 8 to 32 bytes of 32 different rows.
-// Weight gradients and K-slice partials (part_tile; ld kBN, no epilogue) are
-// written with non-temporal stores.  For LnGrad each 16-lane group holds one
+// Weight gradients are written with non-temporal stores; K-slice partials
+// (part_tile: ld kBN, no epilogue), which the reduction reads right after,
+// with ordinary ones.  For LnGrad each 16-lane group holds one
 // row's 64-column group and sums its row terms across the group.
 // acc[i][j][4 jj + e] is row mw + 32 i + fr, column nw + 32 j + 8 jj + 4 fh +
 // e.  All LDS reads of the main loop must be finished (block barrier) first.
@@ -489,8 +490,7 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
       const int m = m0h + r;
       const bool ok = m < M && n < N;
       if (part_tile) {
-        if (ok)
-          __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(part_tile + m * kBN + n));
+        if (ok) *reinterpret_cast<f32x4*>(part_tile + m * kBN + n) = v;
         continue;
       }
       float o[4];
