@@ -55,9 +55,14 @@
  * ---------------------------------------------------------------- ownership
  * The caller allocates every buffer (inputs, outputs, the stash, the
  * workspace).  The library allocates no device memory and keeps no per-call
- * state.  Every call is asynchronous on the given HIP stream; buffers must stay
- * valid until the stream has passed the call.  Calls on disjoint buffers may
- * run concurrently.  Parameter gradients are overwritten, not accumulated.
+ * state.  Two exceptions, both host-side: the pipelined all-gather and
+ * reduce-scatter calls keep HIP events per device (created on their first
+ * call and held until the process ends; calls of the same one of them must
+ * not overlap on one device), and pblock_set_step_events keeps a
+ * process-wide copy of the caller's event handles.  Every call is
+ * asynchronous on the given HIP stream; buffers must stay valid until the
+ * stream has passed the call.  Other calls on disjoint buffers may run
+ * concurrently.  Parameter gradients are overwritten, not accumulated.
  *
  * ---------------------------------------------------------------- errors
  * Functions return a pb_status.  Arguments are checked on the host before any
