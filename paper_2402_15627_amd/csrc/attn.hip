@@ -191,6 +191,23 @@ PB_DEV bf16x8 load_row_frag(const bf16* p, bool ok) {
   return ok ? __builtin_bit_cast(bf16x8, v) : bf16x8{};
 }
 
+// Work order across heads.  The bf16 kernels' grids are (blocks, heads,
+// batch) and workgroups start in linear order, x fastest: head after head.
+// Within a head the block index runs from the longest block (most tiles
+// under the causal window) to the shortest, so in that order the longest
+// blocks of the last heads start only once earlier heads' workgroups have
+// left, and the chip idles while they finish.  Renumbering the linear id
+// with the block index slowest starts the longest block of every head first.
+struct WorkItem {
+  int bx, head, b;
+};
+PB_DEV WorkItem work_item() {
+  const int hb_n = (int)(gridDim.y * gridDim.z);
+  const int L = (int)(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z));
+  const int hb = L % hb_n;
+  return WorkItem{L / hb_n, hb % (int)gridDim.y, hb / (int)gridDim.y};
+}
+
 // ============================================================== forward
 // Workgroup: 32 kWavesQ queries of one (batch row, head); wave w owns queries
 // q0 + 32 w .. +31, lane l query q0 + 32 w + (l & 31).  Per key tile:
@@ -209,14 +226,15 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
   auto v_off = [&](int s) { return (2 * s + 1) * TB; };
 
   const int nqb = (S + NB - 1) / NB;
-  const int chunk = (int)blockIdx.x % nc;
-  const int q0 = (nqb - 1 - (int)blockIdx.x / nc) * NB;  // longest rows first
+  const WorkItem wi = work_item();
+  const int chunk = wi.bx % nc;
+  const int q0 = (nqb - 1 - wi.bx / nc) * NB;  // longest rows first
   const int ntot = qblock_tiles(q0, S, W);
   const int t_begin = chunk * cs;
   if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
   const int t_end = min(ntot, t_begin + cs);
   const bool split = ntot > cs;
-  const int head = blockIdx.y, b = blockIdx.z;
+  const int head = wi.head, b = wi.b;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int fr = lane & 31, fh = lane >> 5;
@@ -463,7 +481,7 @@ PB_DEV void dkdv_body(
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV, int ld_d,
     int S, int H, int W, float scale, int cs, int nc, float* __restrict__ pdk,
-    float* __restrict__ pdv, int bx) {
+    float* __restrict__ pdv, int bx, int head, int b) {
   constexpr int TL = kTLdkv;
   constexpr int NB = kBlockK;
   constexpr int TB = TL * 2 * D;
@@ -484,7 +502,6 @@ PB_DEV void dkdv_body(
   if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
   const int t_end = min(ntot, t_begin + cs);
   const bool split = ntot > cs;
-  const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int grp = wave & 1;
@@ -629,7 +646,7 @@ PB_DEV void dq_body(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     const bf16* __restrict__ dO, int ld_o, const float* __restrict__ lse,
     const float* __restrict__ delta, bf16* __restrict__ dQ, int ld_d, int S, int H, int W,
-    float scale, int cs, int nc, float* __restrict__ pdq, int bx) {
+    float scale, int cs, int nc, float* __restrict__ pdq, int bx, int head, int b) {
   constexpr int TL = kTL;
   constexpr int NB = kBlockQ;
   constexpr int TB = TL * 2 * D;
@@ -646,7 +663,6 @@ PB_DEV void dq_body(
   if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
   const int t_end = min(ntot, t_begin + cs);
   const bool split = ntot > cs;
-  const int head = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int fr = lane & 31, fh = lane >> 5;
@@ -770,13 +786,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     int nxk, int q_cs, int q_nc, float* __restrict__ pdk, float* __restrict__ pdv,
     float* __restrict__ pdq) {
   static_assert(64 * kWavesK == 256 && 64 * kWavesQ == 256, "one block size for both roles");
-  const int bx = (int)blockIdx.x;
+  // rank r of the work order (block index slowest, see work_item) alternates
+  // the two roles, each longest first, until the shorter list runs out
+  const WorkItem wi = work_item();
+  const int r = wi.bx, nxq = (int)gridDim.x - nxk, mn = min(nxk, nxq);
+  int bx;  // < nxk: dK/dV block bx; else dQ block bx - nxk
+  if (r < 2 * mn) bx = (r & 1) ? nxk + (r >> 1) : (r >> 1);
+  else bx = nxk > nxq ? r - mn : nxk + (r - mn);
   if (bx < nxk)
     dkdv_body<D>(Q, K, V, ld, dO, ld_o, lse, delta, dK, dV, ld_d, S, H, W, scale, kv_cs, kv_nc,
-                 pdk, pdv, bx);
+                 pdk, pdv, bx, wi.head, wi.b);
   else
     dq_body<D>(Q, K, V, ld, dO, ld_o, lse, delta, dQ, ld_d, S, H, W, scale, q_cs, q_nc, pdq,
-               bx - nxk);
+               bx - nxk, wi.head, wi.b);
 }
 
 // ============================================================ fp32 path
