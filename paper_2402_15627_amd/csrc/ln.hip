@@ -121,7 +121,7 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
     const T* __restrict__ gamma, const float* __restrict__ dh, const float2* __restrict__ rowpart,
     int ngroups, const T* __restrict__ dy, T* __restrict__ dx, float* __restrict__ part_dg,
     float* __restrict__ part_db, float* __restrict__ part_dy, int rows, int H) {
-  __shared__ float stat[kApplyRows][2];
+  __shared__ float stat[kApplyRows][4];  // mean(g), mean(g xhat), mean, rstd
   const int ncb = (H + kApplyCols - 1) / kApplyCols;
   const int cb = (int)blockIdx.x % ncb, chunk = (int)blockIdx.x / ncb;
   const int r0 = chunk * kApplyRows;
@@ -144,6 +144,8 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
     if (l == 0) {
       stat[rr][0] = s1 / (float)H;
       stat[rr][1] = s2 / (float)H;
+      stat[rr][2] = rr < nr ? mean[r0 + rr] : 0.f;
+      stat[rr][3] = rr < nr ? rstd[r0 + rr] : 0.f;
     }
   }
   __syncthreads();
@@ -153,24 +155,45 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
   load8(gamma + c, gm);
 #pragma unroll
   for (int e = 0; e < 8; ++e) adg[e] = adb[e] = ady[e] = 0.f;
-#pragma unroll 2
-  for (int rr = 0; rr < nr; ++rr) {
-    const size_t off = (size_t)(r0 + rr) * H + c;
-    float xv[8], d[8], yv[8], o[8];
-    load8_stream(x + off, xv);
-    load8_stream(dh + off, d);
-    load8_stream(dy + off, yv);
-    const float mu = mean[r0 + rr], rs = rstd[r0 + rr];
-    const float m1 = stat[rr][0], m2 = stat[rr][1];
+  // Rows in batches of kBatch, double-buffered: the next batch's loads are
+  // issued before this batch's dx stores, so waiting for them never waits for
+  // a store as well (one counter covers both; loaded one batch at a time
+  // after the previous stores, every batch paid the full load latency).
+  constexpr int kBatch = 2, kBatches = kApplyRows / kBatch;
+  float xv[2][kBatch][8], dv[2][kBatch][8], yv[2][kBatch][8];
+  auto load_batch = [&](int buf, int rb) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float xh = (xv[e] - mu) * rs;
-      adg[e] += d[e] * xh;
-      adb[e] += d[e];
-      ady[e] += yv[e];
-      o[e] = yv[e] + rs * (gm[e] * d[e] - m1 - xh * m2);
+    for (int i = 0; i < kBatch; ++i) {
+      const size_t off = (size_t)(r0 + min(rb + i, nr - 1)) * H + c;
+      load8_stream(x + off, xv[buf][i]);
+      load8_stream(dh + off, dv[buf][i]);
+      load8_stream(dy + off, yv[buf][i]);
     }
-    store8(dx + off, o);
+  };
+  load_batch(0, 0);
+#pragma unroll
+  for (int bt = 0; bt < kBatches; ++bt) {
+    const int cur = bt & 1;
+    if (bt + 1 < kBatches && (bt + 1) * kBatch < nr) load_batch(cur ^ 1, (bt + 1) * kBatch);
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const int rr = bt * kBatch + i;
+      if (rr < nr) {
+        const size_t off = (size_t)(r0 + rr) * H + c;
+        const float m1 = stat[rr][0], m2 = stat[rr][1], mu = stat[rr][2], rs = stat[rr][3];
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = dv[cur][i][e];
+          const float xh = (xv[cur][i][e] - mu) * rs;
+          adg[e] += d * xh;
+          adb[e] += d;
+          ady[e] += yv[cur][i][e];
+          o[e] = yv[cur][i][e] + rs * (gm[e] * d - m1 - xh * m2);
+        }
+        store8(dx + off, o);
+      }
+    }
   }
   const size_t prow = (size_t)chunk * H + c;
   store8(part_dg + prow, adg);
