@@ -84,7 +84,9 @@ def step_work(s):
         "dh": ("mfma", 2 * T * n_in * H),
         "dw_in": ("mfma", 2 * n_in * H * T),
         "db_in": ("hbm", T * n_in * e + 4 * n_in),
-        "ln_bwd": ("hbm", 3 * T * H * e + 4 * T * H + 8 * T + 12 * H),
+        # x, dh and dy read, dx written (dh in the activation type), the row
+        # statistics, and the three column-sum partial rows
+        "ln_bwd": ("hbm", 4 * T * H * e + 8 * T + 12 * H),
     }
 
 

@@ -33,8 +33,10 @@ namespace {
 // Four consecutive output columns n..n+3 of row m.  GT: tanh form of GeLU.
 template <typename T, Epi EPI, bool GT>
 PB_DEV void epi_store4(const EpiArgs& ep, int m, int n, const float* v) {
-  if constexpr (EPI == Epi::StoreF32 || EPI == Epi::LnGrad) {
+  if constexpr (EPI == Epi::StoreF32) {
     store4((float*)ep.out + (size_t)m * ep.ld_out + n, v);
+  } else if constexpr (EPI == Epi::LnGrad) {
+    store4((T*)ep.out + (size_t)m * ep.ld_out + n, v);
   } else if constexpr (EPI == Epi::BiasGelu) {
     float b[4], z[4];
     load4((const T*)ep.bias + n, b);
@@ -542,7 +544,7 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
         float s1 = 0.f, s2 = 0.f;
         if (ok) {
           const float dh[4] = {v[0], v[1], v[2], v[3]};
-          store4((float*)ep.out + (size_t)m * ep.ld_out + n, dh);
+          store4((bf16*)ep.out + (size_t)m * ep.ld_out + n, dh);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float g = b4[e] * v[e];

@@ -22,7 +22,7 @@ void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta
 // part_dbeta and part_dy [ln_backward_chunks(rows), H].
 int ln_backward_chunks(int rows);
 void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
-                        const void* gamma, const float* dh, const float2* rowpart,
+                        const void* gamma, const void* dh, const float2* rowpart,
                         const void* dy, void* dx, float* part_dgamma, float* part_dbeta,
                         float* part_dy, int rows, int H, hipStream_t s);
 
@@ -96,7 +96,7 @@ enum class Epi {
   DgeluSplit,  // n < split: out[m * ld_out + n] = acc;
                // n >= split: with c = n - split + col2,
                //   out2[m * ld_out2 + c] = acc * gelu'(aux[m * ld_out2 + c])
-  LnGrad,      // out_f32[m * ld_out + n] = acc (= dh), and the LayerNorm
+  LnGrad,      // out[m * ld_out + n] = acc (= dh, activation type), and the LayerNorm
                // backward's row terms per 64-column group g = n / 64:
                //   rowpart[m * rowpart_ld + g] = (sum gamma dh, sum gamma dh xhat)
                // with gamma = bias[n], xhat = (aux[m * ld_out + n] - mean[m]) rstd[m]

@@ -118,7 +118,7 @@ constexpr int kApplyCols = kApplyThreads * 8;
 template <typename T>
 __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
     const T* __restrict__ x, const float* __restrict__ mean, const float* __restrict__ rstd,
-    const T* __restrict__ gamma, const float* __restrict__ dh, const float2* __restrict__ rowpart,
+    const T* __restrict__ gamma, const T* __restrict__ dh, const float2* __restrict__ rowpart,
     int ngroups, const T* __restrict__ dy, T* __restrict__ dx, float* __restrict__ part_dg,
     float* __restrict__ part_db, float* __restrict__ part_dy, int rows, int H) {
   __shared__ float stat[kApplyRows][4];  // mean(g), mean(g xhat), mean, rstd
@@ -322,18 +322,20 @@ void launch_ln_forward(Dt dt, const void* x, const void* gamma, const void* beta
 int ln_backward_chunks(int rows) { return (rows + kApplyRows - 1) / kApplyRows; }
 
 void launch_ln_backward(Dt dt, const void* x, const float* mean, const float* rstd,
-                        const void* gamma, const float* dh, const float2* rowpart,
+                        const void* gamma, const void* dh, const float2* rowpart,
                         const void* dy, void* dx, float* part_dgamma, float* part_dbeta,
                         float* part_dy, int rows, int H, hipStream_t s) {
   const unsigned grid = (unsigned)((H + kApplyCols - 1) / kApplyCols) * ln_backward_chunks(rows);
   const int ng = ln_row_groups(H);
   if (dt == Dt::BF16)
     ln_bwd_apply<bf16><<<grid, kApplyThreads, 0, s>>>(
-        (const bf16*)x, mean, rstd, (const bf16*)gamma, dh, rowpart, ng, (const bf16*)dy,
+        (const bf16*)x, mean, rstd, (const bf16*)gamma, (const bf16*)dh, rowpart, ng,
+        (const bf16*)dy,
         (bf16*)dx, part_dgamma, part_dbeta, part_dy, rows, H);
   else
     ln_bwd_apply<float><<<grid, kApplyThreads, 0, s>>>(
-        (const float*)x, mean, rstd, (const float*)gamma, dh, rowpart, ng, (const float*)dy,
+        (const float*)x, mean, rstd, (const float*)gamma, (const float*)dh, rowpart, ng,
+        (const float*)dy,
         (float*)dx, part_dgamma, part_dbeta, part_dy, rows, H);
 }
 

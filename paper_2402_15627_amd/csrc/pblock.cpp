@@ -161,7 +161,7 @@ BwdLayout bwd_layout(const Dims& d) {
   const int nblk = pb::ln_backward_chunks((int)d.T);
   L.d_o = take((size_t)(d.T * d.A) * d.esz);
   L.dz = take((size_t)(d.T * d.N_in) * d.esz);
-  L.dh = take((size_t)(d.T * d.H) * 4);
+  L.dh = take((size_t)(d.T * d.H) * d.esz);
   L.delta = take((size_t)(d.B * d.heads * d.S) * 4);
   L.rowpart = take((size_t)d.T * pb::ln_row_groups((int)d.H) * sizeof(float2));
   L.pdg = take((size_t)nblk * d.H * 4);
@@ -239,7 +239,7 @@ SerialBwdLayout serial_bwd_layout(const Dims& d) {
   const int nblk = pb::ln_backward_chunks((int)d.T);
   L.d_o = take((size_t)(d.T * d.A) * d.esz);
   L.dz = take((size_t)(d.T * d.N_in) * d.esz);
-  L.dh = take((size_t)(d.T * d.H) * 4);
+  L.dh = take((size_t)(d.T * d.H) * d.esz);
   L.dx1 = take((size_t)(d.T * d.H) * d.esz);
   L.delta = take((size_t)(d.B * d.heads * d.S) * 4);
   L.rowpart = take((size_t)d.T * pb::ln_row_groups((int)d.H) * sizeof(float2));
@@ -467,7 +467,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   char* wb = (char*)ws;
   void* d_o = wb + W.d_o;
   void* dz = wb + W.dz;
-  float* dh = (float*)(wb + W.dh);
+  void* dh = wb + W.dh;
   float* delta = (float*)(wb + W.delta);
   float2* rowpart = (float2*)(wb + W.rowpart);
   float* pdg = (float*)(wb + W.pdg);
@@ -508,8 +508,9 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
                              K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
                              N_in, split_ws, split_f * 4, stream);
   }
-  // B4: dh = dZ W_in (fp32); its epilogue also forms the LayerNorm
-  // backward's row terms (sums of gamma dh and gamma dh xhat per 64 columns)
+  // B4: dh = dZ W_in, stored in the activation type; its epilogue also forms
+  // the LayerNorm backward's row terms (sums of gamma dh and gamma dh xhat per
+  // 64 columns) from the fp32 accumulators
   pb::EpiArgs e4;
   e4.out = dh;
   e4.ld_out = H;
@@ -814,7 +815,7 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   char* wb = (char*)ws;
   void* d_o = wb + W.d_o;
   void* dz = wb + W.dz;
-  float* dh = (float*)(wb + W.dh);
+  void* dh = wb + W.dh;
   void* dx1 = wb + W.dx1;
   float* delta = (float*)(wb + W.delta);
   float2* rowpart = (float2*)(wb + W.rowpart);
