@@ -499,7 +499,8 @@ def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     """The in-projection pipelined with the all-gather of its input over tp
     ranks (shards copied on comm streams, GEMM launches over groups of
     shards as they land), against the GEMM alone and the copies followed by
-    one GEMM.  Each variant is timed with events on the compute stream."""
+    one GEMM.  Rank 0's own shard is in place; the other tp - 1 are copied.
+    Each variant is timed with events on the compute stream."""
     import torch
     T, H = shape.tokens, shape.hidden
     cfg = pb.config_from_shape(shape)
@@ -516,11 +517,12 @@ def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     def timed(per, in_place):
         nws = pb.pblock_ag_in_proj_workspace_bytes(cfg, tp, per)
         ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
-        if in_place:
-            h.copy_(src)
-            shards = [h[j * rows:(j + 1) * rows] for j in range(tp)]
-        else:
-            shards = [src[j * rows:(j + 1) * rows] for j in range(tp)]
+        # this rank's own shard is its local LayerNorm output, already in
+        # place in h; the others arrive from the peers (all in place: no
+        # copies at all)
+        h.copy_(src)
+        shards = [h[j * rows:(j + 1) * rows] if (in_place or j == 0) else
+                  src[j * rows:(j + 1) * rows] for j in range(tp)]
         torch.cuda.synchronize()
 
         def call():
@@ -549,8 +551,8 @@ def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     """The out-projection's partial sums pipelined with their reduce-scatter
     over tp ranks (row chunks sent on comm streams as their GEMM launch
     finishes), against the GEMM alone and one GEMM followed by the copies;
-    and the receiving side's sum of tp chunks.  Events on the compute
-    stream."""
+    and the receiving side's sum of tp chunks.  Rank 0's own chunk stays in
+    place; the other tp - 1 are copied.  Events on the compute stream."""
     import torch
     T, H = shape.tokens, shape.hidden
     cfg = pb.config_from_shape(shape)
@@ -579,8 +581,10 @@ def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     def send(per, in_place):
         nws = pb.pblock_rs_out_proj_workspace_bytes(cfg, tp, per)
         ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
-        dst = ([partial[j * rows:(j + 1) * rows] for j in range(tp)] if in_place
-               else [recv[j] for j in range(tp)])
+        # this rank's own chunk stays in place (it is reduced locally); the
+        # others go to the peers' receive buffers (all in place: no copies)
+        dst = [partial[j * rows:(j + 1) * rows] if (in_place or j == 0) else recv[j]
+               for j in range(tp)]
         return lambda: pb.pblock_rs_out_proj(cfg, tp, 0, c, dev["w_out"], partial, dst, per, ws,
                                              stream, comm)
 
