@@ -249,8 +249,11 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
  * streams in ring order from `rank` (rank, rank + 1, ...; the k-th on
  * comm_streams[k % n_comm]), and the in-projection runs on `stream` in
  * launches of shards_per_launch shards each, every launch waiting (by
- * event) only for its own shards.  shards_per_launch = tp is the
- * unpipelined order: all copies, then one GEMM.
+ * event) only for its own shards.  Shards already in place at the head of
+ * that order (this rank's own LayerNorm output, say) need no copy and form
+ * a first launch of their own, which runs while the first copies land.
+ * shards_per_launch = tp is the unpipelined order: all copies, then one
+ * GEMM.
  *
  * shards[j]: rank j's rows of h, [T / tp, H] in the activation dtype (on
  *   one GPU, buffers in local memory; across GPUs, peer memory opened by IPC

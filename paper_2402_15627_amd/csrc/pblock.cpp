@@ -1036,11 +1036,17 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
     pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, at(h, (long long)r0 * H, e), H, w_in, H,
                     m, N_in, H, e1, split_ws, split_f, stream);
   };
-  for (int k0 = 0; k0 < tp; k0 += shards_per_launch) {
-    const int k1 = std::min(tp, k0 + shards_per_launch);
-    for (int k = k0; k < k1; ++k)
-      if (!ok(hipStreamWaitEvent(stream, ev.landed[k], 0)))
-        return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+  // Shards already in place at the head of the ring order (this rank's own
+  // LayerNorm output, typically) need no copy: unless the call is unpipelined
+  // they form a first launch of their own, which runs while the first copies
+  // land; the rest go in groups of shards_per_launch.
+  int ready = 0;
+  while (ready < tp && shards[(rank + ready) % tp] == (char*)h + (size_t)((rank + ready) % tp) * shard_bytes)
+    ++ready;
+  auto launch_group = [&](int k0, int k1, bool wait) -> bool {
+    if (wait)
+      for (int k = k0; k < k1; ++k)
+        if (!ok(hipStreamWaitEvent(stream, ev.landed[k], 0))) return false;
     const int j0 = (rank + k0) % tp, n = k1 - k0;
     if (j0 + n <= tp) {
       gemm_rows(j0, n);
@@ -1048,7 +1054,16 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
       gemm_rows(j0, tp - j0);
       gemm_rows(0, j0 + n - tp);
     }
+    return true;
+  };
+  int k0 = 0;
+  if (ready > 0 && ready < tp && shards_per_launch < tp) {
+    if (!launch_group(0, ready, false)) return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+    k0 = ready;
   }
+  for (; k0 < tp; k0 += shards_per_launch)
+    if (!launch_group(k0, std::min(tp, k0 + shards_per_launch), true))
+      return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
   return finish_launches();
 }
 

@@ -93,6 +93,9 @@ SMALL_F32 = BlockShape("ag_small_f32", 2, 48, 128, 2, 64, 96, 16, "f32", w_std=0
     (1, 0, 1, (), 1), (1, 0, 1, (0,), 1), (4, 0, 1, (), 1), (4, 2, 2, (2,), 1),
     (8, 5, 3, (5,), 1), (8, 7, 8, (), 3), (6, 1, 4, (0, 1, 2, 3, 4, 5), 2), (8, 6, 2, (), 8),
     (5, 3, 2, (), 4),
+    # several shards in place at the head of the ring order: a first launch of
+    # their own (the second case's run wraps past the last rank)
+    (8, 2, 2, (2, 3, 4), 2), (5, 4, 2, (4, 0), 3),
 ])
 def test_ag_in_proj_matches_oracle(tp, rank, n_comm, in_place, per):
     _say(f"[gpu] ag in-proj tp={tp} rank={rank} n_comm={n_comm} in_place={in_place} per={per}")
