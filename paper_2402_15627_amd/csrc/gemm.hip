@@ -13,7 +13,9 @@
 //     registers on its way into LDS.
 // The MFMA is issued with the roles of the operands swapped (the N tile as
 // MFMA "A"), so each lane ends up holding four consecutive output columns of
-// one row: 8- or 16-byte epilogue stores.
+// one row.  The DMA kernel stages its accumulators through LDS before the
+// epilogue so that the epilogue's loads and stores cover whole lines; the
+// register-staged kernel applies the epilogue from the accumulator layout.
 //
 // The epilogues carry the block's elementwise work (MegaScale Section 3.3
 // fuses these fine-grained ops): in-projection bias + GeLU writing both U and

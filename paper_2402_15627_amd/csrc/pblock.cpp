@@ -222,7 +222,7 @@ size_t serial_split_bwd(const Dims& d, pb::Dt dt) {
   return std::max(m, pb::attn_bwd_partial_bytes(a, pb::attn_bwd_split_plan(dt, a)));
 }
 
-// Backward workspace of the serial block: dO, dZ, dh (fp32, shared by both
+// Backward workspace of the serial block: dO, dZ, dh (activation type, shared by both
 // LayerNorms), dx1, softmax row terms, LN row terms, LN partial column sums,
 // column-sum scratch, then the optional split region.
 struct SerialBwdLayout {
