@@ -570,33 +570,19 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
 // 0 .. n_full - 1); the remaining tail * splits workgroups each compute one
 // K-slice of one of the last `tail` tiles and store its fp32 partial tile
 // (256 x 256, row-major) to part, for splitk_reduce.
+// One work item of the DMA GEMM: K-tiles [kt0, kt1) of output tile lid
+// (slice >= 0: one K-slice of tail tile lid, whose fp32 partial tile goes to
+// part for splitk_reduce).
 template <bool AK, bool BK, Epi EPI, bool GT>
-__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* __restrict__ A,
-                                                                    int lda,
-                                                                    const bf16* __restrict__ B,
-                                                                    int ldb, int M, int N, int K,
-                                                                    EpiArgs ep, int n_full,
-                                                                    int splits,
-                                                                    float* __restrict__ part) {
+PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb,
+                          int M, int N, const EpiArgs& ep, int lid, int slice, int kt0, int kt1,
+                          int n_full, int splits, float* __restrict__ part) {
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
   auto a_off = [&](int s) { return (2 * s) * kDTile; };
   auto b_off = [&](int s) { return (2 * s + 1) * kDTile; };
 
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
-  const int nk_all = K / kBK;  // slices are planned in units of 64
-  int lid, slice = -1, kt0 = 0, kt1 = nk_all;
-  if ((int)blockIdx.x < n_full) {
-    lid = xcd_remap(blockIdx.x, n_full);
-  } else {
-    const int tail = tiles_m * tiles_n - n_full;
-    const int j = xcd_remap(blockIdx.x - n_full, tail * splits);
-    lid = n_full + j / splits;
-    slice = j % splits;
-    const int chunk = (nk_all + splits - 1) / splits;
-    kt0 = min(nk_all, slice * chunk);
-    kt1 = min(nk_all, kt0 + chunk);
-  }
   int tm, tn;
   tile_of(lid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
@@ -719,6 +705,58 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* 
   } else {
     wave_epilogue_lds<EPI, GT>(ep, nullptr, acc, m0 + wm, n0 + wn, M, N, fr, fh, lane, buf);
   }
+}
+
+template <bool AK, bool BK, Epi EPI, bool GT>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_kernel(const bf16* __restrict__ A,
+                                                                    int lda,
+                                                                    const bf16* __restrict__ B,
+                                                                    int ldb, int M, int N, int K,
+                                                                    EpiArgs ep, int n_full,
+                                                                    int splits,
+                                                                    float* __restrict__ part) {
+  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+  const int nk_all = K / kBK;  // slices are planned in units of 64
+  int lid, slice = -1, kt0 = 0, kt1 = nk_all;
+  if ((int)blockIdx.x < n_full) {
+    lid = xcd_remap(blockIdx.x, n_full);
+  } else {
+    const int tail = tiles_m * tiles_n - n_full;
+    const int j = xcd_remap(blockIdx.x - n_full, tail * splits);
+    lid = n_full + j / splits;
+    slice = j % splits;
+    const int chunk = (nk_all + splits - 1) / splits;
+    kt0 = min(nk_all, slice * chunk);
+    kt1 = min(nk_all, kt0 + chunk);
+  }
+  dma_gemm_item<AK, BK, EPI, GT>(A, lda, B, ldb, M, N, ep, lid, slice, kt0, kt1, n_full, splits,
+                                 part);
+}
+
+// Two independent GEMMs in one launch, neither split: workgroups 0 ..
+// tiles1 - 1 compute the first one's tiles, the rest the second one's.  With
+// the longer-K GEMM first, the second one's short tiles fill the CUs the
+// first leaves idle (a partial last round) and its own partial last round is
+// shared with nothing else; run apart, each GEMM pays its own.
+struct DmaGemm {
+  const bf16* A;
+  int lda;
+  const bf16* B;
+  int ldb;
+  int M, N, K;
+  EpiArgs ep;
+};
+template <bool AK1, bool BK1, Epi E1, bool AK2, bool BK2, Epi E2, bool GT>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_pair(DmaGemm g1, int tiles1,
+                                                                  DmaGemm g2, int tiles2) {
+  const int b = (int)blockIdx.x;
+  if (b < tiles1)
+    dma_gemm_item<AK1, BK1, E1, GT>(g1.A, g1.lda, g1.B, g1.ldb, g1.M, g1.N, g1.ep,
+                                    xcd_remap(b, tiles1), -1, 0, g1.K / kBK, tiles1, 1, nullptr);
+  else
+    dma_gemm_item<AK2, BK2, E2, GT>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep,
+                                    xcd_remap(b - tiles1, tiles2), -1, 0, g2.K / kBK, tiles2, 1,
+                                    nullptr);
 }
 
 // Sum of the K-slice partials of each tail tile, in slice order (so the
@@ -895,6 +933,41 @@ SplitPlan gemm_split_plan(Dt dt, int M, int N, int K) {
 
 size_t gemm_split_floats(const SplitPlan& p) {
   return (size_t)p.tail * p.splits * kBM * kBN;
+}
+
+bool gemm_pair_supported(Dt dt, const GemmSpec& g1, const GemmSpec& g2) {
+  if (dt != Dt::BF16) return false;
+  for (const GemmSpec* g : {&g1, &g2})
+    if (g->M <= 0 || g->N <= 0 || g->K <= 0 || g->K % kBK ||
+        !dma_offsets_fit(g->a_kcontig, g->lda, g->b_kcontig, g->ldb))
+      return false;
+  // the pairs of the block's backward pass: dC or dh (A K-contiguous, B
+  // MN-contiguous) first, a weight gradient (both MN-contiguous, fp32) second
+  return g1.a_kcontig && !g1.b_kcontig && (g1.epi == Epi::DgeluSplit || g1.epi == Epi::LnGrad) &&
+         !g2.a_kcontig && !g2.b_kcontig && g2.epi == Epi::StoreF32;
+}
+
+bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, hipStream_t s) {
+  if (!gemm_pair_supported(dt, g1, g2)) return false;
+  auto desc = [](const GemmSpec& g) {
+    return DmaGemm{(const bf16*)g.A, g.lda, (const bf16*)g.B, g.ldb, g.M, g.N, g.K, g.ep};
+  };
+  auto tiles = [](const GemmSpec& g) {
+    return ((g.M + kBM - 1) / kBM) * ((g.N + kBN - 1) / kBN);
+  };
+  const DmaGemm d1 = desc(g1), d2 = desc(g2);
+  const int t1 = tiles(g1), t2 = tiles(g2);
+  const size_t lds = 4 * (size_t)kTileBytes;
+  if (g1.epi == Epi::LnGrad)
+    gemm_bf16_dma_pair<true, false, Epi::LnGrad, false, false, Epi::StoreF32, true>
+        <<<t1 + t2, kThreads, lds, s>>>(d1, t1, d2, t2);
+  else if (g1.ep.gelu_tanh)
+    gemm_bf16_dma_pair<true, false, Epi::DgeluSplit, false, false, Epi::StoreF32, true>
+        <<<t1 + t2, kThreads, lds, s>>>(d1, t1, d2, t2);
+  else
+    gemm_bf16_dma_pair<true, false, Epi::DgeluSplit, false, false, Epi::StoreF32, false>
+        <<<t1 + t2, kThreads, lds, s>>>(d1, t1, d2, t2);
+  return true;
 }
 
 void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,

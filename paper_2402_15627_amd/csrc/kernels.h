@@ -134,6 +134,27 @@ void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, 
                  const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, float* split_ws,
                  size_t split_ws_floats, hipStream_t s);
 
+// Two independent GEMMs in one launch, neither split along K: the first
+// one's tiles are started first (give it the longer K), and the second one's
+// tiles fill the CUs the first leaves idle.  Supported: bf16, K multiples of
+// 64 and operands the LDS-DMA path takes, with the first GEMM A K-contiguous,
+// B MN-contiguous and a DgeluSplit or LnGrad epilogue, the second both
+// MN-contiguous with StoreF32 (the backward pass's dC + dW_out and
+// dh + dW_in).  launch_gemm_pair launches nothing and returns false for any
+// other pair.
+struct GemmSpec {
+  Epi epi;
+  bool a_kcontig, b_kcontig;
+  const void* A;
+  int lda;
+  const void* B;
+  int ldb;
+  int M, N, K;
+  EpiArgs ep;
+};
+bool gemm_pair_supported(Dt dt, const GemmSpec& g1, const GemmSpec& g2);
+bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, hipStream_t s);
+
 // -------------------------------------------------------------- attention
 // Causal sliding-window attention over [batch, seq] rows; q/k/v/o/do/dq/dk/dv
 // element (b, t, head, e) at ptr[(b * seq + t) * ld + head * head_dim + e].

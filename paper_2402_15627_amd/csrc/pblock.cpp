@@ -481,10 +481,18 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   (void)b_in;
   (void)b_out;
 
-  // Order: the chain dC -> attention -> dh -> LayerNorm runs first, each step
-  // reading what the previous one just wrote while it is still in the
-  // last-level cache; the two weight-gradient GEMMs, which write ~4 bytes
-  // per weight, come last so their write-back does not compete with it.
+  // Order: the chain dC -> attention -> dh -> LayerNorm, each step reading
+  // what the previous one just wrote.  Where the two weight-gradient GEMMs can
+  // share a launch with the GEMM before them (dW_out with dC, dW_in with dh:
+  // see launch_gemm_pair), they do, and their short tiles fill the CUs the
+  // long-K tiles leave idle; otherwise they come last, so their write-back
+  // does not compete with the chain.
+  pb::EpiArgs e2;  // B2: dW_out = dy^T C (contraction over tokens)
+  e2.out = dw_out;
+  e2.ld_out = K_out;
+  pb::EpiArgs e5;  // B5: dW_in = dZ^T h
+  e5.out = dw_in;
+  e5.ld_out = H;
 
   // B1: dC = dy W_out; dO = dC[:, :A]; dU = dC[:, A:] * gelu'(U) -> dZ[:, 3A:]
   pb::EpiArgs e1;
@@ -496,10 +504,16 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   e1.split = A;
   e1.col2 = 3 * A;
   e1.gelu_tanh = cfg->gelu_tanh;
+  const pb::GemmSpec g_dc{pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1};
+  const pb::GemmSpec g_dwo{pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2};
+  const bool pair_out = pb::gemm_pair_supported(dt, g_dc, g_dwo);
   {
-    StepScope sc(PB_STEP_DC, stream);
-    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
-                    split_ws, split_f, stream);
+    StepScope sc(PB_STEP_DC, stream);  // with dW_out when they share a launch
+    if (pair_out)
+      pb::launch_gemm_pair(dt, g_dc, g_dwo, stream);
+    else
+      pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
+                      split_ws, split_f, stream);
   }
   // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
   {
@@ -520,10 +534,16 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   e4.rstd = rstd;
   e4.rowpart = rowpart;
   e4.rowpart_ld = pb::ln_row_groups(H);
+  const pb::GemmSpec g_dh{pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e4};
+  const pb::GemmSpec g_dwi{pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5};
+  const bool pair_in = pb::gemm_pair_supported(dt, g_dh, g_dwi);
   {
-    StepScope sc(PB_STEP_DH, stream);
-    pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
-                    split_ws, split_f, stream);
+    StepScope sc(PB_STEP_DH, stream);  // with dW_in when they share a launch
+    if (pair_in)
+      pb::launch_gemm_pair(dt, g_dh, g_dwi, stream);
+    else
+      pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
+                      split_ws, split_f, stream);
   }
   // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
   {
@@ -543,23 +563,17 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
     StepScope sc(PB_STEP_DB_IN, stream);
     pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
   }
-  // B2: dW_out = dy^T C (contraction over tokens)
-  pb::EpiArgs e2;
-  e2.out = dw_out;
-  e2.ld_out = K_out;
   {
-    StepScope sc(PB_STEP_DW_OUT, stream);
-    pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
-                    split_ws, split_f, stream);
+    StepScope sc(PB_STEP_DW_OUT, stream);  // empty when it shared dC's launch
+    if (!pair_out)
+      pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
+                      split_ws, split_f, stream);
   }
-  // B5: dW_in = dZ^T h
-  pb::EpiArgs e5;
-  e5.out = dw_in;
-  e5.ld_out = H;
   {
-    StepScope sc(PB_STEP_DW_IN, stream);
-    pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5,
-                    split_ws, split_f, stream);
+    StepScope sc(PB_STEP_DW_IN, stream);  // empty when it shared dh's launch
+    if (!pair_in)
+      pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5,
+                      split_ws, split_f, stream);
   }
   return finish_launches();
 }
