@@ -63,8 +63,39 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "parallel-block fwd+bwd TFLOP/s and % of MI355X bf16 MFMA peak"
 
 
+# GEMM steps of the backward pass that share one launch (the library's
+# launch_gemm_pair): dC with dW_out, dh with dW_in.
+GEMM_PAIRS = {"dc": "dw_out", "dh": "dw_in"}
+
+
+def paired_steps(s, block="parallel"):
+    """The pairs of GEMM_PAIRS the library launches together for this
+    workload, as gemm_pair_supported decides: bf16, every K a multiple of 64
+    (the operand offsets of the LDS-DMA path fit 32 bits at these sizes)."""
+    if block != "parallel" or s.dtype != "bf16":
+        return {}
+    steps = gemm_steps(s)
+    return {a: b for a, b in GEMM_PAIRS.items() if steps[a][2] % 64 == 0 and steps[b][2] % 64 == 0}
+
+
+def launch_key(step, s):
+    """The launch a step's time is measured on: "dh+dw_in" for a pair."""
+    pairs = paired_steps(s)
+    return f"{step}+{pairs[step]}" if step in pairs else step
+
+
 def step_work(s):
-    """Algorithmic work of each pb_step: ("mfma", FLOPs) or ("hbm", bytes)."""
+    """Algorithmic work of each pb_step: ("mfma", FLOPs) or ("hbm", bytes).
+    A GEMM that shares its partner's launch counts there (its own step is
+    empty)."""
+    work = _step_work(s)
+    for a, b in paired_steps(s).items():
+        work[a] = ("mfma", work[a][1] + work[b][1])
+        work[b] = ("mfma", 0)
+    return work
+
+
+def _step_work(s):
     from paper_2402_15627_amd.inputs import visible_pairs
     T, H, A, F = s.tokens, s.hidden, s.attn_width, s.ffn
     n_in, k_out = s.n_in, s.k_out
@@ -99,7 +130,8 @@ KERNEL_SOURCES = {
 }
 STEP_SOURCE = {"in_proj": "gemm", "out_proj": "gemm", "dc": "gemm", "dw_out": "gemm", "dh": "gemm",
                "dw_in": "gemm", "attn_fwd": "attn", "attn_bwd": "attn", "ln_fwd": "ln",
-               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln", "lamb": "lamb"}
+               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln", "lamb": "lamb",
+               "dc+dw_out": "gemm", "dh+dw_in": "gemm"}
 COPY_BYTES = 1 << 30  # read and written once by the calibration copy
 
 
@@ -151,7 +183,13 @@ def demangle(name):
 def gemm_step_of(name, grid, s, block="parallel"):
     """Block step(s) a GEMM launch belongs to ("" if none; "a/b" when two
     steps launch the same kernel on the same grid)."""
-    hits = [st for st, mnk in gemm_steps(s, block).items()
+    steps = gemm_steps(s, block)
+    if "gemm_bf16_dma_pair" in name:
+        tiles = lambda st: -(-steps[st][0] // 256) * -(-steps[st][1] // 256)  # noqa: E731
+        hits = [f"{a}+{b}" for a, b in paired_steps(s, block).items()
+                if GEMM_SIGNATURE[a] in name and (tiles(a) + tiles(b)) * 512 == grid]
+        return "/".join(hits)
+    hits = [st for st, mnk in steps.items()
             if "gemm_bf16" in name and GEMM_SIGNATURE[st] in name
             and gemm_grid_threads(*mnk) == grid]
     return "/".join(hits)
@@ -190,7 +228,7 @@ def gemm_grid_threads(M, N, K):
 
 
 def traffic_path(step, workload):
-    return os.path.join(ROOT, "profiles", f"{step}_{workload}_traffic.md")
+    return os.path.join(ROOT, "profiles", f"{step.replace('+', '_')}_{workload}_traffic.md")
 
 
 def _counter_rows(d):
@@ -217,9 +255,14 @@ def traffic_summary(dirs, workload, step):
     by what the same counters read for the calibration copy of COPY_BYTES."""
     from paper_2402_15627_amd.inputs import WORKLOADS
     s = WORKLOADS[workload]
-    if step not in gemm_steps(s):
-        raise SystemExit(f"traffic summary supports the GEMM steps, not {step}")
-    grid = gemm_grid_threads(*gemm_steps(s)[step])
+    parts = step.split("+")
+    if any(p not in gemm_steps(s) for p in parts):
+        raise SystemExit(f"traffic summary supports the GEMM steps and pairs, not {step}")
+    if len(parts) == 2:
+        tiles = lambda st: -(-gemm_steps(s)[st][0] // 256) * -(-gemm_steps(s)[st][1] // 256)  # noqa: E731
+        grid = (tiles(parts[0]) + tiles(parts[1])) * 512
+    else:
+        grid = gemm_grid_threads(*gemm_steps(s)[step])
     pick = lambda r: gemm_step_of(r["Kernel_Name"], int(r["Grid_Size"]), s) == step  # noqa: E731
     copy_pick = lambda r: "neg_kernel" in r["Kernel_Name"]  # noqa: E731
     fetch, n1 = _per_dispatch(_counter_rows(dirs[0]), "FETCH_SIZE", pick)
@@ -227,9 +270,11 @@ def traffic_summary(dirs, workload, step):
     cfetch, _ = _per_dispatch(_counter_rows(dirs[2]), "FETCH_SIZE", copy_pick)
     cwrite, _ = _per_dispatch(_counter_rows(dirs[3]), "WRITE_SIZE", copy_pick)
     ff, wf = COPY_BYTES / 1024 / cfetch, COPY_BYTES / 1024 / cwrite
-    M, N, K = gemm_steps(s)[step]
     e = 2 if s.dtype == "bf16" else 4
-    out_bytes = 4 if step in ("dw_in", "dw_out", "dh") else e
+
+    def algorithmic(st):  # operands read once, the output written once
+        M, N, K = gemm_steps(s)[st]
+        return (M * K + N * K) * e + M * N * (4 if st in ("dw_in", "dw_out") else e)
     rec = {
         "step": step, "workload": workload, "grid_threads": grid, "dispatches": [n1, n2],
         "fetch_kib": round(fetch, 1), "write_kib": round(write, 1),
@@ -237,7 +282,7 @@ def traffic_summary(dirs, workload, step):
         "copy_write_kib": round(cwrite, 1), "fetch_scale": round(ff, 4),
         "write_scale": round(wf, 4),
         "traffic_bytes": int(fetch * 1024 * ff + write * 1024 * wf),
-        "algorithmic_bytes": (M * K + N * K) * e + M * N * out_bytes,
+        "algorithmic_bytes": sum(algorithmic(p) for p in parts),
         "source_fingerprint": source_fingerprint(step),
     }
     return rec
@@ -652,7 +697,7 @@ def main():
     ap.add_argument("--traffic-summary", nargs=4, metavar="DIR",
                     help="rocprofv3 --pmc output dirs: FETCH_SIZE and WRITE_SIZE of the bench, "
                          "then of --copy-calibration; writes profiles/<step>_<workload>_traffic.md")
-    ap.add_argument("--traffic-step", default="dw_in",
+    ap.add_argument("--traffic-step", default="dh+dw_in",
                     help="a GEMM step, or lamb (the LAMB step's two streaming kernels)")
     ap.add_argument("--trace-summary", metavar="DIR",
                     help="print a markdown table of a rocprofv3 --kernel-trace output dir")
@@ -753,6 +798,11 @@ def main():
                for j, n in enumerate(names)}
     dominant = max(step_ms, key=step_ms.get)
     dj = names.index(dominant)
+    # a GEMM the library folded into its partner's launch must take no time
+    for a, b in paired_steps(shape).items():
+        if step_ms[b] > 0.05 * step_ms[a]:
+            raise SystemExit(f"step {b} took {step_ms[b]:.3f} ms: not launched with {a} as "
+                             "paired_steps assumes")
 
     # Pass 2 (the timed region): K steps; events only around the dominant kernel.
     db = [new_event() for _ in range(K)]
@@ -791,8 +841,9 @@ def main():
         achieved = amount / (dom_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": read_traffic(dominant, shape.name), "kernel": dominant,
-                "flops_per_launch": amount, "avg_ms": round(dom_ms, 4)}
+                "traffic": read_traffic(launch_key(dominant, shape), shape.name),
+                "kernel": launch_key(dominant, shape), "flops_per_launch": amount,
+                "avg_ms": round(dom_ms, 4)}
     else:
         achieved = amount / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,

@@ -61,7 +61,7 @@ def test_traffic_is_reported_only_for_unchanged_sources(tmp_path, monkeypatch):
 
 
 def test_committed_traffic_profile_parses():
-    p = bench.traffic_path("dw_in", "175b_tp8_share")
+    p = bench.traffic_path("dh+dw_in", "175b_tp8_share")
     if not os.path.exists(p):
         pytest.skip("no traffic profile committed")
     text = open(p).read()
@@ -86,3 +86,28 @@ def test_serial_gemm_steps_are_labelled():
     assert "dw_down/dw_up" in labels
     # 48 tiles of the dO GEMM, K = 12288: 5 slices each
     assert bench.split_plan(*steps["d_o"]) == (0, 48, 5)
+
+
+def test_paired_gemm_launches_are_labelled_and_counted():
+    """The backward's dC + dW_out and dh + dW_in share one launch each: the
+    pair kernel is found by its first GEMM's template and the two tile
+    counts, and the pair's step carries both GEMMs' FLOPs."""
+    s = WORKLOADS["175b_tp8_share"]
+    assert bench.paired_steps(s) == {"dc": "dw_out", "dh": "dw_in"}
+    assert bench.paired_steps(s, "serial") == {}
+    assert bench.paired_steps(WORKLOADS["tiny_f32"]) == {}
+    name = ("void pb::(anonymous namespace)::gemm_bf16_dma_pair<true, false, (pb::Epi)4, "
+            "false, false, (pb::Epi)0, true>()")
+    # dh: 8 x 48 tiles, dW_in: 42 x 48 tiles, unsplit
+    assert bench.gemm_step_of(name, (384 + 2016) * 512, s) == "dh+dw_in"
+    assert bench.gemm_step_of(name, 384 * 512, s) == ""
+    dc = name.replace("(pb::Epi)4", "(pb::Epi)3")
+    # dC: 8 x 30 tiles, dW_out: 48 x 30 tiles
+    assert bench.gemm_step_of(dc, (240 + 1440) * 512, s) == "dc+dw_out"
+    work, plain = bench.step_work(s), bench._step_work(s)
+    assert work["dh"][1] == plain["dh"][1] + plain["dw_in"][1] and work["dw_in"][1] == 0
+    assert work["dc"][1] == plain["dc"][1] + plain["dw_out"][1] and work["dw_out"][1] == 0
+    assert sum(v for k, v in work.values() if k == "mfma") == \
+        sum(v for k, v in plain.values() if k == "mfma")
+    assert bench.launch_key("dh", s) == "dh+dw_in" and bench.launch_key("in_proj", s) == "in_proj"
+    assert bench.traffic_path("dh+dw_in", "w").endswith("dh_dw_in_w_traffic.md")
