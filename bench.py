@@ -64,18 +64,21 @@ METRIC = "parallel-block fwd+bwd TFLOP/s and % of MI355X bf16 MFMA peak"
 
 
 # GEMM steps of the backward pass that share one launch (the library's
-# launch_gemm_pair): dC with dW_out, dh with dW_in.
+# launch_gemm_pair): dC with dW_out, dh with dW_in; in the serial block each
+# weight gradient with the GEMM before it.
 GEMM_PAIRS = {"dc": "dw_out", "dh": "dw_in"}
+SERIAL_GEMM_PAIRS = {"dg": "dw_down", "dh2": "dw_up", "d_o": "dw_o", "dh1": "dw_qkv"}
 
 
 def paired_steps(s, block="parallel"):
     """The pairs of GEMM_PAIRS the library launches together for this
     workload, as gemm_pair_supported decides: bf16, every K a multiple of 64
     (the operand offsets of the LDS-DMA path fit 32 bits at these sizes)."""
-    if block != "parallel" or s.dtype != "bf16":
+    if s.dtype != "bf16":
         return {}
-    steps = gemm_steps(s)
-    return {a: b for a, b in GEMM_PAIRS.items() if steps[a][2] % 64 == 0 and steps[b][2] % 64 == 0}
+    steps = gemm_steps(s, block)
+    pairs = GEMM_PAIRS if block == "parallel" else SERIAL_GEMM_PAIRS
+    return {a: b for a, b in pairs.items() if steps[a][2] % 64 == 0 and steps[b][2] % 64 == 0}
 
 
 def launch_key(step, s):

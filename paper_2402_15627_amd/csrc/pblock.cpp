@@ -848,6 +848,36 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   (void)b_o;
   (void)b_down;
 
+  // Each weight gradient (a token contraction, fp32) shares one launch with
+  // the GEMM before it where launch_gemm_pair takes the pair, so its short
+  // tiles fill the CUs the other leaves idle; any other runs at the end.
+  pb::EpiArgs wd, wo, wu, wq;
+  wd.out = at(dw_out, A, 4);  // dW_down = dy^T G
+  wd.ld_out = K_out;
+  wo.out = dw_out;  // dW_o = dx1^T O
+  wo.ld_out = K_out;
+  wu.out = at(dw_in, 3LL * A * H, 4);  // dW_up = dU^T h2
+  wu.ld_out = H;
+  wq.out = dw_in;  // dW_qkv = dQKV^T h1
+  wq.ld_out = H;
+  const pb::GemmSpec g_wd{pb::Epi::StoreF32, false, false, dy, H, at(c, A, e), K_out, H, F, T, wd};
+  const pb::GemmSpec g_wo{pb::Epi::StoreF32, false, false, dx1, H, c, K_out, H, A, T, wo};
+  const pb::GemmSpec g_wu{pb::Epi::StoreF32, false, false, at(dz, 3LL * A, e), N_in, h2, H, F, H,
+                          T, wu};
+  const pb::GemmSpec g_wq{pb::Epi::StoreF32, false, false, dz, N_in, h1, H, 3 * A, H, T, wq};
+  auto run = [&](const pb::GemmSpec& g) {
+    pb::launch_gemm(dt, g.epi, g.a_kcontig, g.b_kcontig, g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K,
+                    g.ep, split_ws, split_f, stream);
+  };
+  const pb::GemmSpec* deferred[4];
+  int n_deferred = 0;
+  auto run_with = [&](const pb::GemmSpec& g, const pb::GemmSpec& wg) {
+    if (!pb::launch_gemm_pair(dt, g, wg, stream)) {
+      run(g);
+      deferred[n_deferred++] = &wg;
+    }
+  };
+
   // MLP: dG = dy W_down, dU = dG * gelu'(U) -> dZ[:, 3A:]
   pb::EpiArgs e1;
   e1.out = dz;
@@ -858,8 +888,9 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   e1.split = 0;
   e1.col2 = 3 * A;
   e1.gelu_tanh = cfg->gelu_tanh;
-  pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, at(w_out, A, e), K_out, T, F, H,
-                  e1, split_ws, split_f, stream);
+  run_with(pb::GemmSpec{pb::Epi::DgeluSplit, true, false, dy, H, at(w_out, A, e), K_out, T, F, H,
+                        e1},
+           g_wd);
   // dh2 = dU W_up, with LN2's row terms
   pb::EpiArgs e2;
   e2.out = dh;
@@ -870,8 +901,9 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   e2.rstd = rstd2;
   e2.rowpart = rowpart;
   e2.rowpart_ld = pb::ln_row_groups(H);
-  pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, at(dz, 3LL * A, e), N_in,
-                  at(w_in, 3LL * A * H, e), H, T, H, F, e2, split_ws, split_f, stream);
+  run_with(pb::GemmSpec{pb::Epi::LnGrad, true, false, at(dz, 3LL * A, e), N_in,
+                        at(w_in, 3LL * A * H, e), H, T, H, F, e2},
+           g_wu);
   // dx1 = dy + LN2'(dh2); dgamma2, dbeta2, and db_down = sum dy
   pb::launch_ln_backward(dt, x1, mean2, rstd2, ln2_gamma, dh, rowpart, dy, dx1, pdg, pdb, pdy, T,
                          H, stream);
@@ -882,8 +914,8 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   e3.ld_out = A;
   e3.split = A;  // every column is dO
   e3.gelu_tanh = cfg->gelu_tanh;
-  pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dx1, H, w_out, K_out, T, A, H, e3,
-                  split_ws, split_f, stream);
+  run_with(pb::GemmSpec{pb::Epi::DgeluSplit, true, false, dx1, H, w_out, K_out, T, A, H, e3},
+           g_wo);
   pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
                            d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in,
                            split_ws, split_f * 4, stream);
@@ -897,30 +929,15 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   e4.rstd = rstd1;
   e4.rowpart = rowpart;
   e4.rowpart_ld = pb::ln_row_groups(H);
-  pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, 3 * A, e4, split_ws,
-                  split_f, stream);
+  run_with(pb::GemmSpec{pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, 3 * A, e4}, g_wq);
   // dx = dx1 + LN1'(dh1); dgamma1, dbeta1, and db_o = sum dx1
   pb::launch_ln_backward(dt, x, mean1, rstd1, ln1_gamma, dh, rowpart, dx1, dx, pdg, pdb, pdy, T,
                          H, stream);
   pb::launch_colsum3_f32(pdg, pdb, pdy, H, nblk, H, dln1_gamma, dln1_beta, db_o, stream);
   // bias gradients of the input projections: db_in = sum over tokens of dZ
   pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
-  // weight gradients (token contractions), last
-  pb::EpiArgs w;
-  w.ld_out = K_out;
-  w.out = at(dw_out, A, 4);  // dW_down = dy^T G
-  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, at(c, A, e), K_out, H, F, T, w,
-                  split_ws, split_f, stream);
-  w.out = dw_out;  // dW_o = dx1^T O
-  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dx1, H, c, K_out, H, A, T, w, split_ws,
-                  split_f, stream);
-  w.ld_out = H;
-  w.out = at(dw_in, 3LL * A * H, 4);  // dW_up = dU^T h2
-  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, at(dz, 3LL * A, e), N_in, h2, H, F, H, T,
-                  w, split_ws, split_f, stream);
-  w.out = dw_in;  // dW_qkv = dQKV^T h1
-  pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h1, H, 3 * A, H, T, w, split_ws,
-                  split_f, stream);
+  // weight gradients that did not share a launch, last
+  for (int i = 0; i < n_deferred; ++i) run(*deferred[i]);
   return finish_launches();
 }
 

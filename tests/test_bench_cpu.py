@@ -84,6 +84,10 @@ def test_serial_gemm_steps_are_labelled():
         assert st in lab.split("/"), (st, lab)
         labels.add(lab)
     assert "dw_down/dw_up" in labels
+    # paired launches of the serial backward: dG + dW_down, 8 x 24 + 48 x 24 tiles
+    pair = ("void pb::(anonymous namespace)::gemm_bf16_dma_pair<true, false, (pb::Epi)3, "
+            "false, false, (pb::Epi)0, true>()")
+    assert bench.gemm_step_of(pair, (192 + 1152) * 512, s, "serial") == "dg+dw_down"
     # 48 tiles of the dO GEMM, K = 12288: 5 slices each
     assert bench.split_plan(*steps["d_o"]) == (0, 48, 5)
 
@@ -94,7 +98,7 @@ def test_paired_gemm_launches_are_labelled_and_counted():
     counts, and the pair's step carries both GEMMs' FLOPs."""
     s = WORKLOADS["175b_tp8_share"]
     assert bench.paired_steps(s) == {"dc": "dw_out", "dh": "dw_in"}
-    assert bench.paired_steps(s, "serial") == {}
+    assert bench.paired_steps(s, "serial") == bench.SERIAL_GEMM_PAIRS
     assert bench.paired_steps(WORKLOADS["tiny_f32"]) == {}
     name = ("void pb::(anonymous namespace)::gemm_bf16_dma_pair<true, false, (pb::Epi)4, "
             "false, false, (pb::Epi)0, true>()")
