@@ -24,6 +24,7 @@
 //
 // fp32 path: a plain LDS-tiled SIMT kernel with the same epilogues.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -331,20 +332,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const bf16* __re
 // straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
 // LDS base + 16 * lane), so there is no register staging and no LDS write
 // instruction.  K-tiles of 64 (a K-contiguous row then spans whole 128-byte
-// lines) through two LDS stages (2 x 64 KB).  Each wave keeps the MFMA
-// fragments of four k-steps in registers and reads them two k-steps ahead,
-// so a tile's last reads are issued before its second k-step's MFMAs; the one
-// workgroup barrier of the K-tile sits there.  After it the tile's stage is
-// free for the loads of tile t + 2 and tile t + 1 is visible, whose first
-// fragments are read while k-steps 2 and 3 multiply: the matrix pipe keeps
-// running through the barrier and the loads have a whole tile to land.
+// lines) through two LDS stages (2 x 64 KB).
+//
+// The main loop runs on v_mfma_f32_16x16x32_bf16: on random bf16 operands
+// the chip holds ~2.0 GHz issuing it back to back, against ~1.65 GHz for
+// v_mfma_f32_32x32x16_bf16 at the same FLOP rate per clock (a power limit,
+// measured with MFMA-only loops), so the same schedule gets ~20% more clock.
+// A wave's 64 x 128 block is 4 x 8 MFMA blocks of 16 x 16; a K-tile is two
+// k-steps of 32, and each k-step's MFMAs are issued in two phases (N blocks
+// 0-3, then 4-7).  Each wave keeps the fragments of both k-steps in registers
+// and reads them two phases ahead, so a tile's last reads are issued before
+// its second phase's MFMAs; the one workgroup barrier of the K-tile sits
+// there.  After it the tile's stage is free for the loads of tile t + 2 and
+// tile t + 1 is visible, whose first fragments are read while the second
+// k-step multiplies: the matrix pipe keeps running through the barrier and
+// the loads have a whole tile to land.
 //
 // A K-contiguous operand is stored K-major (128-byte rows, the 16-byte chunk
 // index XOR-swizzled by the row); an MN-contiguous operand is stored MN-major,
-// 64 k-rows of 512 bytes with the chunk index XOR-ed by 4 (k mod 4), and its
-// MFMA fragments are read with ds_read_b64_tr_b16, which transposes 4 (k) x
-// 16 (mn) blocks across a 16-lane group.  Both patterns are free of bank
-// conflicts.  The DMA instructions are issued from inline assembly as scalar
+// 64 k-rows of 512 bytes with the chunk index XOR-ed by 4 (k mod 4) and by
+// 2 (k / 8 mod 2), and its MFMA fragments are read with ds_read_b64_tr_b16,
+// which transposes 4 (k) x 16 (mn) blocks across a 16-lane group (the four
+// groups of a wave read k-rows 8 apart).  Both patterns are free of bank
+// conflicts (64 banks).  The DMA instructions are issued from inline assembly as scalar
 // base + per-lane offset (no per-load address arithmetic) and waited for
 // explicitly, so the compiler adds no conservative waits between them and the
 // LDS reads of the other stage.
@@ -359,7 +369,13 @@ constexpr int kDmaPerStage = 2 * kPieces;   // DMA instructions per wave per sta
 static_assert(kBM == kBN && kPieces * 1024 * (kThreads / 64) == kDTile, "tile split over waves");
 static_assert(kDK == kBK, "the DMA path's K-tile is the planning unit");
 
-PB_DEV int swz_mn(int krow, int c) { return c ^ (4 * (krow & 3)); }
+// Materialise a wave-uniform value in scalar registers at this point.
+template <typename T>
+PB_DEV void pin_sgpr(T v) {
+  asm volatile("" ::"s"(v));
+}
+
+PB_DEV int swz_mn(int krow, int c) { return c ^ (4 * (krow & 3)) ^ (2 * ((krow >> 3) & 1)); }
 
 PB_DEV void dma16s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
@@ -368,7 +384,15 @@ PB_DEV void dma16s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
 }
 template <int N>
 PB_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
-PB_DEV void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// The wait for LDS (and scalar) loads is the compiler's own instruction
+// (lgkmcnt(0), vmcnt and expcnt left open), so its wait bookkeeping knows
+// that nothing counted by lgkmcnt is outstanding past the barrier; hidden
+// inside the asm, a kernel-argument load issued earlier would look pending
+// and force a full wait at the main loop's head.
+PB_DEV void block_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  asm volatile("s_barrier" ::: "memory");
+}
 
 // Byte offset, from the operand tile's base (its first row, or first column,
 // at the tile's k), of this lane's 16 bytes in DMA piece i of this wave.
@@ -412,6 +436,21 @@ PB_DEV bf16x8 dma_frag(const unsigned char* lds_tile, int row, int ks, int h, in
   }
 }
 
+// Fragment of v_mfma_f32_16x16x32_bf16 for the 16-row block at tile row
+// `base` (a multiple of 16), k-step s (32 k) of the K-tile: lane l supplies
+// row base + (l & 15) and its k values 32 s + 8 (l >> 4) .. + 7, i.e. the
+// 16-byte chunk 4 s + (l >> 4) of that row.
+template <bool KC>
+PB_DEV bf16x8 dma_frag16(const unsigned char* lds_tile, int base, int s, int lane) {
+  return dma_frag<KC>(lds_tile, base + (lane & 15), 2 * s + (lane >> 5), (lane >> 4) & 1, lane);
+}
+
+// A wave's 64 x 128 block as 16 x 16 MFMA blocks.  acc[i][j][e] is C(m, n)
+// with m = mw + 16 i + (lane & 15), n = nw + 16 j + 4 (lane >> 4) + e (the N
+// tile is the MFMA's "A" operand, so each lane holds four consecutive columns
+// of one row).
+constexpr int kTM16 = kWTM / 16, kTN16 = kWTN / 16;
+
 // The epilogue of a wave's 64 x 128 block of the tile, staged through the
 // wave's 16 KB of LDS so that every global access of the epilogue covers
 // whole lines.  Per 32-row half, the lanes write their accumulators row-major
@@ -431,8 +470,8 @@ constexpr int kEpiWaveLds = 32 * kWTN * 4;  // one half: 16 KB
 static_assert(kEpiWaveLds * kWavesM * kWavesN <= 4 * kTileBytes, "epilogue staging fits");
 template <Epi EPI, bool GT>
 PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
-                              const f32x16 (&acc)[kTM][kTN], int mw, int nw, int M, int N, int fr,
-                              int fh, int lane, unsigned char* buf) {
+                              const f32x4 (&acc)[kTM16][kTN16], int mw, int nw, int M, int N,
+                              int lane, unsigned char* buf) {
   const int c = lane & 31, hi = lane >> 5;
   const int n = nw + 4 * c;  // this lane's four columns, the same in every row
   const int ncl = min(n, N - 4);
@@ -442,15 +481,14 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
     if (!part_tile) load4<bf16>((const bf16*)ep.bias + ncl, b4);
   const bool dg_aux = EPI == Epi::DgeluSplit && ep.split < N;  // any GeLU' column at all
 #pragma unroll
-  for (int i = 0; i < kTM; ++i) {
+  for (int i = 0; i < kWTM / 32; ++i) {
+    // rows 16 ii + (lane & 15) of the half, 16-byte column chunk 4 j + (lane >> 4)
 #pragma unroll
-    for (int j = 0; j < kTN; ++j)
+    for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int cw = 8 * j + 2 * jj + fh;
-        *reinterpret_cast<f32x4*>(buf + fr * (kWTN * 4) + ((cw ^ fr) & 31) * 16) =
-            f32x4{acc[i][j][4 * jj], acc[i][j][4 * jj + 1], acc[i][j][4 * jj + 2],
-                  acc[i][j][4 * jj + 3]};
+      for (int j = 0; j < kTN16; ++j) {
+        const int rr = 16 * ii + (lane & 15), cw = 4 * j + (lane >> 4);
+        *reinterpret_cast<f32x4*>(buf + rr * (kWTN * 4) + ((cw ^ rr) & 31) * 16) = acc[2 * i + ii][j];
       }
     const int m0h = mw + 32 * i;  // first row of this half
     // Per-row inputs of the half, all issued before any result is stored (a
@@ -589,7 +627,6 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
-  const int fr = lane & 31, fh = lane >> 5;
 
   // K-tiles [kt0, kt1) of this work item
   const int nt = kt1 - kt0;
@@ -624,37 +661,50 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
     issue_half(t, 1);
   };
 
-  f32x16 acc[kTM][kTN];
+  f32x4 acc[kTM16][kTN16];
 #pragma unroll
-  for (int i = 0; i < kTM; ++i)
+  for (int i = 0; i < kTM16; ++i)
 #pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    for (int j = 0; j < kTN16; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  constexpr int kSteps = kDK / 16;  // k-steps per K-tile: 4
-  bf16x8 fa[kSteps][kTM], fb[kSteps][kTN];
-  auto read_frags = [&](int t, int ks) {
-    const int s = t % kStages;
-    const unsigned char* pa = smem + a_off(s);
-    const unsigned char* pb = smem + b_off(s);
+  // Phase p (0..7) of a K-tile: k-step s = p / 4 (32 k), N blocks 2 (p % 4)
+  // and 2 (p % 4) + 1, eight MFMAs.  Fragments are read kLook phases before
+  // the phase that first uses them: the A blocks of k-step s with the batch
+  // of phase 4 s, each pair of N blocks with its own phase's batch.  The
+  // reads of a K-tile's last phase are issued kLook phases before its end;
+  // the one workgroup barrier of the K-tile follows them, after which the
+  // tile's stage takes the loads of tile t + 2 (issued over the next two
+  // phases) while the next tile's first fragments are read.  With kLook = 2
+  // at most 14 fragments are live (56 registers beside the 128 of the
+  // accumulators) and a load has a whole K-tile to land.
+  constexpr int kPh = 8, kLook = 2;
+  static_assert(kLook >= 2 && kLook < kPh, "DMA halves are issued after the barrier");
+  bf16x8 fa[2][kTM16], fb[2][kTN16];
+  auto read_frags = [&](int t, int p) {
+    const int st = t % kStages, ks = p >> 2, r = p & 3;
+    const unsigned char* pa = smem + a_off(st);
+    const unsigned char* pb = smem + b_off(st);
+    if (r == 0) {
 #pragma unroll
-    for (int i = 0; i < kTM; ++i) fa[ks][i] = dma_frag<AK>(pa, wm + 32 * i + fr, ks, fh, lane);
+      for (int i = 0; i < kTM16; ++i) fa[ks][i] = dma_frag16<AK>(pa, wm + 16 * i, ks, lane);
+    }
 #pragma unroll
-    for (int j = 0; j < kTN; ++j) fb[ks][j] = dma_frag<BK>(pb, wn + 32 * j + fr, ks, fh, lane);
+    for (int j = 2 * r; j < 2 * r + 2; ++j) fb[ks][j] = dma_frag16<BK>(pb, wn + 16 * j, ks, lane);
   };
-  // LDS read instructions per k-step (a transposed fragment takes two)
-  constexpr int kReads = (AK ? kTM : 2 * kTM) + (BK ? kTN : 2 * kTN);
-  constexpr int kMfma = kTM * kTN;
-  auto mma = [&](int ks) {
+  auto mma = [&](auto P) {
+    constexpr int p = decltype(P)::value, ks = p >> 2, j0 = 2 * (p & 3);
 #pragma unroll
-    for (int i = 0; i < kTM; ++i)
+    for (int i = 0; i < kTM16; ++i)
 #pragma unroll
-      for (int j = 0; j < kTN; ++j)
+      for (int j = j0; j < j0 + 2; ++j)
         acc[i][j] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
-    // alternate one MFMA and one LDS read (fragments two k-steps ahead) so
-    // the reads are in flight early and the matrix pipe stays fed
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+    // alternate one MFMA and one LDS read (the batch of phase p + kLook; a
+    // transposed fragment takes two reads) so the reads are in flight early
+    // and the matrix pipe stays fed
+    constexpr int pn = (p + kLook) % kPh;
+    constexpr int kReads = ((pn & 3) == 0 ? (AK ? 1 : 2) * kTM16 : 0) + (BK ? 1 : 2) * 2;
+    constexpr int kMfma = kTM16 * 2;
     constexpr int pairs = kReads < kMfma ? kReads : kMfma;
 #pragma unroll
     for (int u = 0; u < pairs; ++u) {
@@ -664,36 +714,57 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
     if constexpr (kMfma > pairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - pairs, 0);
     if constexpr (kReads > pairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - pairs, 0);
   };
+  auto phase = [&](int t, auto P) {
+    constexpr int p = decltype(P)::value;
+    if constexpr (p == kPh - kLook) {
+      // Every wave has issued (and with the barrier, finished) its reads of
+      // tile t, so its stage can take tile t + 2; tile t + 1 has landed for
+      // this wave, and after the barrier for all.
+      wait_dma<0>();
+      block_barrier();
+      if (t + 2 < nt) issue_half(t + 2, 0);
+    }
+    if constexpr (p == kPh - kLook + 1)
+      if (t + 2 < nt) issue_half(t + 2, 1);
+    // the batch kLook phases ahead (past the last tile: a stale stage, unused)
+    if constexpr (p + kLook < kPh) read_frags(t, p + kLook);
+    else read_frags(t + 1, p + kLook - kPh);
+    mma(P);
+    // each phase its own scheduling region: otherwise the scheduler may move
+    // a later phase's MFMA (whose fragments were just requested) to the
+    // front and the wait for it stalls on every outstanding LDS read
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
+  // The epilogue's kernel arguments are fetched before the first barrier,
+  // whose wait covers them: a scalar load still in flight at the main loop's
+  // head would make the loop's first LDS wait a full one (scalar loads return
+  // out of order), on every K-tile.
+  pin_sgpr(ep.out), pin_sgpr(ep.ld_out), pin_sgpr(ep.out2), pin_sgpr(ep.ld_out2);
+  pin_sgpr(ep.bias), pin_sgpr(ep.resid), pin_sgpr(ep.aux), pin_sgpr(ep.split);
+  pin_sgpr(ep.col2), pin_sgpr(ep.mean), pin_sgpr(ep.rstd), pin_sgpr(ep.rowpart);
+  pin_sgpr(ep.rowpart_ld), pin_sgpr(part);
   if (nt > 0) issue(0);
   if (nt > 1) issue(1);
   if (nt > 1) wait_dma<kDmaPerStage>();  // tile 0 landed; tile 1 may be in flight
   else wait_dma<0>();
   block_barrier();
-  read_frags(0, 0);
-  read_frags(0, 1);
+  // batch by batch, as in the loop, so the wait at the loop's head (merged
+  // over both ways in) can leave the later batches in flight
+#pragma unroll
+  for (int p = 0; p < kLook; ++p) {
+    read_frags(0, p);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   for (int t = 0; t < nt; ++t) {
-    read_frags(t, 2);
-    mma(0);
-    read_frags(t, 3);
-    mma(1);
-    // Every wave has issued (and with the barrier, finished) its reads of
-    // tile t, so its stage can take tile t + 2; tile t + 1 has landed for
-    // this wave, and after the barrier for all.
-    wait_dma<0>();
-    block_barrier();
-    // the loads of tile t + 2 spread over k-steps 2 and 3, each half issued
-    // ahead of that k-step's fragment reads (about 0.5% faster than after
-    // them), and the next tile's first fragments (past the last tile: a
-    // stale stage, unused)
-    if (t + 2 < nt) issue_half(t + 2, 0);
-    read_frags(t + 1, 0);
-    mma(2);
-    __builtin_amdgcn_sched_barrier(0);
-    if (t + 2 < nt) issue_half(t + 2, 1);
-    read_frags(t + 1, 1);
-    mma(3);
-    __builtin_amdgcn_sched_barrier(0);
+    phase(t, std::integral_constant<int, 0>{});
+    phase(t, std::integral_constant<int, 1>{});
+    phase(t, std::integral_constant<int, 2>{});
+    phase(t, std::integral_constant<int, 3>{});
+    phase(t, std::integral_constant<int, 4>{});
+    phase(t, std::integral_constant<int, 5>{});
+    phase(t, std::integral_constant<int, 6>{});
+    phase(t, std::integral_constant<int, 7>{});
   }
 
   block_barrier();  // every wave is done with the main loop's LDS
@@ -701,9 +772,9 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   if (slice >= 0) {
     // partial tile of one K-slice, stored whole (bounds are applied on reduce)
     float* pt = part + ((size_t)(lid - n_full) * splits + slice) * (kBM * kBN);
-    wave_epilogue_lds<EPI, GT>(ep, pt, acc, wm, wn, kBM, kBN, fr, fh, lane, buf);
+    wave_epilogue_lds<EPI, GT>(ep, pt, acc, wm, wn, kBM, kBN, lane, buf);
   } else {
-    wave_epilogue_lds<EPI, GT>(ep, nullptr, acc, m0 + wm, n0 + wn, M, N, fr, fh, lane, buf);
+    wave_epilogue_lds<EPI, GT>(ep, nullptr, acc, m0 + wm, n0 + wn, M, N, lane, buf);
   }
 }
 
