@@ -31,6 +31,26 @@ template <> PB_DEV void load8_stream<float>(const float* p, float* v) {
   for (int i = 0; i < 4; ++i) { v[i] = a[i]; v[4 + i] = b[i]; }
 }
 
+// Eight elements as loaded (packed bf16, or two fp32 quads, read once:
+// non-temporal), unpacked where they are used: packed, a bf16 batch of rows
+// takes half the registers.
+template <typename T> struct Raw8;
+template <> struct Raw8<bf16> {
+  u32x4 w;
+  PB_DEV void load(const bf16* p) {
+    w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  }
+  PB_DEV float operator[](int e) const { return (e & 1) ? hi_bf(w[e >> 1]) : lo_bf(w[e >> 1]); }
+};
+template <> struct Raw8<float> {
+  f32x4 a, b;
+  PB_DEV void load(const float* p) {
+    a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
+  }
+  PB_DEV float operator[](int e) const { return e < 4 ? a[e] : b[e - 4]; }
+};
+
 constexpr int kLnThreads = 512;
 constexpr int kLnWaves = kLnThreads / 64;
 
@@ -104,6 +124,77 @@ __global__ __launch_bounds__(kLnThreads) void ln_fwd_kernel(const T* __restrict_
   }
 }
 
+// One wave per row for bf16 rows of NC * 512 columns: the row stays in
+// registers as packed bf16 (NC 16-byte chunks per lane, each load
+// instruction covering 1 KB of the row), the statistics come from wave
+// reductions with no workgroup barrier, and a 2048-row input has every row
+// in flight at once (2048 waves on 256 CUs) instead of two rounds of
+// 512-thread workgroups.  Same two passes as above (mean, then the sum of
+// squared deviations), fp32 throughout.
+// An empty asm that claims to rewrite the packed row, so values unpacked
+// from it before this point are not reused after it.
+template <int NC>
+PB_DEV void keep_packed(u32x4 (&w)[NC]) {
+#pragma unroll
+  for (int j = 0; j < NC; ++j) asm volatile("" : "+v"(w[j]));
+}
+
+template <int NC>
+__global__ __launch_bounds__(256) void ln_fwd_wave_bf16(const bf16* __restrict__ x,
+                                                        const bf16* __restrict__ gamma,
+                                                        const bf16* __restrict__ beta,
+                                                        bf16* __restrict__ h,
+                                                        float* __restrict__ mean_out,
+                                                        float* __restrict__ rstd_out, int rows,
+                                                        float eps) {
+  constexpr int H = NC * 512;
+  const int lane = threadIdx.x & 63;
+  const int row = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (row >= rows) return;  // wave-uniform
+  const bf16* xr = x + (size_t)row * H;
+  u32x4 w[NC];
+#pragma unroll
+  for (int j = 0; j < NC; ++j)
+    w[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(xr + (j * 64 + lane) * 8));
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NC; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s += lo_bf(w[j][i]) + hi_bf(w[j][i]);
+  const float mu = wave_sum(s) / (float)H;
+  // each pass unpacks the row again: kept unpacked from one pass to the
+  // next, the row would need twice the registers
+  keep_packed<NC>(w);
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < NC; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float d0 = lo_bf(w[j][i]) - mu, d1 = hi_bf(w[j][i]) - mu;
+      q += d0 * d0 + d1 * d1;
+    }
+  const float rs = 1.0f / sqrtf(wave_sum(q) / (float)H + eps);
+  keep_packed<NC>(w);
+  bf16* hr = h + (size_t)row * H;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const int c = (j * 64 + lane) * 8;
+    float g[8], b[8], o[8];
+    load8(gamma + c, g);
+    load8(beta + c, b);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = (lo_bf(w[j][i]) - mu) * rs * g[2 * i] + b[2 * i];
+      o[2 * i + 1] = (hi_bf(w[j][i]) - mu) * rs * g[2 * i + 1] + b[2 * i + 1];
+    }
+    store8(hr + c, o);
+  }
+  if (lane == 0) {
+    mean_out[row] = mu;
+    rstd_out[row] = rs;
+  }
+}
+
 // Column-parallel LayerNorm backward.  The row terms sum gamma dh and
 // sum gamma dh xhat arrive as 64-column group partials from the dh GEMM's
 // epilogue, so no row-wide reduction is left here: each workgroup owns 16
@@ -159,15 +250,17 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
   // issued before this batch's dx stores, so waiting for them never waits for
   // a store as well (one counter covers both; loaded one batch at a time
   // after the previous stores, every batch paid the full load latency).
-  constexpr int kBatch = 2, kBatches = kApplyRows / kBatch;
-  float xv[2][kBatch][8], dv[2][kBatch][8], yv[2][kBatch][8];
+  // bf16 rows are held packed, four to a batch (four batches per workgroup
+  // instead of eight, with the same registers).
+  constexpr int kBatch = sizeof(T) == 2 ? 4 : 2, kBatches = kApplyRows / kBatch;
+  Raw8<T> xv[2][kBatch], dv[2][kBatch], yv[2][kBatch];
   auto load_batch = [&](int buf, int rb) {
 #pragma unroll
     for (int i = 0; i < kBatch; ++i) {
       const size_t off = (size_t)(r0 + min(rb + i, nr - 1)) * H + c;
-      load8_stream(x + off, xv[buf][i]);
-      load8_stream(dh + off, dv[buf][i]);
-      load8_stream(dy + off, yv[buf][i]);
+      xv[buf][i].load(x + off);
+      dv[buf][i].load(dh + off);
+      yv[buf][i].load(dy + off);
     }
   };
   load_batch(0, 0);
@@ -293,9 +386,35 @@ void ln_fwd_nv(const void* x, const void* gamma, const void* beta, void* h, floa
                                                    (const T*)beta, (T*)h, mean, rstd, H, eps);
 }
 
+template <int NC>
+void ln_fwd_wave(const void* x, const void* gamma, const void* beta, void* h, float* mean,
+                 float* rstd, int rows, float eps, hipStream_t s) {
+  ln_fwd_wave_bf16<NC><<<(rows + 3) / 4, 256, 0, s>>>((const bf16*)x, (const bf16*)gamma,
+                                                      (const bf16*)beta, (bf16*)h, mean, rstd,
+                                                      rows, eps);
+}
+
+// bf16 rows of 512 NC columns for the NC instantiated here (H = 5120 and
+// 12288 among them) take the wave-per-row kernel; true if launched.
+bool ln_fwd_wave_dispatch(const void* x, const void* gamma, const void* beta, void* h,
+                          float* mean, float* rstd, int rows, int H, float eps, hipStream_t s) {
+  if (H % 512 != 0) return false;
+  switch (H / 512) {
+    case 4: ln_fwd_wave<4>(x, gamma, beta, h, mean, rstd, rows, eps, s); return true;
+    case 8: ln_fwd_wave<8>(x, gamma, beta, h, mean, rstd, rows, eps, s); return true;
+    case 10: ln_fwd_wave<10>(x, gamma, beta, h, mean, rstd, rows, eps, s); return true;
+    case 12: ln_fwd_wave<12>(x, gamma, beta, h, mean, rstd, rows, eps, s); return true;
+    case 16: ln_fwd_wave<16>(x, gamma, beta, h, mean, rstd, rows, eps, s); return true;
+    case 24: ln_fwd_wave<24>(x, gamma, beta, h, mean, rstd, rows, eps, s); return true;
+    default: return false;
+  }
+}
+
 template <typename T>
 void ln_fwd_t(const void* x, const void* gamma, const void* beta, void* h, float* mean,
               float* rstd, int rows, int H, float eps, hipStream_t s) {
+  if constexpr (sizeof(T) == 2)
+    if (ln_fwd_wave_dispatch(x, gamma, beta, h, mean, rstd, rows, H, eps, s)) return;
   const int nv = (H + kLnThreads * 8 - 1) / (kLnThreads * 8);
   switch (nv) {
     case 1: ln_fwd_nv<T, 1>(x, gamma, beta, h, mean, rstd, rows, H, eps, s); break;
