@@ -51,6 +51,10 @@ CASES = [
     # tiles plus 2 tail tiles split 8 ways along K
     shape("bf16_split_tail", batch=1, seq=520, hidden=512, heads=4, head_dim=128, ffn=20360,
           window=100),
+    # a hidden size that takes the one-wave-per-row LayerNorm forward (2048 =
+    # 4 x 512 columns), with 262 rows: the last workgroup holds two rows
+    shape("bf16_h2048_wave_ln", batch=2, seq=131, hidden=2048, heads=4, head_dim=128, ffn=512,
+          window=90),
 ]
 
 
