@@ -1,16 +1,16 @@
 // Projection GEMMs of the parallel block with fused epilogues.
 //
-// bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 256x256 output tile per
-// workgroup of eight waves (each wave 64x128).  Two kernels share the tile,
-// the wave layout and the epilogues:
+// bf16 path: 256x256 output tile per workgroup of eight waves (each wave
+// 64x128).  Two kernels share the tile, the wave layout and the epilogues:
 //   - K a multiple of 64 (every GEMM of the block at the benchmarked sizes):
-//     operands reach LDS by LDS-DMA, K-tiles of 64 through two stages,
-//     fragments read two k-steps ahead and the barrier placed mid-tile (see
-//     the DMA kernel below);
-//   - otherwise (ragged token counts in the weight-gradient GEMMs): K-tile
-//     64, double-buffered LDS, loads staged through registers with zero fill;
-//     an M- or N-contiguous operand is loaded as 8x8 blocks and transposed in
-//     registers on its way into LDS.
+//     MFMA v_mfma_f32_16x16x32_bf16, operands reach LDS by LDS-DMA, K-tiles
+//     of 64 through two stages, fragments read two phases ahead and the
+//     barrier placed before the K-tile's last two phases (see the DMA kernel
+//     below);
+//   - otherwise (ragged token counts in the weight-gradient GEMMs): MFMA
+//     v_mfma_f32_32x32x16_bf16, K-tile 64, double-buffered LDS, loads staged
+//     through registers with zero fill; an M- or N-contiguous operand is
+//     loaded as 8x8 blocks and transposed in registers on its way into LDS.
 // The MFMA is issued with the roles of the operands swapped (the N tile as
 // MFMA "A"), so each lane ends up holding four consecutive output columns of
 // one row.  The DMA kernel stages its accumulators through LDS before the
