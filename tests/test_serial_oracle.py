@@ -2,11 +2,21 @@
 
 * special cases where the serial block reduces to the parallel one (checked
   against the separately pinned parallel oracle), which catch a dropped
-  residual, a missing bias or the wrong LayerNorm feeding the MLP;
+  residual or a missing bias; each zeroes one branch, so on their own they
+  cannot tell which tensor feeds the second LayerNorm;
+* fp64 autograd of an independent torch-module implementation with both
+  branches active, which fixes the forward composition (the second
+  LayerNorm reads x1 = x + attention, not x) and every gradient;
 * central finite differences of every gradient on a tiny block.
+
+test_serial_oracle_mutations.py plants slips in the serial oracle and checks
+that these pins catch them.
 """
+import math
+
 import numpy as np
 import pytest
+import torch
 
 from oracle import pblock_oracle as po
 from oracle import serial_oracle as so
@@ -102,3 +112,50 @@ def test_gradients_match_finite_differences(name):
     fd = (loss(eps) - loss(-eps)) / (2 * eps)
     an = float((grads[key] * direction).sum())
     assert abs(fd - an) <= 1e-6 * max(1.0, abs(fd)), (name, fd, an)
+
+
+# --------------------------------------------------------------------------
+# An independent autograd implementation of the standard pre-LN block, with
+# both branches active (Section 3.1, Eq. 1 read as the serial block the text
+# names).  Written from torch modules and explicit -inf masks; no code is
+# shared with the oracle's forward or its chain rule.
+def torch_serial_block(cfg, t):
+    A, d, S = cfg.attn_width, cfg.head_dim, cfg.seq
+    x = t["x"]
+    h1 = torch.nn.functional.layer_norm(x, (cfg.hidden,), t["gamma1"], t["beta1"], cfg.ln_eps)
+    qkv = torch.nn.functional.linear(h1, t["w_in"][:3 * A], t["b_in"][:3 * A])
+    q, k, v = torch.split(qkv, [A, A, A], dim=-1)
+    i = torch.arange(S)[:, None]
+    j = torch.arange(S)[None, :]
+    keep = (j <= i) & (j > i - cfg.window)
+    heads = []
+    for hd in range(cfg.heads):
+        sl = slice(hd * d, (hd + 1) * d)
+        s = (q[..., sl] @ k[..., sl].transpose(-1, -2)) / math.sqrt(d)
+        heads.append(torch.softmax(s.masked_fill(~keep, float("-inf")), dim=-1) @ v[..., sl])
+    x1 = x + torch.nn.functional.linear(torch.cat(heads, dim=-1), t["w_out"][:, :A], t["b_o"])
+    h2 = torch.nn.functional.layer_norm(x1, (cfg.hidden,), t["gamma2"], t["beta2"], cfg.ln_eps)
+    u = torch.nn.functional.linear(h2, t["w_in"][3 * A:], t["b_in"][3 * A:])
+    g = torch.nn.functional.gelu(u, approximate="tanh" if cfg.gelu_tanh else "none")
+    return x1 + torch.nn.functional.linear(g, t["w_out"][:, A:], t["b_down"])
+
+
+@pytest.mark.parametrize("window,tanh", [(1, True), (3, True), (7, False), (20, True)])
+def test_matches_torch_autograd_with_both_branches(window, tanh):
+    """Both branches on, every gradient: y and all ten gradients equal fp64
+    autograd of the block built from torch modules."""
+    cfg = po.OracleConfig(batch=2, seq=7, hidden=12, heads=2, head_dim=4, ffn=10, window=window,
+                          ln_eps=1e-5, gelu_tanh=tanh)
+    p = draw(cfg, 20 + window)
+    s = so.run_serial(cfg, p)
+    t = {n: torch.from_numpy(p[n].copy()).requires_grad_() for n in so.PARAMS}
+    y = torch_serial_block(cfg, t)
+    y.backward(torch.from_numpy(p["dy"]))
+    # both branches really reach y at these draws
+    A = cfg.attn_width
+    assert np.abs(p["w_out"][:, :A]).max() > 0 and np.abs(p["w_out"][:, A:]).max() > 0
+    np.testing.assert_allclose(s["y"], y.detach().numpy(), rtol=1e-11, atol=1e-12)
+    for n in so.PARAMS:
+        key = {"x": "dx"}.get(n, "d" + n)
+        np.testing.assert_allclose(s[key], t[n].grad.numpy(), rtol=1e-9, atol=1e-11,
+                                   err_msg=n)
