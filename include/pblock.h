@@ -142,6 +142,17 @@ pb_status pblock_forward(const pb_config* cfg, const void* x,
                          void* y, void* saved, void* ws, size_t ws_bytes,
                          hipStream_t stream);
 
+/* Byte offsets, within the backward workspace, of the intermediates that
+ * pblock_backward leaves there, in the order:
+ *   d_o [T, A]     act  the attention output's gradient (dC[:, :A])
+ *   dz  [T, N_in]  act  dQ | dK | dV | dU, the in-projection's output
+ *                       gradient (dQ, dK, dV from the attention backward)
+ *   dh  [T, H]     act  the LayerNorm output's gradient
+ * They hold these values once the backward call has passed on its stream,
+ * until the workspace is used again.  offsets must hold 3 entries.  Host
+ * only; for inspection and tests. */
+pb_status pblock_workspace_offsets(const pb_config* cfg, size_t* offsets);
+
 /* Backward pass: the gradients of sum(y * dy) with respect to x and every
  * parameter, given the stash of the matching forward call.  dx is in the
  * activation dtype; the six parameter gradients are fp32 and overwritten.

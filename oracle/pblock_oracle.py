@@ -53,6 +53,7 @@ __all__ = [
     "swa_head_backward",
     "block_forward",
     "block_backward",
+    "head_attention",
 ]
 
 SQRT_2_OVER_PI = math.sqrt(2.0 / math.pi)
@@ -265,6 +266,35 @@ def block_backward(cfg: OracleConfig, x, gamma, beta, w_in, b_in, w_out, b_out,
     dx = dy + dx_ln
     return dict(dx=dx, dgamma=dgamma, dbeta=dbeta, dw_in=dw_in, db_in=db_in,
                 dw_out=dw_out, db_out=db_out)
+
+
+def head_attention(cfg: OracleConfig, inputs: dict, b: int, hd: int):
+    """One (batch row b, head hd) of the block's attention, forward and
+    backward, from the block's inputs (Eq. 2 of Section 3.1 and its
+    sliding-window attention; the FlashAttention-2 result of Section 3.3).
+
+    The same definitions as block_forward / block_backward restricted to one
+    head: h = LN(x) of row b; q, k, v from that head's rows of w_in and b_in;
+    (o, lse) by swa_head_forward; the head's output gradient
+    do = dy W_o[:, head columns] (the attention half of dC = dy W_out); and
+    (dq, dk, dv) by swa_head_backward.  Only this head's columns are formed,
+    so it stays cheap at full size.  Returns a dict of float64 arrays
+    q, k, v, o, lse, do, dq, dk, dv ([S, d], lse [S]).
+    """
+    A, d = cfg.attn_width, cfg.head_dim
+    f = {n: np.asarray(inputs[n], dtype=np.float64)
+         for n in ("x", "gamma", "beta", "w_in", "b_in", "w_out", "dy")}
+    h, _, _, _ = layer_norm(f["x"][b], f["gamma"], f["beta"], cfg.ln_eps)
+    cols = slice(hd * d, (hd + 1) * d)
+    qkv = []
+    for j in range(3):
+        rows = slice(j * A + hd * d, j * A + (hd + 1) * d)
+        qkv.append(h @ f["w_in"][rows].T + f["b_in"][rows])
+    q, k, v = qkv
+    o, lse = swa_head_forward(q, k, v, cfg.window)
+    do = f["dy"][b] @ f["w_out"][:, cols]
+    dq, dk, dv = swa_head_backward(q, k, v, do, cfg.window)
+    return dict(q=q, k=k, v=v, o=o, lse=lse, do=do, dq=dq, dk=dk, dv=dv)
 
 
 def run_block(cfg: OracleConfig, inputs: dict, weight_rows=None):

@@ -343,6 +343,16 @@ size_t pblock_workspace_bytes(const pb_config* cfg, int mode) {
   }
 }
 
+pb_status pblock_workspace_offsets(const pb_config* cfg, size_t* offsets) {
+  PB_CHECK(check_config(cfg));
+  if (!offsets) return fail(PB_ERR_INVALID_ARG, "offsets is NULL");
+  const BwdLayout W = bwd_layout(dims_of(cfg));
+  offsets[0] = W.d_o;
+  offsets[1] = W.dz;
+  offsets[2] = W.dh;
+  return PB_OK;
+}
+
 pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gamma,
                          const void* ln_beta, const void* w_in, const void* b_in,
                          const void* w_out, const void* b_out, void* y, void* saved, void* ws,

@@ -24,11 +24,13 @@ ATTN_WS_FORWARD, ATTN_WS_BACKWARD_MIN, ATTN_WS_BACKWARD = 0, 1, 2
 STATUS = {0: "PB_OK", 1: "PB_ERR_INVALID_ARG", 2: "PB_ERR_UNSUPPORTED", 3: "PB_ERR_WORKSPACE",
           4: "PB_ERR_HIP"}
 SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
+WORKSPACE_REGIONS = ("d_o", "dz", "dh")
 SERIAL_SAVED_REGIONS = ("h1", "z", "c", "mean1", "rstd1", "lse", "x1", "h2", "mean2", "rstd2")
 
 # Every function the header declares (checked by the CPU tests).
 EXPORTS = (
     "pblock_validate", "pblock_saved_bytes", "pblock_saved_offsets", "pblock_workspace_bytes",
+    "pblock_workspace_offsets",
     "pblock_forward", "pblock_backward", "pblock_swattn_forward",
     "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_set_step_events",
     "pblock_status_string", "pblock_last_error", "pblock_serial_saved_bytes",
@@ -88,6 +90,7 @@ def load_library(path: str = LIB_PATH):
         "pblock_saved_bytes": (c_size_t, [cfgp]),
         "pblock_saved_offsets": (c_int, [cfgp, POINTER(c_size_t)]),
         "pblock_workspace_bytes": (c_size_t, [cfgp, c_int]),
+        "pblock_workspace_offsets": (c_int, [cfgp, POINTER(c_size_t)]),
         "pblock_forward": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, c_size_t, P]),
         "pblock_backward": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P,
                                     c_size_t, P]),
@@ -180,6 +183,13 @@ def pblock_saved_offsets(cfg: PbConfig) -> dict:
 def pblock_workspace_bytes(cfg: PbConfig, mode: int) -> int:
     """mode: WS_FORWARD, WS_FORWARD_WITH_STASH or WS_BACKWARD."""
     return load_library().pblock_workspace_bytes(ctypes.byref(cfg), int(mode))
+
+
+def pblock_workspace_offsets(cfg: PbConfig) -> dict:
+    """Offsets of d_o, dz and dh in the backward workspace."""
+    arr = (c_size_t * len(WORKSPACE_REGIONS))()
+    _check(load_library().pblock_workspace_offsets(ctypes.byref(cfg), arr))
+    return dict(zip(WORKSPACE_REGIONS, list(arr)))
 
 
 def pblock_forward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, y, saved=None, ws=None,
@@ -404,6 +414,18 @@ class ParallelBlock:
     def saved_view(self, name: str):
         """A typed view of one stash region (h, z, c, mean, rstd, lse)."""
         return _stash_view(self.cfg, self.saved, pblock_saved_offsets(self.cfg), name)
+
+    def workspace_view(self, name: str):
+        """A typed view of one backward intermediate (d_o, dz, dh) in the
+        workspace, valid after backward() until the next call."""
+        import torch
+        cfg = self.cfg
+        T, H, A = cfg.batch * cfg.seq, cfg.hidden, cfg.heads * cfg.head_dim
+        act = torch.bfloat16 if cfg.dtype == PB_BF16 else torch.float32
+        cols = {"d_o": A, "dz": 3 * A + cfg.ffn, "dh": H}[name]
+        off = pblock_workspace_offsets(cfg)[name]
+        nbytes = T * cols * torch.empty((), dtype=act).element_size()
+        return self.ws[off:off + nbytes].view(act).view(T, cols)
 
 
 def _stash_view(cfg, saved, offsets: dict, name: str):

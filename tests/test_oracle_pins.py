@@ -364,3 +364,39 @@ def test_causal_locality(window, t):
     expect = np.zeros(cfg.seq, dtype=bool)
     expect[t:t + window] = True
     np.testing.assert_array_equal(changed, expect)
+
+
+@pytest.mark.parametrize("window", [1, 4, 12])
+def test_head_attention_matches_block_and_autograd(window):
+    """head_attention (one head of the block, forward and backward) against
+    the block oracle's own cache, and its gradients against torch autograd of
+    the independent block: the head's rows of dW_in are sum_b dq_b^T h_b (and
+    likewise dk, dv), of db_in sum_b sum_s dq_b."""
+    cfg = tiny_cfg(window, batch=2)
+    inp = tiny_inputs(cfg, seed=30 + window)
+    f = {n: np.asarray(v, np.float64) for n, v in inp.items()}
+    _, cache = orc.block_forward(cfg, f["x"], f["gamma"], f["beta"], f["w_in"], f["b_in"],
+                                 f["w_out"], f["b_out"])
+    t = {n: torch.from_numpy(inp[n].copy()).requires_grad_() for n in NAMES}
+    torch_block(cfg, t).backward(torch.from_numpy(inp["dy"]))
+    A, d = cfg.attn_width, cfg.head_dim
+    for hd in range(cfg.heads):
+        cols = slice(hd * d, (hd + 1) * d)
+        acc_w = [0.0, 0.0, 0.0]
+        acc_b = [0.0, 0.0, 0.0]
+        for b in range(cfg.batch):
+            r = orc.head_attention(cfg, inp, b, hd)
+            np.testing.assert_allclose(r["o"], cache["o"][b, :, cols], rtol=1e-12, atol=1e-13)
+            np.testing.assert_allclose(r["lse"], cache["lse"][b, hd], rtol=1e-12, atol=1e-13)
+            for j, n in enumerate("qkv"):
+                zc = slice(j * A + hd * d, j * A + (hd + 1) * d)
+                np.testing.assert_allclose(r[n], cache["z"][b, :, zc], rtol=1e-12, atol=1e-13)
+            for j, n in enumerate(("dq", "dk", "dv")):
+                acc_w[j] = acc_w[j] + r[n].T @ cache["h"][b]
+                acc_b[j] = acc_b[j] + r[n].sum(axis=0)
+        for j in range(3):
+            rows = slice(j * A + hd * d, j * A + (hd + 1) * d)
+            np.testing.assert_allclose(acc_w[j], t["w_in"].grad.numpy()[rows], rtol=1e-9,
+                                       atol=1e-11)
+            np.testing.assert_allclose(acc_b[j], t["b_in"].grad.numpy()[rows], rtol=1e-9,
+                                       atol=1e-11)
