@@ -30,7 +30,7 @@ FLAGS = [
 # with vector arithmetic; keeping all matrix results in ordinary vector
 # registers avoids per-tile copies between the two register files.
 EXTRA = {
-    "attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1", "-mllvm", "-disable-lsr"],
 }
 
 

@@ -22,6 +22,7 @@
 //
 // fp32 kernels: one thread per query (or key), plain loops; parity path.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -208,22 +209,203 @@ PB_DEV WorkItem work_item() {
   return WorkItem{L / hb_n, hb % (int)gridDim.y, hb / (int)gridDim.y};
 }
 
-// ============================================================== forward
-// Workgroup: 32 kWavesQ queries of one (batch row, head); wave w owns queries
-// q0 + 32 w .. +31, lane l query q0 + 32 w + (l & 31).  Per key tile:
-// S^T = K Q^T (keys x queries), online softmax per lane, O^T += V^T P^T.
+// ====================================================== 16x16x32 tiles
+// Tiles for the v_mfma_f32_16x16x32_bf16 kernels, natural token-major like
+// the ones above, with their own chunk swizzle: chunk c of row r is stored
+// at slot c ^ swz16(r).  The maps are linear in the row bits and were found
+// by exhaustive search under a model of the LDS (64 banks of 4 bytes) that
+// reproduces the measured behaviour of earlier layouts: a 16-byte read is
+// free of conflicts when each 16 lanes hit distinct banks; a transposing
+// 8-byte read when each 32 lanes hit distinct banks and, in addition, the
+// four rows a 16-lane group reads lie in four distinct 64-byte quarters of
+// the bank space (a layout with two of them in one quarter ran the
+// forward's O update about six times slower).  Both of the forward's reads
+// (K rows in the permuted key order below, one chunk per 16 lanes; the
+// transposing reads of V, rows 8 g + j of lane group g) satisfy these for
+// head dims 64, 96 and 128; for 96 only the low two chunk bits move, which
+// keeps the slot below 12.  Only row bits 0, 1, 3 and 4 enter.
 template <int D>
-__global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2))) void attn_fwd_bf16(
+PB_DEV int swz16(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | (((r >> 3) & 1) << 1) | ((r >> 4) & 1);
+  else if constexpr (D == 96) return (((r >> 3) & 1) << 1) | ((r >> 4) & 1);
+  else return (((r >> 1) & 1) << 2) | (((r >> 3) & 1) << 1) | ((r >> 4) & 1);
+}
+// The swizzle of tiles read only by transposing reads (V in the forward).
+// Same rules, and in addition the two 16-byte halves of a 32-byte row
+// segment are never swapped (bit 0 stays), as in the GEMM's transposed
+// layout.
+template <int D>
+PB_DEV int swz16v(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | (((r >> 3) & 1) << 1);
+  else if constexpr (D == 96) return ((r >> 3) & 1) << 1;
+  else return (((r >> 1) & 1) << 2) | (((r >> 3) & 1) << 1);
+}
+
+// Key order inside a 64-key tile for the score MFMAs.  Score block kb (16
+// keys; kb = 2 s + h) uses, as its MFMA row i, key 32 s + 8 (i / 4) + 4 h +
+// (i mod 4).  The result row i lands in lane group i / 4 as element i mod 4,
+// so lane group g holds keys 32 s + 8 g + 0..3 (block 2 s) and + 4..7 (block
+// 2 s + 1): exactly the eight consecutive keys that the probability operand
+// of the next MFMA (k-step s of 32 keys) wants from that lane group.
+PB_DEV int score_key(int kb, int i) { return 32 * (kb >> 1) + 8 * (i >> 2) + 4 * (kb & 1) + (i & 3); }
+constexpr int score_row_off(int kb) { return 32 * (kb >> 1) + 4 * (kb & 1); }
+
+// This lane's LDS byte offsets for the forward's fragment reads inside one
+// tile.  swz16 depends only on row bits 0, 1, 3 and 4, which are fixed per
+// lane for both reads, so each block's row offset (bits 2 and 5) is a
+// constant added to one per-lane base: D/32 bases for K and D/16 for V.
+//   k[ks]: A operand of K for score block kb, k-step ks (features 32 ks ..
+//          + 31) at k[ks] + 2 D score_row_off(kb): lane l supplies row
+//          score_key(kb, l & 15), features 32 ks + 8 (l >> 4) .. + 7.
+//   v[db]: A operand of V^T for features 16 db .. + 15 and keys 32 s ..
+//          + 31, by two transposing reads at v[db] + 2 D (32 s) and
+//          + 2 D (32 s + 4): lane 4 j + q of a 16-lane group addresses key
+//          base + j, features 16 db + 4 q .. + 3, and receives keys base ..
+//          base + 3 of its own feature 16 db + (l & 15); lane group g takes
+//          keys 32 s + 8 g .. + 7.
+template <int D>
+struct FwdLds {
+  uint32_t k[D / 32];
+  uint32_t v[D / 16];
+  PB_DEV explicit FwdLds(int lane) {
+    const int i = lane & 15, g = lane >> 4;
+    const int rk = score_key(0, i);
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+      k[ks] = (uint32_t)(rk * 2 * D + (((4 * ks + g) ^ swz16<D>(rk)) * 16));
+    const int j = i >> 2, q = i & 3;
+    const int tv = 8 * g + j;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      const int d0 = 16 * db + 4 * q;
+      v[db] = (uint32_t)(tv * 2 * D + (((d0 >> 3) ^ swz16v<D>(tv)) * 16) + (d0 & 7) * 2);
+    }
+  }
+};
+PB_DEV bf16x8 lds_b128(uint32_t addr) { return *(const PB_LDS bf16x8*)addr; }
+// Two transposing reads at addr and addr + gap bytes (four keys each).
+PB_DEV bf16x8 lds_tr2(uint32_t addr, uint32_t gap) {
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PB_LDS s16x4*)addr);
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((PB_LDS s16x4*)(addr + gap));
+  const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
+  return bf16x8{a4[0], a4[1], a4[2], a4[3], b4[0], b4[1], b4[2], b4[3]};
+}
+// Values consumed by an empty asm: computed by this point (IR passes would
+// otherwise sink them to their first use, out of the phase that interleaves
+// them with MFMAs).
+PB_DEV void keep(const bf16x8& x) { asm volatile("" ::"v"(__builtin_bit_cast(u32x4, x))); }
+PB_DEV void keep(float x) { asm volatile("" ::"v"(x)); }
+// Scheduling-group masks (sched_group_barrier): matrix, vector ALU, LDS read.
+constexpr int kSgMfma = 0x008, kSgValu = 0x002, kSgDsRead = 0x100;
+
+// LDS-DMA of a TL-row tile in the swz16 layout: this wave's NP / NW 1 KB
+// pieces (NP = TL 2 D / 1024, a multiple of NW).  Row r of the tile is token
+// row0 + r of a [rows_valid, ld] matrix (rows past the end read the last
+// one: finite values the window mask always zeroes).  The lane's 16 bytes
+// of piece i are global chunk slot ^ swz(row) of its row (swz16, or swz16v
+// with VSWZ); row[i] and cof[i] (that chunk's byte offset) are fixed per
+// lane.
+template <int D, int TL, int NW, bool VSWZ = false>
+struct DmaRows {
+  static constexpr int NP = TL * 2 * D / 1024;
+  static constexpr int NPW = NP / NW;
+  static_assert(NP % NW == 0, "whole pieces per wave");
+  int row[NPW];
+  uint32_t cof[NPW];
+  PB_DEV DmaRows(int wave, int lane) {
+    constexpr int RB = 2 * D;
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int p = (wave * NPW + i) * 1024 + 16 * lane;
+      row[i] = p / RB;
+      const int sw = VSWZ ? swz16v<D>(row[i]) : swz16<D>(row[i]);
+      cof[i] = (uint32_t)(((p / 16) % (RB / 16)) ^ sw) * 16u;
+    }
+  }
+  // offsets of this wave's pieces for the tile starting at token row0
+  PB_DEV void offsets(int row0, int rows_valid, int ld, uint32_t (&off)[NPW]) const {
+#pragma unroll
+    for (int i = 0; i < NPW; ++i)
+      off[i] = (uint32_t)min(row0 + row[i], rows_valid - 1) * (uint32_t)(2 * ld) + cof[i];
+  }
+  PB_DEV void issue(const bf16* base, const uint32_t (&off)[NPW], uint32_t lds_tile,
+                    int wave) const {
+#pragma unroll
+    for (int i = 0; i < NPW; ++i)
+      dma16s(base, off[i], lds_tile + (uint32_t)((wave * NPW + i) * 1024));
+  }
+};
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+PB_DEV f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+PB_DEV f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+// Reductions over the four lane groups (lanes l, l ^ 16, l ^ 32, l ^ 48),
+// by the two lane-swap instructions.
+PB_DEV float max4groups(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false,
+                                                  false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+PB_DEV float sum4groups(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false,
+                                                  false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+// Sum of the eight bf16 values of an operand, added to acc (two-element dot
+// products with (1, 1): the row sums use exactly the rounded probabilities
+// that the output MFMA multiplies).
+PB_DEV float add_bf16x8(const bf16x8& p, float acc) {
+  const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+  acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[0], p[1]}, one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[2], p[3]}, one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[4], p[5]}, one, acc, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[6], p[7]}, one, acc, false);
+}
+
+// ============================================================== forward
+// Workgroup: four waves, 128 queries of one (batch row, head); wave w owns
+// queries q0 + 32 w .. + 31 as two 16-query column blocks.  Per 64-key tile
+// it computes S^T = K Q^T (keys x queries, 4 x 2 blocks of 16 x 16: each
+// lane holds 16 scores of each of its two queries), the online softmax, and
+// O^T += V^T P^T (D/16 x 2 blocks).  A query's scores of one tile sit in four
+// lanes (one per lane group), which share one running maximum: the maximum
+// moves, with a cross-lane reduction, only when some lane's scores exceed it
+// by more than 8 (base 2), so probabilities stay below 256 and most tiles
+// skip both the reduction and the rescale (output and row sum share the
+// reference, so the final quotient is unchanged).  Row sums are kept per
+// lane and added across the four lanes at the end.
+// Software pipeline, so that the matrix cores always have independent work
+// next to the vector code: iteration t runs tile t + 1's score MFMAs next to
+// tile t's exponentials, then tile t's O^T MFMAs next to tile t + 1's mask
+// and maximum.  Each phase (one k-step of the scores, one 16-feature block
+// of O^T) is its own scheduling region that reads the next phase's
+// fragments while its MFMAs run.  LDS: K in two slots (tile t + 2 loads
+// while t + 1 is read), V in three (t + 2 loads while t is read and t + 1
+// waits).  Tiles outside a wave's window (one or two at either end of the
+// block's range) are masked entirely rather than skipped, which keeps the
+// loop free of branches around the pipelined code.
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_fwd_bf16(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V, int ld,
     bf16* __restrict__ O, int ld_o, float* __restrict__ lse, int S, int H, int W, float scale,
     int cs, int nc, float* __restrict__ po, float* __restrict__ plse) {
   constexpr int TL = kTL;
   constexpr int NB = kBlockQ;
   constexpr int TB = TL * 2 * D;  // bytes per tile
+  constexpr int KS = D / 32, DB = D / 16;
+  static_assert(kWavesQ == 4 && NB == 128 && TL == 64, "four waves of 32 queries, 64-key tiles");
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
-  auto k_off = [&](int s) { return (2 * s) * TB; };
-  auto v_off = [&](int s) { return (2 * s + 1) * TB; };
+  auto k_off = [](int s) { return (uint32_t)(s * TB); };        // K slots 0, 1
+  auto v_off = [](int s) { return (uint32_t)((2 + s) * TB); };  // V slots 0, 1, 2
 
   const int nqb = (S + NB - 1) / NB;
   const WorkItem wi = work_item();
@@ -233,140 +415,286 @@ __global__ __launch_bounds__(64 * kWavesQ) __attribute__((amdgpu_waves_per_eu(2)
   const int t_begin = chunk * cs;
   if (t_begin >= ntot) return;  // this block has fewer chunks than the longest
   const int t_end = min(ntot, t_begin + cs);
+  const int n = t_end - t_begin;
   const bool split = ntot > cs;
   const int head = wi.head, b = wi.b;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int fr = lane & 31, fh = lane >> 5;
+  const int g = lane >> 4, col = lane & 15;
   const size_t tok0 = (size_t)b * S;
-  const bf16* qb = Q + tok0 * ld + head * D;
   const bf16* kb = K + tok0 * ld + head * D;
   const bf16* vb = V + tok0 * ld + head * D;
 
   const int qw0 = q0 + 32 * wave;
-  const int q = qw0 + fr;
-  bf16x8 qf[D / 16];
+  bf16x8 qf[2][KS];
+  {
+    const bf16* qb = Q + tok0 * ld + head * D;
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-    qf[ks] = load_row_frag(qb + (size_t)min(q, S - 1) * ld + 16 * ks + 8 * fh, q < S);
-
-  const float c2 = scale * kLog2e;
-  float m_run = kNegInf, l_run = 0.f;
-  f32x16 o[D / 32];
+    for (int j = 0; j < 2; ++j) {
+      const int q = qw0 + 16 * j + col;
 #pragma unroll
-  for (int i = 0; i < D / 32; ++i) o[i] = zero16();
-
-  const int kv_begin = (max(0, q0 - W + 1) / TL) * TL;
-  const int w_lo = qw0 - W + 1, w_hi = min(qw0 + 31, S - 1);
-
-  dma_tile<D, TL, kWavesQ>(kb, ld, kv_begin + t_begin * TL, S, lds0 + k_off(0), wave, lane);
-  dma_tile<D, TL, kWavesQ>(vb, ld, kv_begin + t_begin * TL, S, lds0 + v_off(0), wave, lane);
-
-  for (int t = t_begin; t < t_end; ++t) {
-    const int cur = (t - t_begin) & 1;
-    const int kv0 = kv_begin + t * TL;
-    wait_dma_all();
-    block_barrier();
-    if (t + 1 < t_end) {
-      dma_tile<D, TL, kWavesQ>(kb, ld, kv0 + TL, S, lds0 + k_off(cur ^ 1), wave, lane);
-      dma_tile<D, TL, kWavesQ>(vb, ld, kv0 + TL, S, lds0 + v_off(cur ^ 1), wave, lane);
-    }
-    if (qw0 < S && kv0 <= w_hi && kv0 + TL - 1 >= w_lo) {
-      const unsigned char* kt = smem + k_off(cur);
-      const unsigned char* vt = smem + v_off(cur);
-      f32x16 s[TL / 32];
-#pragma unroll
-      for (int h2 = 0; h2 < TL / 32; ++h2) {
-        s[h2] = zero16();
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks)
-          s[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<D>(kt, 32 * h2 + fr, ks, fh),
-                                                          qf[ks], s[h2], 0, 0, 0);
-      }
-      const bool full = (kv0 + TL - 1 <= qw0) && (qw0 + 31 - kv0 < W) && (kv0 + TL <= S) &&
-                        (qw0 + 32 <= S);
-      if (!full) {
-        // element r of block h2 is key kv0 + 32 h2 + 8 (r >> 2) + 4 fh + (r & 3)
-        const int d0 = q - kv0 - 4 * fh, s0 = S - kv0 - 4 * fh;
-#pragma unroll
-        for (int h2 = 0; h2 < TL / 32; ++h2)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int c = 32 * h2 + 8 * (r >> 2) + (r & 3);
-            const bool ok = (unsigned)(d0 - c) < (unsigned)W && c < s0;
-            s[h2][r] = ok ? s[h2][r] : kNegInf;
-          }
-      }
-      float mx = kNegInf;
-#pragma unroll
-      for (int h2 = 0; h2 < TL / 32; ++h2)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[h2][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
-      // The reference maximum moves only when some query's scores exceed it
-      // by more than 8 (base 2): probabilities then stay below 256 and most
-      // tiles skip the rescale.  Output and sum share the reference, so the
-      // final quotient is unchanged.
-      if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = m_new == kNegInf ? 1.f : exp2_hw(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
-      }
-      const float m_use = m_run == kNegInf ? 0.f : m_run;
-      float ls = 0.f;
-#pragma unroll
-      for (int h2 = 0; h2 < TL / 32; ++h2)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = exp2_hw(fmaf(s[h2][r], c2, -m_use));
-          s[h2][r] = p;
-          ls += p;
-        }
-      l_run += ls;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-        for (int s2 = 0; s2 < TL / 16; ++s2)
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              frag_tr<D>(vt, 32 * db + fr, s2, fh, lane), probs_frag(s, s2), o[db], 0, 0, 0);
-      }
+      for (int ks = 0; ks < KS; ++ks)
+        qf[j][ks] = load_row_frag(qb + (size_t)min(q, S - 1) * ld + 32 * ks + 8 * g, q < S);
     }
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (q < S) {
+  const float c2 = scale * kLog2e;
+  float m_run[2] = {kNegInf, kNegInf}, l_run[2] = {0.f, 0.f};
+  f32x4 o[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db][0] = o[db][1] = zero4();
+
+  const int kv_begin = (max(0, q0 - W + 1) / TL) * TL;
+  const DmaRows<D, TL, kWavesQ> dk(wave, lane);
+  const DmaRows<D, TL, kWavesQ, true> dv(wave, lane);
+  constexpr int PK = DmaRows<D, TL, kWavesQ>::NPW;  // DMA instructions per tile and operand
+  const FwdLds<D> la(lane);
+  auto issue = [&](int i) {  // tile t_begin + i into K slot i % 2 and V slot i % 3
+    uint32_t off[PK];
+    dk.offsets(kv_begin + (t_begin + i) * TL, S, ld, off);
+    dk.issue(kb, off, lds0 + k_off(i & 1), wave);
+    dv.offsets(kv_begin + (t_begin + i) * TL, S, ld, off);
+    dv.issue(vb, off, lds0 + v_off(i % 3), wave);
+  };
+
+  f32x4 sa[4][2], sb[4][2];  // scores of two consecutive tiles (roles alternate)
+  bf16x8 pf[2][2];  // probabilities of tile t [k-step of 32 keys][query block]
+  bf16x8 kf[2][4];  // K fragments of two k-steps
+  bf16x8 vf[3][2];  // V^T fragments of three feature blocks [block mod 3][k-step]
+  float m_use[2];
+
+  auto read_k = [&](uint32_t base, int ks) {
+#pragma unroll
+    for (int k4 = 0; k4 < 4; ++k4)
+      kf[ks & 1][k4] = lds_b128(base + la.k[ks] + 2 * D * score_row_off(k4));
+  };
+  auto read_v = [&](uint32_t base, int db) {
+#pragma unroll
+    for (int sp = 0; sp < 2; ++sp)
+      vf[db % 3][sp] = lds_tr2(base + la.v[db] + 2 * D * 32 * sp, 2 * D * 4);
+  };
+  // exponentials of half a probability operand: unit u = (query block
+  // u / 4, k-step (u / 2) % 2, half u % 2), four values of block 2 sp + h
+  auto exp_unit = [&](const f32x4 (&sc)[4][2], int u) {
+    const int j = u >> 2, sp = (u >> 1) & 1, h = u & 1;
+    float p[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) p[e] = exp2_hw(fmaf(sc[2 * sp + h][j][e], c2, -m_use[j]));
+    const bf16 p0 = (bf16)p[0], p1 = (bf16)p[1], p2 = (bf16)p[2], p3 = (bf16)p[3];
+    pf[sp][j][4 * h] = p0, pf[sp][j][4 * h + 1] = p1;
+    pf[sp][j][4 * h + 2] = p2, pf[sp][j][4 * h + 3] = p3;
+    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+    l_run[j] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p0, p1}, one, l_run[j], false);
+    l_run[j] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p2, p3}, one, l_run[j], false);
+  };
+  // phase ks of the next tile's scores into sn (reads of k-step ks + 1
+  // inside), with the current tile's exponential units ks 8 / KS ..
+  auto score_phase = [&](uint32_t kbase, int ks, f32x4 (&sn)[4][2]) {
+    if (ks + 1 < KS) read_k(kbase, ks + 1);
+#pragma unroll
+    for (int k4 = 0; k4 < 4; ++k4) {
+      sn[k4][0] = mfma16(kf[ks & 1][k4], qf[0][ks], ks ? sn[k4][0] : zero4());
+      sn[k4][1] = mfma16(kf[ks & 1][k4], qf[1][ks], ks ? sn[k4][1] : zero4());
+    }
+  };
+  auto score_sched_pattern = [&](int ks, bool valu) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+      if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+      if (valu) __builtin_amdgcn_sched_group_barrier(kSgValu, 3, 0);
+      __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+      if (valu) __builtin_amdgcn_sched_group_barrier(kSgValu, 3, 0);
+    }
+  };
+  auto score_sched = [&](int ks, bool valu) {
+    score_sched_pattern(ks, valu);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto exp_phase = [&](const f32x4 (&sc)[4][2], int ks) {
+#pragma unroll
+    for (int u = ks * 8 / KS; u < (ks + 1) * 8 / KS; ++u) exp_unit(sc, u);
+  };
+  auto keep_exps = [&](int ks) {  // the units of exp_phase(ks), done
+#pragma unroll
+    for (int u = ks * 8 / KS; u < (ks + 1) * 8 / KS; ++u)
+      if (u % 2 == 1 || u == (ks + 1) * 8 / KS - 1) keep(pf[(u >> 1) & 1][u >> 2]);
+    keep(l_run[0]);
+    keep(l_run[1]);
+  };
+  // mask of a partial tile; its own region
+  auto mask_tile = [&](f32x4 (&sc)[4][2], int kv0) {
+    const bool full = (kv0 + TL - 1 <= qw0) && (qw0 + 31 - kv0 < W) && (kv0 + TL <= S) &&
+                      (qw0 + 32 <= S);
+    if (!full) {
+#pragma unroll
+      for (int k4 = 0; k4 < 4; ++k4)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int key = kv0 + score_key(k4, 4 * g + e);
+            const int q = qw0 + 16 * j + col;
+            const bool ok = (unsigned)(q - key) < (unsigned)W && key < S;
+            sc[k4][j][e] = ok ? sc[k4][j][e] : kNegInf;
+          }
+    }
+  };
+  // the scaled lane maxima of a tile's scores
+  auto lane_max = [&](const f32x4 (&sc)[4][2], float (&mx)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float m = sc[0][j][0];
+#pragma unroll
+      for (int k4 = 0; k4 < 4; ++k4)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m = fmaxf(m, sc[k4][j][e]);
+      mx[j] = m * c2;
+    }
+  };
+  // phase db of the current tile's O^T update (reads of block db + 2 inside)
+  auto pv_phase = [&](uint32_t vbase, int db) {
+    if (db + 2 < DB) read_v(vbase, db + 2);
+#pragma unroll
+    for (int sp = 0; sp < 2; ++sp) {
+      o[db][0] = mfma16(vf[db % 3][sp], pf[sp][0], o[db][0]);
+      o[db][1] = mfma16(vf[db % 3][sp], pf[sp][1], o[db][1]);
+    }
+  };
+  auto pv_sched_pattern = [&](int db, bool valu) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+      if (db + 2 < DB) __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
+      if (valu) __builtin_amdgcn_sched_group_barrier(kSgValu, 4, 0);
+    }
+  };
+  // new reference maxima from the lane maxima mx; returns whether any lane
+  // rescales, with the factors for O and l
+  auto update_max = [&](const float (&mx)[2], float (&alpha)[2]) {
+    alpha[0] = alpha[1] = 1.f;
+    const bool any = __builtin_amdgcn_ballot_w64(mx[0] > m_run[0] + 8.f || mx[1] > m_run[1] + 8.f);
+    if (any) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const float m_new = fmaxf(m_run[j], max4groups(mx[j]));
+        alpha[j] = m_new == kNegInf ? 1.f : exp2_hw(m_run[j] - m_new);
+        m_run[j] = m_new;
+      }
+    }
+    return any;
+  };
+
+  // One iteration: tile i's scores are in cur (masked, m_run covers them).
+  // With NEXT, tile i + 1's scores go to nxt next to tile i's exponentials,
+  // and its mask and maximum next to tile i's O^T update.
+  auto iteration = [&](int i, f32x4 (&cur)[4][2], f32x4 (&nxt)[4][2], auto NEXT) {
+    constexpr bool has_next = decltype(NEXT)::value;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) m_use[j] = m_run[j] == kNegInf ? 0.f : m_run[j];
+    wait_dma_upto(has_next ? PK : 0);  // V of tile i and K of tile i + 1 have landed
+    block_barrier();  // ... for every wave; the slots of tile i - 1 are free
+    if (i + 2 < n) issue(i + 2);
+    const uint32_t kbase = lds0 + k_off((i + 1) & 1), vbase = lds0 + v_off(i % 3);
+    if (has_next) read_k(kbase, 0);
+    read_v(vbase, 0);
+    read_v(vbase, 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (has_next) score_phase(kbase, ks, nxt);
+      exp_phase(cur, ks);
+      score_sched_pattern(ks, true);
+      keep_exps(ks);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float mx[2] = {kNegInf, kNegInf};
+    if (has_next) {
+      mask_tile(nxt, kv_begin + (t_begin + i + 1) * TL);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      pv_phase(vbase, db);
+      if (has_next && db == 0) lane_max(nxt, mx);
+      pv_sched_pattern(db, has_next && db == 0);
+      if (has_next && db == 0) keep(mx[0]), keep(mx[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (has_next) {
+      float alpha[2];
+      if (update_max(mx, alpha)) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          l_run[j] *= alpha[j];
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[db][j][e] *= alpha[j];
+        }
+      }
+    }
+  };
+
+  // prologue: tiles 0 and 1 requested; tile 0's scores, mask and maximum
+  issue(0);
+  if (n > 1) issue(1);
+  wait_dma_upto(n > 1 ? 3 * PK : PK);  // K of tile 0
+  block_barrier();
+  read_k(lds0 + k_off(0), 0);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    score_phase(lds0 + k_off(0), ks, sa);
+    score_sched(ks, false);
+  }
+  {
+    mask_tile(sa, kv_begin + t_begin * TL);
+    float mx[2], alpha[2];
+    lane_max(sa, mx);
+    update_max(mx, alpha);  // o and l are zero: nothing to rescale
+  }
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  int i = 0;
+  for (; i + 2 < n; i += 2) {
+    iteration(i, sa, sb, T_{});
+    iteration(i + 1, sb, sa, T_{});
+  }
+  if (n - i == 2) {
+    iteration(i, sa, sb, T_{});
+    iteration(i + 1, sb, sa, F_{});
+  } else {
+    iteration(i, sa, sb, F_{});
+  }
+
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const float l_tot = sum4groups(l_run[j]);
+    const int q = qw0 + 16 * j + col;
+    if (q >= S) continue;
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-    const float m_use = m_run == kNegInf ? 0.f : m_run;
+    const float mu = m_run[j] == kNegInf ? 0.f : m_run[j];
     const size_t row = ((size_t)b * H + head) * S + q;
     if (!split) {
-      bf16* orow = O + (tok0 + q) * ld_o + head * D;
+      bf16* orow = O + (tok0 + q) * ld_o + head * D + 4 * g;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float v[4] = {o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
-                        o[db][4 * j + 3] * inv};
-          store4(orow + 32 * db + 8 * j + 4 * fh, v);
-        }
-      if (fh == 0) lse[row] = (m_use + log2f(l_tot)) * kLn2;
+      for (int db = 0; db < DB; ++db) {
+        float v[4] = {o[db][j][0] * inv, o[db][j][1] * inv, o[db][j][2] * inv,
+                      o[db][j][3] * inv};
+        store4(orow + 16 * db, v);
+      }
+      if (g == 0) lse[row] = (mu + log2f(l_tot)) * kLn2;
     } else {
       // this chunk's normalised output and its base-2 log-sum-exp (-inf when
       // none of the chunk's keys is visible to the query)
       const size_t bhs = (size_t)gridDim.z * H * S;
-      float* prow = po + ((size_t)chunk * bhs + row) * D;
+      float* prow = po + ((size_t)chunk * bhs + row) * D + 4 * g;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          *reinterpret_cast<f32x4*>(prow + 32 * db + 8 * j + 4 * fh) =
-              f32x4{o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
-                    o[db][4 * j + 3] * inv};
-      if (fh == 0) plse[(size_t)chunk * bhs + row] = l_tot > 0.f ? m_use + log2f(l_tot) : kNegInf;
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<f32x4*>(prow + 16 * db) =
+            f32x4{o[db][j][0] * inv, o[db][j][1] * inv, o[db][j][2] * inv, o[db][j][3] * inv};
+      if (g == 0) plse[(size_t)chunk * bhs + row] = l_tot > 0.f ? mu + log2f(l_tot) : kNegInf;
     }
   }
 }
@@ -908,7 +1236,7 @@ __global__ __launch_bounds__(64) void attn_dkdv_f32(const float* __restrict__ Q,
 }
 
 template <int D>
-size_t fwd_lds() { return 2 * 2 * (size_t)kTL * 2 * D; }
+size_t fwd_lds() { return 5 * (size_t)kTL * 2 * D; }  // K: two slots, V: three
 template <int D>
 size_t dkdv_lds() {
   return kStagesDkdv * (2 * (size_t)kTLdkv * 2 * D + 2 * kTLdkv * 4) + 2 * 64 * 16 * 4;

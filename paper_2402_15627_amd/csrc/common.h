@@ -94,6 +94,15 @@ PB_DEV void transpose8x8(const u32x4* in, u32x4* out) {
   }
 }
 
+// ------------------------------------------------------------- LDS-DMA
+// One 16-byte LDS-DMA per lane: global sbase + voff (a wave-uniform 64-bit
+// base and a 32-bit lane offset in bytes) -> LDS lds_byte_addr + 16 * lane.
+PB_DEV void dma16s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
+               "s"(lds_byte_addr)
+               : "memory", "m0");
+}
+
 // -------------------------------------------------------------- reductions
 PB_DEV float wave_sum(float v) {
 #pragma unroll

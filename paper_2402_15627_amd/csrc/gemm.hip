@@ -377,11 +377,6 @@ PB_DEV void pin_sgpr(T v) {
 
 PB_DEV int swz_mn(int krow, int c) { return c ^ (4 * (krow & 3)) ^ (2 * ((krow >> 3) & 1)); }
 
-PB_DEV void dma16s(const void* sbase, uint32_t voff, uint32_t lds_byte_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
-               "s"(lds_byte_addr)
-               : "memory", "m0");
-}
 template <int N>
 PB_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 // The wait for LDS (and scalar) loads is the compiler's own instruction
