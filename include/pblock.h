@@ -241,6 +241,25 @@ pb_status pblock_swattn_forward(const pb_config* cfg, const void* q,
                                 void* o, int ld_o, float* lse, void* ws,
                                 size_t ws_bytes, hipStream_t stream);
 
+/* pblock_swattn_forward without a workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, layouts and results as
+ * pblock_swattn_forward with a full PB_ATTN_WS_FORWARD workspace (the same
+ * kernels and split plan; bitwise the same output).  The split partials
+ * live in a device array inside the library, PB_NOALLOC_SCRATCH_BYTES per
+ * GPU, held from the first call on that GPU (made with it current) until the
+ * process ends.  Nothing is allocated per call and nothing in it needs
+ * clearing.  A shape whose split plan needs more scratch than that is
+ * rejected with PB_ERR_UNSUPPORTED before any HIP call.  Every call on one
+ * GPU shares that GPU's scratch: calls that overlap on one GPU (on
+ * different streams, or from several host threads) race and must be
+ * ordered by the caller. */
+#define PB_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+pb_status pblock_swattn_forward_noalloc(const pb_config* cfg, const void* q,
+                                        const void* k, const void* v,
+                                        int ld_qkv, void* o, int ld_o,
+                                        float* lse, hipStream_t stream);
+
 /* Gradient of pblock_swattn_forward: given q, k, v, o (ld_o), lse and the
  * output gradient d_o (ld_do), writes dq, dk, dv (ld_dqkv).  ws: see above
  * (at least PB_ATTN_WS_BACKWARD_MIN bytes, else PB_ERR_WORKSPACE). */

@@ -9,7 +9,9 @@
 
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <initializer_list>
+#include <mutex>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -608,6 +610,79 @@ pb_status pblock_swattn_forward(const pb_config* cfg, const void* q, const void*
   if (ws) PB_CHECK(check_ptr(ws, "ws"));
   pb::launch_attn_forward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, lse, ws, ws ? ws_bytes : 0,
                           stream);
+  return finish_launches();
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of pblock_swattn_forward_noalloc: the split forward's fp32 chunk
+// partials live in this file-scope device array instead of a caller
+// workspace.  Every GPU the library runs on holds its own copy, at its own
+// address, until the process ends.  Host code never passes the array's name
+// to a kernel or a copy (on the host it is a stand-in, not a device
+// address); it uses the address hipGetSymbolAddress returns for the current
+// device, looked up once per device.
+constexpr size_t kNoallocScratchBytes = PB_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+pb_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(PB_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(PB_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p)
+        return fail(PB_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", dev,
+                    hipGetErrorString(e));
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return PB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pb_status pblock_swattn_forward_noalloc(const pb_config* cfg, const void* q, const void* k,
+                                        const void* v, int ld_qkv, void* o, int ld_o,
+                                        float* lse, hipStream_t stream) {
+  PB_CHECK(check_attn_config(cfg));
+  PB_CHECK(check_ptr(q, "q"));
+  PB_CHECK(check_ptr(k, "k"));
+  PB_CHECK(check_ptr(v, "v"));
+  PB_CHECK(check_ptr(o, "o"));
+  PB_CHECK(check_ptr(lse, "lse"));
+  PB_CHECK(check_ld(ld_qkv, cfg, "ld_qkv"));
+  PB_CHECK(check_ld(ld_o, cfg, "ld_o"));
+  pb::AttnShape a;
+  a.batch = cfg->batch;
+  a.seq = cfg->seq;
+  a.heads = cfg->heads;
+  a.head_dim = cfg->head_dim;
+  a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
+  const size_t need = pb::attn_fwd_partial_bytes(a, pb::attn_split_plan(dt_of(cfg), a));
+  if (need > kNoallocScratchBytes)
+    return fail(PB_ERR_UNSUPPORTED,
+                "this shape's split forward needs %zu bytes of scratch, more than the %zu the "
+                "allocation-free entry point holds; use pblock_swattn_forward with a workspace",
+                need, kNoallocScratchBytes);
+  void* ws = nullptr;
+  if (need) PB_CHECK(scratch_address(&ws));
+  pb::launch_attn_forward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, lse, ws, need, stream);
   return finish_launches();
 }
 

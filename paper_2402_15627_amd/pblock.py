@@ -38,7 +38,9 @@ EXPORTS = (
     "pblock_serial_backward", "pblock_lamb_workspace_bytes", "pblock_lamb_step",
     "pblock_ag_in_proj_workspace_bytes", "pblock_ag_in_proj",
     "pblock_rs_out_proj_workspace_bytes", "pblock_rs_out_proj", "pblock_rs_reduce",
+    "pblock_swattn_forward_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 32 << 20  # PB_NOALLOC_SCRATCH_BYTES
 LAMB_MAX_TENSORS = 16
 
 # pb_step order of include/pblock.h
@@ -96,6 +98,7 @@ def load_library(path: str = LIB_PATH):
                                     c_size_t, P]),
         "pblock_swattn_forward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, P, c_size_t, P]),
         "pblock_swattn_workspace_bytes": (c_size_t, [cfgp, c_int]),
+        "pblock_swattn_forward_noalloc": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, P]),
         "pblock_swattn_backward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, c_int, P, P, P, P,
                                            c_int, P, c_size_t, P]),
         "pblock_set_step_events": (c_int, [P, P]),
@@ -212,6 +215,12 @@ def pblock_swattn_forward(cfg, q, k, v, ld_qkv, o, ld_o, lse, ws=None, stream=No
     _check(load_library().pblock_swattn_forward(
         ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(lse), _ptr(ws),
         _nbytes(ws), _stream(stream)))
+
+
+def pblock_swattn_forward_noalloc(cfg, q, k, v, ld_qkv, o, ld_o, lse, stream=None):
+    _check(load_library().pblock_swattn_forward_noalloc(
+        ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(lse),
+        _stream(stream)))
 
 
 def pblock_swattn_workspace_bytes(cfg, mode: int) -> int:

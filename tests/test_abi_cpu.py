@@ -380,3 +380,22 @@ def test_rs_out_proj_and_reduce_reject_bad_arguments_before_launching():
     assert reduce(tp=0) == 1 and reduce(tp=65) == 1
     assert reduce(parts=[FAKE] * 7 + [FAKE + 4]) == 1 and "parts[7]" in pb.pblock_last_error()
     assert reduce(y=None) == 1 and reduce(b=FAKE + 2) == 1
+
+
+def test_noalloc_attention_rejects_oversized_scratch_on_host():
+    """The allocation-free attention forward refuses, before any HIP call, a
+    shape whose split plan needs more than PB_NOALLOC_SCRATCH_BYTES of
+    scratch (2 heads x 128 over 24000 tokens needs ~47 MB); the pointers are
+    never touched."""
+    c = pb.make_config(1, 24000, 64, 2, 128, 64, 24000)
+    assert pb.pblock_swattn_workspace_bytes(c, pb.ATTN_WS_FORWARD) > pb.NOALLOC_SCRATCH_BYTES
+    fake = 1 << 20  # aligned, never dereferenced: the call fails its host check first
+    lib = pb.load_library()
+    st = lib.pblock_swattn_forward_noalloc(ctypes.byref(c), fake, fake, fake, 256, fake, 256,
+                                           fake, None)
+    assert st == 2  # PB_ERR_UNSUPPORTED
+    assert "scratch" in pb.pblock_last_error()
+    # and a bad argument is still an argument error
+    st = lib.pblock_swattn_forward_noalloc(ctypes.byref(c), None, fake, fake, 256, fake, 256,
+                                           fake, None)
+    assert st == 1
