@@ -71,14 +71,12 @@ SERIAL_GEMM_PAIRS = {"dg": "dw_down", "dh2": "dw_up", "d_o": "dw_o", "dh1": "dw_
 
 
 def paired_steps(s, block="parallel"):
-    """The pairs of GEMM_PAIRS the library launches together for this
-    workload, as gemm_pair_supported decides: bf16, every K a multiple of 64
-    (the operand offsets of the LDS-DMA path fit 32 bits at these sizes)."""
-    if s.dtype != "bf16":
-        return {}
-    steps = gemm_steps(s, block)
+    """The pairs of GEMM_PAIRS (SERIAL_GEMM_PAIRS) that the library launches
+    together for this workload, from its own host query."""
+    from paper_2402_15627_amd import pblock as pb
     pairs = GEMM_PAIRS if block == "parallel" else SERIAL_GEMM_PAIRS
-    return {a: b for a, b in pairs.items() if steps[a][2] % 64 == 0 and steps[b][2] % 64 == 0}
+    shared = pb.pblock_backward_pairs(pb.config_from_shape(s), block)
+    return {a: b for (a, b), on in zip(pairs.items(), shared) if on}
 
 
 def launch_key(step, s):
@@ -188,7 +186,7 @@ def gemm_step_of(name, grid, s, block="parallel"):
     steps launch the same kernel on the same grid)."""
     steps = gemm_steps(s, block)
     if "gemm_bf16_dma_pair" in name:
-        tiles = lambda st: -(-steps[st][0] // 256) * -(-steps[st][1] // 256)  # noqa: E731
+        tiles = lambda st: gemm_tiles(*steps[st])  # noqa: E731
         hits = [f"{a}+{b}" for a, b in paired_steps(s, block).items()
                 if GEMM_SIGNATURE[a] in name and (tiles(a) + tiles(b)) * 512 == grid]
         return "/".join(hits)
@@ -198,36 +196,20 @@ def gemm_step_of(name, grid, s, block="parallel"):
     return "/".join(hits)
 
 
-def split_plan(M, N, K):
-    """(n_full, tail, splits) of a bf16 GEMM with a full workspace, as the
-    library plans it: 256 x 256 tiles, one workgroup per CU on 256 CUs; a
-    partial last wave is split along K to fill the chip, and a grid of fewer
-    tiles than CUs is split along K when the estimate (waves x K-steps, plus
-    3 + 1/16 per partial tile for the reduction) wins."""
-    tiles = -(-M // 256) * -(-N // 256)
-    n_full = tiles // 256 * 256
-    tail = tiles - n_full
-    nk = K // 64
-    if K % 64 or tail == 0:
-        return tiles, 0, 1
-    if n_full:
-        splits = min(256 // tail, nk)
-    else:
-        def cost(sp):
-            c = -(-tiles * sp // 256) * -(-nk // sp)
-            return c if sp == 1 else c + 3 + tiles * sp / 16
-        splits = 1
-        for sp in range(2, min(16, nk) + 1):
-            if cost(sp) < cost(splits):
-                splits = sp
-    return (n_full, tail, splits) if splits >= 2 else (tiles, 0, 1)
+def gemm_tiles(M, N, K):
+    """Output tiles of a bf16 GEMM (a shared launch has one workgroup per
+    tile of either GEMM)."""
+    from paper_2402_15627_amd import pblock as pb
+    return pb.pblock_gemm_plan(pb.PB_BF16, M, N, K).tiles
 
 
-def gemm_grid_threads(M, N, K):
-    """Work-items of a bf16 GEMM launch: 512 threads per workgroup, one per
-    whole tile and one per K-slice of each split tile."""
-    n_full, tail, splits = split_plan(M, N, K)
-    return (n_full + tail * splits) * 512
+def gemm_grid_threads(M, N, K, dtype="bf16"):
+    """Work-items of a GEMM's main launch as the library plans it (its host
+    query pblock_gemm_plan): one workgroup per whole tile and one per K-slice
+    of each split tile."""
+    from paper_2402_15627_amd import pblock as pb
+    p = pb.pblock_gemm_plan(pb.PB_BF16 if dtype == "bf16" else pb.PB_F32, M, N, K)
+    return p.workgroups * p.threads
 
 
 def traffic_path(step, workload):
@@ -262,7 +244,7 @@ def traffic_summary(dirs, workload, step):
     if any(p not in gemm_steps(s) for p in parts):
         raise SystemExit(f"traffic summary supports the GEMM steps and pairs, not {step}")
     if len(parts) == 2:
-        tiles = lambda st: -(-gemm_steps(s)[st][0] // 256) * -(-gemm_steps(s)[st][1] // 256)  # noqa: E731
+        tiles = lambda st: gemm_tiles(*gemm_steps(s)[st])  # noqa: E731
         grid = (tiles(parts[0]) + tiles(parts[1])) * 512
     else:
         grid = gemm_grid_threads(*gemm_steps(s)[step])
@@ -560,6 +542,7 @@ def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     rows = T // tp
     stream = torch.cuda.Stream()
     comm = [torch.cuda.Stream() for _ in range(n_comm)]
+    ctx = pb.TpContext(tp)
     out = {}
 
     def timed(per, in_place):
@@ -575,7 +558,7 @@ def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
 
         def call():
             pb.pblock_ag_in_proj(cfg, tp, 0, shards, h, dev["w_in"], dev["b_in"], z, c, per, ws,
-                                 stream, comm)
+                                 stream, comm, ctx)
         for _ in range(warmup):
             call()
         e0 = torch.cuda.Event(enable_timing=True)
@@ -592,6 +575,7 @@ def time_ag(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     out["copies_then_gemm_ms"] = timed(tp, False)
     for per in (1, 2, 4):
         out[f"pipelined_{per}_shards_per_launch_ms"] = timed(per, False)
+    ctx.close()
     return {"tp": tp, "n_comm": n_comm, "shard_bytes": rows * H * src.element_size(), **out}
 
 
@@ -611,6 +595,7 @@ def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     recv = torch.empty(tp, rows, H, dtype=act, device="cuda")
     stream = torch.cuda.Stream()
     comm = [torch.cuda.Stream() for _ in range(n_comm)]
+    ctx = pb.TpContext(tp)
     out = {}
 
     def timed(call):
@@ -634,7 +619,7 @@ def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
         dst = [partial[j * rows:(j + 1) * rows] if (in_place or j == 0) else recv[j]
                for j in range(tp)]
         return lambda: pb.pblock_rs_out_proj(cfg, tp, 0, c, dev["w_out"], partial, dst, per, ws,
-                                             stream, comm)
+                                             stream, comm, ctx)
 
     out["gemm_only_ms"] = timed(send(tp, True))
     out["gemm_then_copies_ms"] = timed(send(tp, False))
@@ -647,6 +632,7 @@ def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     nbytes = (tp + 2) * rows * H * partial.element_size()
     out["reduce_ms"] = ms
     out["reduce_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
+    ctx.close()
     return {"tp": tp, "n_comm": n_comm, "chunk_bytes": rows * H * partial.element_size(), **out}
 
 
@@ -774,9 +760,9 @@ def main():
     work = step_work(shape)
     names = pb.STEPS
 
-    def step():
-        blk.forward()
-        blk.backward()
+    def step(ev=None):
+        blk.forward(step_ev=ev)
+        blk.backward(step_ev=ev)
 
     for _ in range(args.warmup):
         step()
@@ -793,9 +779,7 @@ def main():
     eve = [[new_event() for _ in names] for _ in range(K)]
     torch.cuda.synchronize()
     for i in range(K):
-        pb.pblock_set_step_events([e.cuda_event for e in evb[i]], [e.cuda_event for e in eve[i]])
-        step()
-    pb.pblock_set_step_events(None, None)
+        step(pb.step_events([e.cuda_event for e in evb[i]], [e.cuda_event for e in eve[i]]))
     torch.cuda.synchronize()
     step_ms = {n: sum(evb[i][j].elapsed_time(eve[i][j]) for i in range(K)) / K
                for j, n in enumerate(names)}
@@ -813,16 +797,17 @@ def main():
     t_start, t_end = new_event(), new_event()
     torch.cuda.synchronize()
     t_start.record()
+    dom_ev = []
     for i in range(K):
         hb = [0] * len(names)
         he = [0] * len(names)
         hb[dj] = db[i].cuda_event
         he[dj] = de[i].cuda_event
-        pb.pblock_set_step_events(hb, he)
-        step()
+        dom_ev.append(pb.step_events(hb, he))
+    for i in range(K):
+        step(dom_ev[i])
     t_end.record()
     torch.cuda.synchronize()
-    pb.pblock_set_step_events(None, None)
     ms = t_start.elapsed_time(t_end) / K
     dom_ms = sum(db[i].elapsed_time(de[i]) for i in range(K)) / K
 

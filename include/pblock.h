@@ -54,12 +54,12 @@
  *
  * ---------------------------------------------------------------- ownership
  * The caller allocates every buffer (inputs, outputs, the stash, the
- * workspace).  The library allocates no device memory and keeps no per-call
- * state.  Two exceptions, both host-side: the pipelined all-gather and
- * reduce-scatter calls keep HIP events per device (created on their first
- * call and held until the process ends; calls of the same one of them must
- * not overlap on one device), and pblock_set_step_events keeps a
- * process-wide copy of the caller's event handles.  Every call is
+ * workspace).  The library allocates no device memory and keeps no state
+ * between calls: the HIP events that the pipelined all-gather and
+ * reduce-scatter order their streams with live in a pb_tp_context that the
+ * caller creates and destroys, and the step events of the *_timed calls are
+ * passed with each call.  (pblock_swattn_forward_noalloc alone uses a
+ * library-owned device array; see there.)  Every call is
  * asynchronous on the given HIP stream; buffers must stay valid until the
  * stream has passed the call.  Other calls on disjoint buffers may run
  * concurrently.  Parameter gradients are overwritten, not accumulated.
@@ -129,6 +129,37 @@ pb_status pblock_saved_offsets(const pb_config* cfg, size_t* offsets);
 enum { PB_WS_FORWARD_WITH_STASH = 0, PB_WS_BACKWARD = 1, PB_WS_FORWARD = 2 };
 size_t pblock_workspace_bytes(const pb_config* cfg, int mode);
 
+/* Steps of the forward and backward passes, for the *_timed calls. */
+typedef enum {
+  PB_STEP_LN_FWD = 0, /* LayerNorm of x                                     */
+  PB_STEP_IN_PROJ,    /* Z = h W_in^T + b_in, G = gelu(U)                   */
+  PB_STEP_ATTN_FWD,   /* sliding-window attention, O and lse                */
+  PB_STEP_OUT_PROJ,   /* y = x + C W_out^T + b_out                          */
+  PB_STEP_DC,         /* dC = dy W_out; dU = dC_mlp * gelu'(U)              */
+  PB_STEP_DW_OUT,     /* dW_out = dy^T C                                    */
+  PB_STEP_DB_OUT,     /* empty: db_out is summed with dgamma and dbeta in
+                         the LN backward step's column sums              */
+  PB_STEP_ATTN_BWD,   /* dQ, dK, dV                                         */
+  PB_STEP_DH,         /* dh = dZ W_in                                       */
+  PB_STEP_DW_IN,      /* dW_in = dZ^T h                                     */
+  PB_STEP_DB_IN,      /* db_in = sum over tokens of dZ                      */
+  PB_STEP_LN_BWD,     /* dx = dy + LN backward; dgamma, dbeta, db_out       */
+  PB_STEP_COUNT
+} pb_step;
+
+/* Per-call step events (benchmarking).  pblock_forward_timed and
+ * pblock_backward_timed record begin[i] on their stream just before the
+ * launches of step i and end[i] just after them; NULL entries, and a NULL
+ * pb_step_events, are skipped.  The events belong to the caller and are
+ * only recorded, never waited on.  A step whose work shares a launch with
+ * another step records nothing between its events (PB_STEP_DW_OUT and
+ * PB_STEP_DW_IN when pblock_backward_pairs reports the pair; PB_STEP_DB_OUT
+ * always). */
+typedef struct {
+  hipEvent_t begin[PB_STEP_COUNT];
+  hipEvent_t end[PB_STEP_COUNT];
+} pb_step_events;
+
 /* Forward pass of the block (Eq. 2).  Writes y [T, H].  When saved is not
  * NULL it also fills the stash that pblock_backward reads, and ws (NULL or
  * up to pblock_workspace_bytes(cfg, PB_WS_FORWARD) bytes) only holds GEMM
@@ -141,6 +172,14 @@ pb_status pblock_forward(const pb_config* cfg, const void* x,
                          const void* w_out, const void* b_out,
                          void* y, void* saved, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+/* pblock_forward, recording step_ev (NULL: none) around each step. */
+pb_status pblock_forward_timed(const pb_config* cfg, const void* x,
+                               const void* ln_gamma, const void* ln_beta,
+                               const void* w_in, const void* b_in,
+                               const void* w_out, const void* b_out,
+                               void* y, void* saved, void* ws,
+                               size_t ws_bytes, hipStream_t stream,
+                               const pb_step_events* step_ev);
 
 /* Byte offsets, within the backward workspace, of the intermediates that
  * pblock_backward leaves there, in the order:
@@ -166,6 +205,44 @@ pb_status pblock_backward(const pb_config* cfg, const void* x,
                           float* dgamma, float* dbeta, float* dw_in,
                           float* db_in, float* dw_out, float* db_out,
                           void* ws, size_t ws_bytes, hipStream_t stream);
+/* pblock_backward, recording step_ev (NULL: none) around each step. */
+pb_status pblock_backward_timed(const pb_config* cfg, const void* x,
+                                const void* ln_gamma, const void* ln_beta,
+                                const void* w_in, const void* b_in,
+                                const void* w_out, const void* b_out,
+                                const void* saved, const void* dy, void* dx,
+                                float* dgamma, float* dbeta, float* dw_in,
+                                float* db_in, float* dw_out, float* db_out,
+                                void* ws, size_t ws_bytes, hipStream_t stream,
+                                const pb_step_events* step_ev);
+
+/* ------------------------------------------------------- launch planning
+ * Host-only queries of how the calls above launch their GEMMs (for
+ * benchmarks and profilers that attribute kernel time to steps).  They make
+ * no HIP call.
+ *
+ * pblock_gemm_plan: the launch of one GEMM C[M, N] = A[M, K] B[K, N] in
+ * dtype, given a full GEMM workspace (as the block's calls have).  256 x 256
+ * output tiles; when the last wave of tiles is partial (or the whole grid is
+ * smaller than the 256 compute units), each of its `tail` tiles is split
+ * into `splits` K-slices whose fp32 partial tiles a second kernel sums.
+ * Fills tiles, n_full (tiles computed whole), tail, splits (1: no split),
+ * workgroups (of the GEMM kernel: n_full + tail * splits) and threads (per
+ * workgroup).  bf16 with K % 64 == 0 takes the matrix-core path that splits;
+ * anything else launches unsplit (the fp32 path's tiles are 64 x 64).
+ *
+ * pblock_backward_pairs: which backward GEMMs share one launch with the
+ * weight-gradient GEMM after them (1) or launch alone (0).  block 0, the
+ * parallel block: paired[0] = dC with dW_out, paired[1] = dh with dW_in.
+ * block 1, the serial block: paired[0..3] = dG with dW_down, dh2 with
+ * dW_up, dO with dW_o, dh1 with dW_qkv.  A shared launch has
+ * tiles(first) + tiles(second) workgroups. */
+typedef struct {
+  int tiles, n_full, tail, splits, workgroups, threads;
+} pb_gemm_plan;
+pb_status pblock_gemm_plan(pb_dtype dtype, int M, int N, int K,
+                           pb_gemm_plan* plan);
+pb_status pblock_backward_pairs(const pb_config* cfg, int block, int* paired);
 
 /* ---------------------------------------------------------- serial block
  * The standard pre-LN block that Eq. 2 replaces (Section 3.1, Eq. 1), for
@@ -270,6 +347,22 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
                                  void* dk, void* dv, int ld_dqkv, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------ tensor-parallel context
+ * The HIP events with which pblock_ag_in_proj and pblock_rs_out_proj order
+ * their copy streams against the GEMM stream: 3 tp + 1 events, created by
+ * pblock_tp_context_create on the device current at that call, with timing
+ * disabled.  A context serves calls with the same tp on that device, one
+ * after another (re-recording an event between calls is safe: a stream
+ * that waits on it has already taken the earlier state); calls from several
+ * host threads need one context each.  pblock_tp_context_destroy may be
+ * called once the calls that used it have been issued (HIP keeps a recorded
+ * event alive until its work has passed); NULL is ignored.
+ * Errors: PB_ERR_INVALID_ARG for tp outside 1..64 or ctx NULL, PB_ERR_HIP
+ * when an event cannot be created (nothing is left allocated). */
+typedef struct pb_tp_context pb_tp_context;
+pb_status pblock_tp_context_create(int tp, pb_tp_context** ctx);
+void pblock_tp_context_destroy(pb_tp_context* ctx);
+
 /* ------------------------------------------- in-projection + all-gather
  * Section 3.2 ("Overlapping in tensor/sequence parallelism", Fig. 3):
  * under sequence parallelism the LayerNorm output h is sharded along the
@@ -298,10 +391,9 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q,
  *   from each other and from `stream`.
  * ws: optional GEMM split region of pblock_ag_in_proj_workspace_bytes(cfg,
  *   tp, shards_per_launch) bytes (NULL/0 runs every launch unsplit).
+ * ctx: a pb_tp_context made for this tp on the current device.
  * The copies start after the work already on `stream`; later work on
- *   `stream` follows every copy and GEMM.  The library keeps 65 HIP events
- *   per device for this call (created on first use): calls on one device
- *   must not run concurrently from several host threads. */
+ *   `stream` follows every copy and GEMM. */
 size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp,
                                          int shards_per_launch);
 pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
@@ -309,7 +401,8 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
                             const void* w_in, const void* b_in, void* z,
                             void* c, int shards_per_launch, void* ws,
                             size_t ws_bytes, hipStream_t stream, int n_comm,
-                            const hipStream_t* comm_streams);
+                            const hipStream_t* comm_streams,
+                            pb_tp_context* ctx);
 
 /* --------------------------------------- out-projection + reduce-scatter
  * Section 3.2 ("Overlapping in tensor/sequence parallelism", Fig. 3), the
@@ -334,10 +427,8 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
  *     + j (T / tp) H) is not copied.
  *   Requirements as for pblock_ag_in_proj; ws: optional GEMM split region
  *   of pblock_rs_out_proj_workspace_bytes(cfg, tp, shards_per_launch)
- *   bytes (NULL/0 runs every launch unsplit).  Later work on `stream`
- *   follows every GEMM and copy.  The library keeps 128 HIP events per
- *   device for this call (created on first use): calls on one device must
- *   not run concurrently from several host threads.
+ *   bytes (NULL/0 runs every launch unsplit); ctx as for pblock_ag_in_proj.
+ *   Later work on `stream` follows every GEMM and copy.
  *
  * pblock_rs_reduce (the receiving side of one rank): y_shard = x_shard +
  * b_out + sum over q = 0 .. tp-1 of parts[q], summed in fp32 in the order
@@ -351,7 +442,8 @@ pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank,
                              const void* c, const void* w_out, void* partial,
                              void* const* dst, int shards_per_launch, void* ws,
                              size_t ws_bytes, hipStream_t stream, int n_comm,
-                             const hipStream_t* comm_streams);
+                             const hipStream_t* comm_streams,
+                             pb_tp_context* ctx);
 pb_status pblock_rs_reduce(const pb_config* cfg, int tp,
                            const void* const* parts, const void* x_shard,
                            const void* b_out, void* y_shard,
@@ -410,31 +502,6 @@ pb_status pblock_lamb_step(const pb_lamb_config* cfg, int n_tensors,
                            float* trust_ratio, void* ws, size_t ws_bytes,
                            hipStream_t stream);
 
-/* Steps of the forward and backward passes, for pblock_set_step_events. */
-typedef enum {
-  PB_STEP_LN_FWD = 0, /* LayerNorm of x                                     */
-  PB_STEP_IN_PROJ,    /* Z = h W_in^T + b_in, G = gelu(U)                   */
-  PB_STEP_ATTN_FWD,   /* sliding-window attention, O and lse                */
-  PB_STEP_OUT_PROJ,   /* y = x + C W_out^T + b_out                          */
-  PB_STEP_DC,         /* dC = dy W_out; dU = dC_mlp * gelu'(U)              */
-  PB_STEP_DW_OUT,     /* dW_out = dy^T C                                    */
-  PB_STEP_DB_OUT,     /* empty: db_out is summed with dgamma and dbeta in
-                         the LN backward step's column sums              */
-  PB_STEP_ATTN_BWD,   /* dQ, dK, dV                                         */
-  PB_STEP_DH,         /* dh = dZ W_in                                       */
-  PB_STEP_DW_IN,      /* dW_in = dZ^T h                                     */
-  PB_STEP_DB_IN,      /* db_in = sum over tokens of dZ                      */
-  PB_STEP_LN_BWD,     /* dx = dy + LN backward; dgamma, dbeta, db_out       */
-  PB_STEP_COUNT
-} pb_step;
-
-/* Benchmark hook.  With begin and end not NULL, later pblock_forward and
- * pblock_backward calls record begin[i] on their stream just before the
- * launches of step i and end[i] just after them (NULL entries are skipped).
- * Both arrays hold PB_STEP_COUNT events and are copied; the events belong to
- * the caller.  pblock_set_step_events(NULL, NULL) turns recording off.  The
- * setting is process-wide and not thread-safe.  Host only. */
-pb_status pblock_set_step_events(const hipEvent_t* begin, const hipEvent_t* end);
 
 /* Human-readable name of a status, and a description of the most recent
  * failed check on the calling thread ("" if none). */

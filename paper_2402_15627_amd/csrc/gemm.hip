@@ -1001,6 +1001,22 @@ size_t gemm_split_floats(const SplitPlan& p) {
   return (size_t)p.tail * p.splits * kBM * kBN;
 }
 
+GemmLaunch gemm_launch_of(Dt dt, int M, int N, int K) {
+  GemmLaunch g;
+  if (dt == Dt::BF16) {
+    g.tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+    g.plan = gemm_split_plan(dt, M, N, K);
+    g.workgroups = g.plan.n_full + g.plan.tail * g.plan.splits;
+    g.threads = kThreads;
+  } else {
+    g.tiles = ((M + kSB - 1) / kSB) * ((N + kSB - 1) / kSB);
+    g.plan = SplitPlan{g.tiles, 0, 1};
+    g.workgroups = g.tiles;
+    g.threads = 256;
+  }
+  return g;
+}
+
 bool gemm_pair_supported(Dt dt, const GemmSpec& g1, const GemmSpec& g2) {
   if (dt != Dt::BF16) return false;
   for (const GemmSpec* g : {&g1, &g2})

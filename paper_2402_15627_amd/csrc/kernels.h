@@ -129,6 +129,15 @@ struct SplitPlan {
 };
 SplitPlan gemm_split_plan(Dt dt, int M, int N, int K);
 size_t gemm_split_floats(const SplitPlan& p);
+// The launch of one GEMM given a full split workspace, as launch_gemm makes
+// it for operands whose LDS-DMA offsets fit 32 bits: output tiles, the tail
+// split, and the main kernel's grid.
+struct GemmLaunch {
+  int tiles;
+  SplitPlan plan;
+  int workgroups, threads;
+};
+GemmLaunch gemm_launch_of(Dt dt, int M, int N, int K);
 // split_ws may be NULL (or too small): the GEMM then runs unsplit.
 void launch_gemm(Dt dt, Epi epi, bool a_kcontig, bool b_kcontig, const void* A, int lda,
                  const void* B, int ldb, int M, int N, int K, const EpiArgs& ep, float* split_ws,

@@ -12,6 +12,7 @@
 #include <atomic>
 #include <initializer_list>
 #include <mutex>
+#include <new>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -30,19 +31,17 @@ pb_status fail(pb_status st, const char* fmt, ...) {
   return st;
 }
 
-// Step events of the benchmark hook (pblock_set_step_events).
-bool g_ev_on = false;
-hipEvent_t g_ev_begin[PB_STEP_COUNT];
-hipEvent_t g_ev_end[PB_STEP_COUNT];
-
+// Records the caller's step events (the *_timed entry points) around the
+// launches of one step; ev may be NULL.
 struct StepScope {
+  const pb_step_events* ev;
   int step;
   hipStream_t s;
-  StepScope(pb_step st, hipStream_t stream) : step(st), s(stream) {
-    if (g_ev_on && g_ev_begin[step]) hipEventRecord(g_ev_begin[step], s);
+  StepScope(const pb_step_events* e, pb_step st, hipStream_t stream) : ev(e), step(st), s(stream) {
+    if (ev && ev->begin[step]) (void)hipEventRecord(ev->begin[step], s);
   }
   ~StepScope() {
-    if (g_ev_on && g_ev_end[step]) hipEventRecord(g_ev_end[step], s);
+    if (ev && ev->end[step]) (void)hipEventRecord(ev->end[step], s);
   }
 };
 
@@ -359,6 +358,15 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
                          const void* ln_beta, const void* w_in, const void* b_in,
                          const void* w_out, const void* b_out, void* y, void* saved, void* ws,
                          size_t ws_bytes, hipStream_t stream) {
+  return pblock_forward_timed(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, y, saved, ws,
+                              ws_bytes, stream, nullptr);
+}
+
+pb_status pblock_forward_timed(const pb_config* cfg, const void* x, const void* ln_gamma,
+                               const void* ln_beta, const void* w_in, const void* b_in,
+                               const void* w_out, const void* b_out, void* y, void* saved,
+                               void* ws, size_t ws_bytes, hipStream_t stream,
+                               const pb_step_events* step_ev) {
   PB_CHECK(check_config(cfg));
   PB_CHECK(check_ptr(x, "x"));
   PB_CHECK(check_ptr(ln_gamma, "ln_gamma"));
@@ -400,7 +408,7 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
 
   // F1: shared LayerNorm
   {
-    StepScope sc(PB_STEP_LN_FWD, stream);
+    StepScope sc(step_ev, PB_STEP_LN_FWD, stream);
     pb::launch_ln_forward(dt, x, ln_gamma, ln_beta, h, mean, rstd, T, H, cfg->ln_eps, stream);
   }
   // F2: Z = h W_in^T + b_in (Q | K | V | U); G = gelu(U) -> C[:, A:]
@@ -414,13 +422,13 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   e1.col2 = A;
   e1.gelu_tanh = cfg->gelu_tanh;
   {
-    StepScope sc(PB_STEP_IN_PROJ, stream);
+    StepScope sc(step_ev, PB_STEP_IN_PROJ, stream);
     pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, h, H, w_in, H, T, N_in, H, e1, split_ws,
                     split_f, stream);
   }
   // F3: sliding-window attention, O -> C[:, :A]
   {
-    StepScope sc(PB_STEP_ATTN_FWD, stream);
+    StepScope sc(step_ev, PB_STEP_ATTN_FWD, stream);
     pb::launch_attn_forward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
                             lse, split_base, split_bytes, stream);
   }
@@ -431,11 +439,110 @@ pb_status pblock_forward(const pb_config* cfg, const void* x, const void* ln_gam
   e2.bias = b_out;
   e2.resid = x;
   {
-    StepScope sc(PB_STEP_OUT_PROJ, stream);
+    StepScope sc(step_ev, PB_STEP_OUT_PROJ, stream);
     pb::launch_gemm(dt, pb::Epi::BiasResid, true, true, c, K_out, w_out, K_out, T, H, K_out, e2,
                     split_ws, split_f, stream);
   }
   return finish_launches();
+}
+
+namespace {
+// The GEMMs of the backward passes that may share a launch, built in one
+// place for the launches and for pblock_backward_pairs, so that the query
+// reports the pairing the launches make.  Null operands and default epilogue
+// arguments describe the shapes alone.
+struct ParallelBwdGemms {
+  pb::GemmSpec dc, dw_out, dh, dw_in;
+};
+ParallelBwdGemms parallel_bwd_gemms(const Dims& d, const void* dy, const void* w_out,
+                                    const void* c, const void* dz, const void* w_in,
+                                    const void* h, const pb::EpiArgs& e_dc,
+                                    const pb::EpiArgs& e_dwo, const pb::EpiArgs& e_dh,
+                                    const pb::EpiArgs& e_dwi) {
+  const int T = (int)d.T, H = (int)d.H, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  return {
+      // dC = dy W_out (B MN-contiguous)
+      {pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e_dc},
+      // dW_out = dy^T C (contraction over tokens)
+      {pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e_dwo},
+      // dh = dZ W_in
+      {pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e_dh},
+      // dW_in = dZ^T h
+      {pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e_dwi}};
+}
+
+struct SerialBwdGemms {
+  pb::GemmSpec dg, dw_down, dh2, dw_up, d_o, dw_o, dh1, dw_qkv;
+};
+struct SerialBwdOperands {
+  const void *dy, *dx1, *c, *dz, *h1, *h2, *w_in, *w_out;
+};
+SerialBwdGemms serial_bwd_gemms(const Dims& d, const SerialBwdOperands& o,
+                                const pb::EpiArgs& e_dg, const pb::EpiArgs& e_wd,
+                                const pb::EpiArgs& e_dh2, const pb::EpiArgs& e_wu,
+                                const pb::EpiArgs& e_do, const pb::EpiArgs& e_wo,
+                                const pb::EpiArgs& e_dh1, const pb::EpiArgs& e_wq) {
+  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, F = (int)d.F, N_in = (int)d.N_in,
+            K_out = (int)d.K_out;
+  const size_t e = d.esz;
+  auto off = [&](const void* p, long long n) { return p ? at(p, n, e) : nullptr; };
+  return {
+      // dG = dy W_down
+      {pb::Epi::DgeluSplit, true, false, o.dy, H, off(o.w_out, A), K_out, T, F, H, e_dg},
+      // dW_down = dy^T G
+      {pb::Epi::StoreF32, false, false, o.dy, H, off(o.c, A), K_out, H, F, T, e_wd},
+      // dh2 = dU W_up
+      {pb::Epi::LnGrad, true, false, off(o.dz, 3LL * A), N_in, off(o.w_in, 3LL * A * H), H, T, H,
+       F, e_dh2},
+      // dW_up = dU^T h2
+      {pb::Epi::StoreF32, false, false, off(o.dz, 3LL * A), N_in, o.h2, H, F, H, T, e_wu},
+      // dO = dx1 W_o
+      {pb::Epi::DgeluSplit, true, false, o.dx1, H, o.w_out, K_out, T, A, H, e_do},
+      // dW_o = dx1^T O
+      {pb::Epi::StoreF32, false, false, o.dx1, H, o.c, K_out, H, A, T, e_wo},
+      // dh1 = dQKV W_qkv
+      {pb::Epi::LnGrad, true, false, o.dz, N_in, o.w_in, H, T, H, 3 * A, e_dh1},
+      // dW_qkv = dQKV^T h1
+      {pb::Epi::StoreF32, false, false, o.dz, N_in, o.h1, H, 3 * A, H, T, e_wq}};
+}
+}  // namespace
+
+pb_status pblock_gemm_plan(pb_dtype dtype, int M, int N, int K, pb_gemm_plan* plan) {
+  if (!plan) return fail(PB_ERR_INVALID_ARG, "plan is NULL");
+  if (dtype != PB_BF16 && dtype != PB_F32) return fail(PB_ERR_INVALID_ARG, "unknown dtype");
+  if (M < 1 || N < 1 || K < 1) return fail(PB_ERR_INVALID_ARG, "M, N, K must be >= 1");
+  const pb::Dt dt = dtype == PB_BF16 ? pb::Dt::BF16 : pb::Dt::F32;
+  const pb::GemmLaunch g = pb::gemm_launch_of(dt, M, N, K);
+  plan->tiles = g.tiles;
+  plan->n_full = g.plan.n_full;
+  plan->tail = g.plan.tail;
+  plan->splits = g.plan.splits;
+  plan->workgroups = g.workgroups;
+  plan->threads = g.threads;
+  return PB_OK;
+}
+
+pb_status pblock_backward_pairs(const pb_config* cfg, int block, int* paired) {
+  PB_CHECK(check_config(cfg));
+  if (!paired) return fail(PB_ERR_INVALID_ARG, "paired is NULL");
+  if (block != 0 && block != 1) return fail(PB_ERR_INVALID_ARG, "block=%d must be 0 or 1", block);
+  const Dims d = dims_of(cfg);
+  const pb::Dt dt = dt_of(cfg);
+  const pb::EpiArgs none;
+  if (block == 0) {
+    const ParallelBwdGemms g = parallel_bwd_gemms(d, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                                  nullptr, none, none, none, none);
+    paired[0] = pb::gemm_pair_supported(dt, g.dc, g.dw_out);
+    paired[1] = pb::gemm_pair_supported(dt, g.dh, g.dw_in);
+  } else {
+    const SerialBwdGemms g =
+        serial_bwd_gemms(d, SerialBwdOperands{}, none, none, none, none, none, none, none, none);
+    paired[0] = pb::gemm_pair_supported(dt, g.dg, g.dw_down);
+    paired[1] = pb::gemm_pair_supported(dt, g.dh2, g.dw_up);
+    paired[2] = pb::gemm_pair_supported(dt, g.d_o, g.dw_o);
+    paired[3] = pb::gemm_pair_supported(dt, g.dh1, g.dw_qkv);
+  }
+  return PB_OK;
 }
 
 pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_gamma,
@@ -444,6 +551,18 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
                           const void* dy, void* dx, float* dgamma, float* dbeta, float* dw_in,
                           float* db_in, float* dw_out, float* db_out, void* ws, size_t ws_bytes,
                           hipStream_t stream) {
+  return pblock_backward_timed(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, saved, dy, dx,
+                               dgamma, dbeta, dw_in, db_in, dw_out, db_out, ws, ws_bytes, stream,
+                               nullptr);
+}
+
+pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void* ln_gamma,
+                                const void* ln_beta, const void* w_in, const void* b_in,
+                                const void* w_out, const void* b_out, const void* saved,
+                                const void* dy, void* dx, float* dgamma, float* dbeta,
+                                float* dw_in, float* db_in, float* dw_out, float* db_out, void* ws,
+                                size_t ws_bytes, hipStream_t stream,
+                                const pb_step_events* step_ev) {
   PB_CHECK(check_config(cfg));
   PB_CHECK(check_ptr(x, "x"));
   PB_CHECK(check_ptr(ln_gamma, "ln_gamma"));
@@ -516,28 +635,7 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   e1.split = A;
   e1.col2 = 3 * A;
   e1.gelu_tanh = cfg->gelu_tanh;
-  const pb::GemmSpec g_dc{pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1};
-  const pb::GemmSpec g_dwo{pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2};
-  const bool pair_out = pb::gemm_pair_supported(dt, g_dc, g_dwo);
-  {
-    StepScope sc(PB_STEP_DC, stream);  // with dW_out when they share a launch
-    if (pair_out)
-      pb::launch_gemm_pair(dt, g_dc, g_dwo, stream);
-    else
-      pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, dy, H, w_out, K_out, T, K_out, H, e1,
-                      split_ws, split_f, stream);
-  }
-  // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
-  {
-    StepScope sc(PB_STEP_ATTN_BWD, stream);
-    pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
-                             K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
-                             N_in, split_ws, split_f * 4, stream);
-  }
-  // B4: dh = dZ W_in, stored in the activation type; its epilogue also forms
-  // the LayerNorm backward's row terms (sums of gamma dh and gamma dh xhat per
-  // 64 columns) from the fp32 accumulators
-  pb::EpiArgs e4;
+  pb::EpiArgs e4;  // B4 (below): dh = dZ W_in with the LayerNorm backward's row terms
   e4.out = dh;
   e4.ld_out = H;
   e4.aux = x;
@@ -546,20 +644,41 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
   e4.rstd = rstd;
   e4.rowpart = rowpart;
   e4.rowpart_ld = pb::ln_row_groups(H);
-  const pb::GemmSpec g_dh{pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e4};
-  const pb::GemmSpec g_dwi{pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5};
+  const ParallelBwdGemms G = parallel_bwd_gemms(d, dy, w_out, c, dz, w_in, h, e1, e2, e4, e5);
+  const pb::GemmSpec &g_dc = G.dc, &g_dwo = G.dw_out, &g_dh = G.dh, &g_dwi = G.dw_in;
+  auto run = [&](const pb::GemmSpec& g) {
+    pb::launch_gemm(dt, g.epi, g.a_kcontig, g.b_kcontig, g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K,
+                    g.ep, split_ws, split_f, stream);
+  };
+  const bool pair_out = pb::gemm_pair_supported(dt, g_dc, g_dwo);
+  {
+    StepScope sc(step_ev, PB_STEP_DC, stream);  // with dW_out when they share a launch
+    if (pair_out)
+      pb::launch_gemm_pair(dt, g_dc, g_dwo, stream);
+    else
+      run(g_dc);
+  }
+  // B3: attention backward -> dQ, dK, dV into dZ[:, :3A]
+  {
+    StepScope sc(step_ev, PB_STEP_ATTN_BWD, stream);
+    pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
+                             K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
+                             N_in, split_ws, split_f * 4, stream);
+  }
+  // B4: dh = dZ W_in, stored in the activation type; its epilogue also forms
+  // the LayerNorm backward's row terms (sums of gamma dh and gamma dh xhat per
+  // 64 columns) from the fp32 accumulators
   const bool pair_in = pb::gemm_pair_supported(dt, g_dh, g_dwi);
   {
-    StepScope sc(PB_STEP_DH, stream);  // with dW_in when they share a launch
+    StepScope sc(step_ev, PB_STEP_DH, stream);  // with dW_in when they share a launch
     if (pair_in)
       pb::launch_gemm_pair(dt, g_dh, g_dwi, stream);
     else
-      pb::launch_gemm(dt, pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, N_in, e4,
-                      split_ws, split_f, stream);
+      run(g_dh);
   }
   // B6: LN backward plus the residual path: dx = dy + LN'(dh); dgamma, dbeta
   {
-    StepScope sc(PB_STEP_LN_BWD, stream);
+    StepScope sc(step_ev, PB_STEP_LN_BWD, stream);
     pb::launch_ln_backward(dt, x, mean, rstd, ln_gamma, dh, rowpart, dy, dx, pdg, pdb, pdy, T, H,
                            stream);
     // dgamma, dbeta and db_out (= sum over tokens of dy) from the LN
@@ -568,24 +687,22 @@ pb_status pblock_backward(const pb_config* cfg, const void* x, const void* ln_ga
                            stream);
   }
   {
-    StepScope sc(PB_STEP_DB_OUT, stream);  // now inside the LN backward's column sums
+    StepScope sc(step_ev, PB_STEP_DB_OUT, stream);  // now inside the LN backward's column sums
   }
   // db_in = sum over tokens of dZ
   {
-    StepScope sc(PB_STEP_DB_IN, stream);
+    StepScope sc(step_ev, PB_STEP_DB_IN, stream);
     pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
   }
   {
-    StepScope sc(PB_STEP_DW_OUT, stream);  // empty when it shared dC's launch
+    StepScope sc(step_ev, PB_STEP_DW_OUT, stream);  // empty when it shared dC's launch
     if (!pair_out)
-      pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dy, H, c, K_out, H, K_out, T, e2,
-                      split_ws, split_f, stream);
+      run(g_dwo);
   }
   {
-    StepScope sc(PB_STEP_DW_IN, stream);  // empty when it shared dh's launch
+    StepScope sc(step_ev, PB_STEP_DW_IN, stream);  // empty when it shared dh's launch
     if (!pair_in)
-      pb::launch_gemm(dt, pb::Epi::StoreF32, false, false, dz, N_in, h, H, N_in, H, T, e5,
-                      split_ws, split_f, stream);
+      run(g_dwi);
   }
   return finish_launches();
 }
@@ -945,11 +1062,44 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   wu.ld_out = H;
   wq.out = dw_in;  // dW_qkv = dQKV^T h1
   wq.ld_out = H;
-  const pb::GemmSpec g_wd{pb::Epi::StoreF32, false, false, dy, H, at(c, A, e), K_out, H, F, T, wd};
-  const pb::GemmSpec g_wo{pb::Epi::StoreF32, false, false, dx1, H, c, K_out, H, A, T, wo};
-  const pb::GemmSpec g_wu{pb::Epi::StoreF32, false, false, at(dz, 3LL * A, e), N_in, h2, H, F, H,
-                          T, wu};
-  const pb::GemmSpec g_wq{pb::Epi::StoreF32, false, false, dz, N_in, h1, H, 3 * A, H, T, wq};
+  // dG = dy W_down, dU = dG * gelu'(U) -> dZ[:, 3A:]
+  pb::EpiArgs e1;
+  e1.out = dz;
+  e1.ld_out = N_in;
+  e1.out2 = dz;
+  e1.ld_out2 = N_in;
+  e1.aux = z;
+  e1.split = 0;
+  e1.col2 = 3 * A;
+  e1.gelu_tanh = cfg->gelu_tanh;
+  // dh2 = dU W_up, with LN2's row terms
+  pb::EpiArgs e2;
+  e2.out = dh;
+  e2.ld_out = H;
+  e2.aux = x1;
+  e2.bias = ln2_gamma;
+  e2.mean = mean2;
+  e2.rstd = rstd2;
+  e2.rowpart = rowpart;
+  e2.rowpart_ld = pb::ln_row_groups(H);
+  // dO = dx1 W_o
+  pb::EpiArgs e3;
+  e3.out = d_o;
+  e3.ld_out = A;
+  e3.split = A;  // every column is dO
+  e3.gelu_tanh = cfg->gelu_tanh;
+  // dh1 = dQKV W_qkv, with LN1's row terms
+  pb::EpiArgs e4;
+  e4.out = dh;
+  e4.ld_out = H;
+  e4.aux = x;
+  e4.bias = ln1_gamma;
+  e4.mean = mean1;
+  e4.rstd = rstd1;
+  e4.rowpart = rowpart;
+  e4.rowpart_ld = pb::ln_row_groups(H);
+  const SerialBwdGemms G = serial_bwd_gemms(
+      d, SerialBwdOperands{dy, dx1, c, dz, h1, h2, w_in, w_out}, e1, wd, e2, wu, e3, wo, e4, wq);
   auto run = [&](const pb::GemmSpec& g) {
     pb::launch_gemm(dt, g.epi, g.a_kcontig, g.b_kcontig, g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K,
                     g.ep, split_ws, split_f, stream);
@@ -963,58 +1113,19 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
     }
   };
 
-  // MLP: dG = dy W_down, dU = dG * gelu'(U) -> dZ[:, 3A:]
-  pb::EpiArgs e1;
-  e1.out = dz;
-  e1.ld_out = N_in;
-  e1.out2 = dz;
-  e1.ld_out2 = N_in;
-  e1.aux = z;
-  e1.split = 0;
-  e1.col2 = 3 * A;
-  e1.gelu_tanh = cfg->gelu_tanh;
-  run_with(pb::GemmSpec{pb::Epi::DgeluSplit, true, false, dy, H, at(w_out, A, e), K_out, T, F, H,
-                        e1},
-           g_wd);
-  // dh2 = dU W_up, with LN2's row terms
-  pb::EpiArgs e2;
-  e2.out = dh;
-  e2.ld_out = H;
-  e2.aux = x1;
-  e2.bias = ln2_gamma;
-  e2.mean = mean2;
-  e2.rstd = rstd2;
-  e2.rowpart = rowpart;
-  e2.rowpart_ld = pb::ln_row_groups(H);
-  run_with(pb::GemmSpec{pb::Epi::LnGrad, true, false, at(dz, 3LL * A, e), N_in,
-                        at(w_in, 3LL * A * H, e), H, T, H, F, e2},
-           g_wu);
+  // MLP: dG and dU, then dh2
+  run_with(G.dg, G.dw_down);
+  run_with(G.dh2, G.dw_up);
   // dx1 = dy + LN2'(dh2); dgamma2, dbeta2, and db_down = sum dy
   pb::launch_ln_backward(dt, x1, mean2, rstd2, ln2_gamma, dh, rowpart, dy, dx1, pdg, pdb, pdy, T,
                          H, stream);
   pb::launch_colsum3_f32(pdg, pdb, pdy, H, nblk, H, dln2_gamma, dln2_beta, db_down, stream);
   // attention: dO = dx1 W_o, then dQ, dK, dV -> dZ[:, :3A]
-  pb::EpiArgs e3;
-  e3.out = d_o;
-  e3.ld_out = A;
-  e3.split = A;  // every column is dO
-  e3.gelu_tanh = cfg->gelu_tanh;
-  run_with(pb::GemmSpec{pb::Epi::DgeluSplit, true, false, dx1, H, w_out, K_out, T, A, H, e3},
-           g_wo);
+  run_with(G.d_o, G.dw_o);
   pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
                            d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in,
                            split_ws, split_f * 4, stream);
-  // dh1 = dQKV W_qkv, with LN1's row terms
-  pb::EpiArgs e4;
-  e4.out = dh;
-  e4.ld_out = H;
-  e4.aux = x;
-  e4.bias = ln1_gamma;
-  e4.mean = mean1;
-  e4.rstd = rstd1;
-  e4.rowpart = rowpart;
-  e4.rowpart_ld = pb::ln_row_groups(H);
-  run_with(pb::GemmSpec{pb::Epi::LnGrad, true, false, dz, N_in, w_in, H, T, H, 3 * A, e4}, g_wq);
+  run_with(G.dh1, G.dw_qkv);
   // dx = dx1 + LN1'(dh1); dgamma1, dbeta1, and db_o = sum dx1
   pb::launch_ln_backward(dt, x, mean1, rstd1, ln1_gamma, dh, rowpart, dx1, dx, pdg, pdb, pdy, T,
                          H, stream);
@@ -1026,18 +1137,64 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   return finish_launches();
 }
 
-// -------------------------------------------- in-projection + all-gather
+// -------------------------------------------- tensor-parallel context
 namespace {
 constexpr int kAgMaxComm = 8;
 constexpr int kAgMaxTp = 64;
-constexpr int kAgMaxDevices = 64;
-// Events of the fused call, per device, created on first use.
-struct AgEvents {
-  bool ready = false;
-  hipEvent_t start;
-  hipEvent_t landed[kAgMaxTp];
+}  // namespace
+
+// Events of the pipelined all-gather and reduce-scatter calls, tp of each
+// kind plus one, on one device.
+struct pb_tp_context {
+  int device;
+  int tp;
+  hipEvent_t start;             // AG: the work on `stream` before the copies
+  hipEvent_t landed[kAgMaxTp];  // AG: per position in the ring order
+  hipEvent_t computed[kAgMaxTp];// RS: per launch group, on `stream`
+  hipEvent_t sent[kAgMaxTp];    // RS: per chunk, on its comm stream
 };
-AgEvents g_ag[kAgMaxDevices];
+
+pb_status pblock_tp_context_create(int tp, pb_tp_context** ctx) {
+  if (!ctx) return fail(PB_ERR_INVALID_ARG, "ctx is NULL");
+  *ctx = nullptr;
+  if (tp < 1 || tp > kAgMaxTp) return fail(PB_ERR_INVALID_ARG, "tp=%d must be in 1..64", tp);
+  pb_tp_context* c = new (std::nothrow) pb_tp_context{};
+  if (!c) return fail(PB_ERR_INVALID_ARG, "out of host memory");
+  c->tp = tp;
+  bool ok = hipGetDevice(&c->device) == hipSuccess;
+  auto make = [&](hipEvent_t* ev) {
+    ok = ok && hipEventCreateWithFlags(ev, hipEventDisableTiming) == hipSuccess;
+  };
+  make(&c->start);
+  for (int i = 0; i < tp; ++i) {
+    make(&c->landed[i]);
+    make(&c->computed[i]);
+    make(&c->sent[i]);
+  }
+  if (!ok) {
+    pblock_tp_context_destroy(c);
+    return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
+  }
+  *ctx = c;
+  return PB_OK;
+}
+
+void pblock_tp_context_destroy(pb_tp_context* ctx) {
+  if (!ctx) return;
+  auto drop = [](hipEvent_t e) {
+    if (e) (void)hipEventDestroy(e);
+  };
+  drop(ctx->start);
+  for (int i = 0; i < ctx->tp; ++i) {
+    drop(ctx->landed[i]);
+    drop(ctx->computed[i]);
+    drop(ctx->sent[i]);
+  }
+  delete ctx;
+}
+
+// -------------------------------------------- in-projection + all-gather
+namespace {
 
 // Largest GEMM split region over the launches of one call: row ranges of
 // m whole shards, m = 1 .. per_launch.
@@ -1070,6 +1227,19 @@ pb_status check_tp_streams(int tp, int rank, long long T, int per_launch, int n_
   }
   return PB_OK;
 }
+// Checked after every other argument: the one check that asks HIP (for the
+// current device).
+pb_status check_ctx(const pb_tp_context* ctx, int tp) {
+  if (!ctx) return fail(PB_ERR_INVALID_ARG, "ctx is NULL");
+  if (ctx->tp != tp)
+    return fail(PB_ERR_INVALID_ARG, "ctx was made for tp=%d, called with tp=%d", ctx->tp, tp);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(PB_ERR_HIP, "hipGetDevice failed");
+  if (dev != ctx->device)
+    return fail(PB_ERR_INVALID_ARG, "ctx belongs to device %d, the current device is %d",
+                ctx->device, dev);
+  return PB_OK;
+}
 }  // namespace
 
 size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
@@ -1082,7 +1252,7 @@ size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp, int shard
 pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* const* shards,
                             void* h, const void* w_in, const void* b_in, void* z, void* c,
                             int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
-                            int n_comm, const hipStream_t* comm_streams) {
+                            int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
   PB_CHECK(check_config(cfg));
   const Dims d = dims_of(cfg);
   PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
@@ -1098,18 +1268,8 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
   PB_CHECK(check_ptr(c, "c"));
   if (ws_bytes && (!ws || (uintptr_t)ws % 256))
     return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kAgMaxDevices)
-    return fail(PB_ERR_HIP, "hipGetDevice failed");
-  AgEvents& ev = g_ag[dev];
-  if (!ev.ready) {
-    if (hipEventCreateWithFlags(&ev.start, hipEventDisableTiming) != hipSuccess)
-      return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
-    for (int i = 0; i < kAgMaxTp; ++i)
-      if (hipEventCreateWithFlags(&ev.landed[i], hipEventDisableTiming) != hipSuccess)
-        return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
-    ev.ready = true;
-  }
+  PB_CHECK(check_ctx(ctx, tp));
+  pb_tp_context& ev = *ctx;
   auto ok = [](hipError_t e) { return e == hipSuccess; };
 
   const pb::Dt dt = dt_of(cfg);
@@ -1185,14 +1345,6 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
 
 // --------------------------------------- out-projection + reduce-scatter
 namespace {
-// Events of the fused call, per device, created on first use.
-struct RsEvents {
-  bool ready = false;
-  hipEvent_t computed[kAgMaxTp];  // per launch group, on `stream`
-  hipEvent_t sent[kAgMaxTp];      // per chunk, on its comm stream
-};
-RsEvents g_rs[kAgMaxDevices];
-
 size_t rs_split_bytes(const pb_config* cfg, int tp, int per_launch) {
   const Dims d = dims_of(cfg);
   const int rows = (int)(d.T / tp);
@@ -1216,7 +1368,7 @@ size_t pblock_rs_out_proj_workspace_bytes(const pb_config* cfg, int tp, int shar
 pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank, const void* c,
                              const void* w_out, void* partial, void* const* dst,
                              int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
-                             int n_comm, const hipStream_t* comm_streams) {
+                             int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
   PB_CHECK(check_config(cfg));
   const Dims d = dims_of(cfg);
   PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
@@ -1230,17 +1382,8 @@ pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank, const void*
   PB_CHECK(check_ptr(partial, "partial"));
   if (ws_bytes && (!ws || (uintptr_t)ws % 256))
     return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kAgMaxDevices)
-    return fail(PB_ERR_HIP, "hipGetDevice failed");
-  RsEvents& ev = g_rs[dev];
-  if (!ev.ready) {
-    for (int i = 0; i < kAgMaxTp; ++i)
-      if (hipEventCreateWithFlags(&ev.computed[i], hipEventDisableTiming) != hipSuccess ||
-          hipEventCreateWithFlags(&ev.sent[i], hipEventDisableTiming) != hipSuccess)
-        return fail(PB_ERR_HIP, "hipEventCreateWithFlags failed");
-    ev.ready = true;
-  }
+  PB_CHECK(check_ctx(ctx, tp));
+  pb_tp_context& ev = *ctx;
   auto ok = [](hipError_t e) { return e == hipSuccess; };
 
   const pb::Dt dt = dt_of(cfg);
@@ -1408,18 +1551,6 @@ pb_status pblock_lamb_step(const pb_lamb_config* cfg, int n_tensors,
   return finish_launches();
 }
 
-pb_status pblock_set_step_events(const hipEvent_t* begin, const hipEvent_t* end) {
-  if (!begin || !end) {
-    g_ev_on = false;
-    return PB_OK;
-  }
-  for (int i = 0; i < PB_STEP_COUNT; ++i) {
-    g_ev_begin[i] = begin[i];
-    g_ev_end[i] = end[i];
-  }
-  g_ev_on = true;
-  return PB_OK;
-}
 
 const char* pblock_status_string(pb_status status) {
   switch (status) {

@@ -32,7 +32,9 @@ EXPORTS = (
     "pblock_validate", "pblock_saved_bytes", "pblock_saved_offsets", "pblock_workspace_bytes",
     "pblock_workspace_offsets",
     "pblock_forward", "pblock_backward", "pblock_swattn_forward",
-    "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_set_step_events",
+    "pblock_swattn_workspace_bytes", "pblock_swattn_backward", "pblock_forward_timed",
+    "pblock_backward_timed", "pblock_gemm_plan", "pblock_backward_pairs",
+    "pblock_tp_context_create", "pblock_tp_context_destroy",
     "pblock_status_string", "pblock_last_error", "pblock_serial_saved_bytes",
     "pblock_serial_saved_offsets", "pblock_serial_workspace_bytes", "pblock_serial_forward",
     "pblock_serial_backward", "pblock_lamb_workspace_bytes", "pblock_lamb_step",
@@ -52,6 +54,17 @@ class PbConfig(ctypes.Structure):
     _fields_ = [("batch", c_int), ("seq", c_int), ("hidden", c_int), ("heads", c_int),
                 ("head_dim", c_int), ("ffn", c_int), ("window", c_int), ("ln_eps", c_float),
                 ("gelu_tanh", c_int), ("dtype", c_int)]
+
+
+class StepEvents(ctypes.Structure):
+    """pb_step_events: raw hipEvent_t handles, NULL to skip a step."""
+    _fields_ = [("begin", c_void_p * len(STEPS)), ("end", c_void_p * len(STEPS))]
+
+
+class GemmPlan(ctypes.Structure):
+    """pb_gemm_plan."""
+    _fields_ = [("tiles", c_int), ("n_full", c_int), ("tail", c_int), ("splits", c_int),
+                ("workgroups", c_int), ("threads", c_int)]
 
 
 class LambConfig(ctypes.Structure):
@@ -101,7 +114,14 @@ def load_library(path: str = LIB_PATH):
         "pblock_swattn_forward_noalloc": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, P]),
         "pblock_swattn_backward": (c_int, [cfgp, P, P, P, c_int, P, c_int, P, c_int, P, P, P, P,
                                            c_int, P, c_size_t, P]),
-        "pblock_set_step_events": (c_int, [P, P]),
+        "pblock_forward_timed": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, c_size_t, P,
+                                         POINTER(StepEvents)]),
+        "pblock_backward_timed": (c_int, [cfgp, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P,
+                                          P, c_size_t, P, POINTER(StepEvents)]),
+        "pblock_gemm_plan": (c_int, [c_int, c_int, c_int, c_int, POINTER(GemmPlan)]),
+        "pblock_backward_pairs": (c_int, [cfgp, c_int, POINTER(c_int)]),
+        "pblock_tp_context_create": (c_int, [c_int, POINTER(c_void_p)]),
+        "pblock_tp_context_destroy": (None, [P]),
         "pblock_status_string": (ctypes.c_char_p, [c_int]),
         "pblock_last_error": (ctypes.c_char_p, []),
         "pblock_serial_saved_bytes": (c_size_t, [cfgp]),
@@ -112,10 +132,10 @@ def load_library(path: str = LIB_PATH):
         "pblock_lamb_workspace_bytes": (c_size_t, [c_int, POINTER(LambTensor)]),
         "pblock_ag_in_proj_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
         "pblock_ag_in_proj": (c_int, [cfgp, c_int, c_int, POINTER(c_void_p), P, P, P, P, P, c_int,
-                                      P, c_size_t, P, c_int, POINTER(c_void_p)]),
+                                      P, c_size_t, P, c_int, POINTER(c_void_p), P]),
         "pblock_rs_out_proj_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
         "pblock_rs_out_proj": (c_int, [cfgp, c_int, c_int, P, P, P, POINTER(c_void_p), c_int, P,
-                                       c_size_t, P, c_int, POINTER(c_void_p)]),
+                                       c_size_t, P, c_int, POINTER(c_void_p), P]),
         "pblock_rs_reduce": (c_int, [cfgp, c_int, POINTER(c_void_p), P, P, P, P]),
         "pblock_lamb_step": (c_int, [POINTER(LambConfig), c_int, POINTER(LambTensor), c_int, P, P,
                                      c_size_t, P]),
@@ -195,20 +215,86 @@ def pblock_workspace_offsets(cfg: PbConfig) -> dict:
     return dict(zip(WORKSPACE_REGIONS, list(arr)))
 
 
+def step_events(begin, end) -> StepEvents:
+    """A pb_step_events from two sequences of len(STEPS) raw hipEvent_t
+    handles (ints; 0 or None skips a step)."""
+    n = len(STEPS)
+    if len(begin) != n or len(end) != n:
+        raise ValueError(f"step events need {n} begin and {n} end handles")
+    ev = StepEvents()
+    for i in range(n):
+        ev.begin[i] = begin[i] or None
+        ev.end[i] = end[i] or None
+    return ev
+
+
 def pblock_forward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, y, saved=None, ws=None,
-                   stream=None):
-    _check(load_library().pblock_forward(
-        ctypes.byref(cfg), _ptr(x), _ptr(ln_gamma), _ptr(ln_beta), _ptr(w_in), _ptr(b_in),
-        _ptr(w_out), _ptr(b_out), _ptr(y), _ptr(saved), _ptr(ws), _nbytes(ws), _stream(stream)))
+                   stream=None, step_ev=None):
+    """step_ev: None, or a StepEvents (see step_events) recorded around each
+    step (pblock_forward_timed)."""
+    args = (ctypes.byref(cfg), _ptr(x), _ptr(ln_gamma), _ptr(ln_beta), _ptr(w_in), _ptr(b_in),
+            _ptr(w_out), _ptr(b_out), _ptr(y), _ptr(saved), _ptr(ws), _nbytes(ws),
+            _stream(stream))
+    lib = load_library()
+    if step_ev is None:
+        _check(lib.pblock_forward(*args))
+    else:
+        _check(lib.pblock_forward_timed(*args, ctypes.byref(step_ev)))
 
 
 def pblock_backward(cfg, x, ln_gamma, ln_beta, w_in, b_in, w_out, b_out, saved, dy, dx, dgamma,
-                    dbeta, dw_in, db_in, dw_out, db_out, ws, stream=None):
-    _check(load_library().pblock_backward(
-        ctypes.byref(cfg), _ptr(x), _ptr(ln_gamma), _ptr(ln_beta), _ptr(w_in), _ptr(b_in),
-        _ptr(w_out), _ptr(b_out), _ptr(saved), _ptr(dy), _ptr(dx), _ptr(dgamma), _ptr(dbeta),
-        _ptr(dw_in), _ptr(db_in), _ptr(dw_out), _ptr(db_out), _ptr(ws), _nbytes(ws),
-        _stream(stream)))
+                    dbeta, dw_in, db_in, dw_out, db_out, ws, stream=None, step_ev=None):
+    """step_ev as for pblock_forward (pblock_backward_timed)."""
+    args = (ctypes.byref(cfg), _ptr(x), _ptr(ln_gamma), _ptr(ln_beta), _ptr(w_in), _ptr(b_in),
+            _ptr(w_out), _ptr(b_out), _ptr(saved), _ptr(dy), _ptr(dx), _ptr(dgamma), _ptr(dbeta),
+            _ptr(dw_in), _ptr(db_in), _ptr(dw_out), _ptr(db_out), _ptr(ws), _nbytes(ws),
+            _stream(stream))
+    lib = load_library()
+    if step_ev is None:
+        _check(lib.pblock_backward(*args))
+    else:
+        _check(lib.pblock_backward_timed(*args, ctypes.byref(step_ev)))
+
+
+def pblock_gemm_plan(dtype: int, M: int, N: int, K: int) -> GemmPlan:
+    """The launch of one GEMM as the library makes it (host only)."""
+    plan = GemmPlan()
+    _check(load_library().pblock_gemm_plan(int(dtype), int(M), int(N), int(K),
+                                           ctypes.byref(plan)))
+    return plan
+
+
+def pblock_backward_pairs(cfg: PbConfig, block: str = "parallel") -> tuple:
+    """Which backward GEMMs share a launch with the weight gradient after them
+    (host only): parallel (dC+dW_out, dh+dW_in); serial (dG+dW_down,
+    dh2+dW_up, dO+dW_o, dh1+dW_qkv)."""
+    n = 2 if block == "parallel" else 4
+    out = (c_int * n)()
+    _check(load_library().pblock_backward_pairs(ctypes.byref(cfg), 0 if block == "parallel" else 1,
+                                                out))
+    return tuple(bool(v) for v in out)
+
+
+class TpContext:
+    """A pb_tp_context: the events of the pipelined all-gather and
+    reduce-scatter calls for one tp on the current device."""
+
+    def __init__(self, tp: int):
+        h = c_void_p()
+        _check(load_library().pblock_tp_context_create(int(tp), ctypes.byref(h)))
+        self.tp = int(tp)
+        self.handle = h.value
+
+    def close(self):
+        if self.handle:
+            load_library().pblock_tp_context_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
 
 
 def pblock_swattn_forward(cfg, q, k, v, ld_qkv, o, ld_o, lse, ws=None, stream=None):
@@ -234,20 +320,6 @@ def pblock_swattn_backward(cfg, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, dq, d
         ctypes.byref(cfg), _ptr(q), _ptr(k), _ptr(v), ld_qkv, _ptr(o), ld_o, _ptr(d_o), ld_do,
         _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), ld_dqkv, _ptr(ws), _nbytes(ws),
         _stream(stream)))
-
-
-def pblock_set_step_events(begin, end):
-    """begin/end: sequences of len(STEPS) raw hipEvent_t handles (ints, 0 to
-    skip a step), or None to turn recording off."""
-    lib = load_library()
-    if begin is None or end is None:
-        _check(lib.pblock_set_step_events(None, None))
-        return
-    n = len(STEPS)
-    assert len(begin) == n and len(end) == n
-    b = (c_void_p * n)(*[h or None for h in begin])
-    e = (c_void_p * n)(*[h or None for h in end])
-    _check(lib.pblock_set_step_events(b, e))
 
 
 def pblock_serial_saved_bytes(cfg: PbConfig) -> int:
@@ -319,10 +391,10 @@ def pblock_ag_in_proj_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch:
 
 
 def pblock_ag_in_proj(cfg, tp, rank, shards, h, w_in, b_in, z, c, shards_per_launch, ws, stream,
-                      comm_streams):
+                      comm_streams, ctx: TpContext):
     """shards: tp tensors (or addresses), rank j's rows of h; comm_streams: a
     non-empty sequence of streams other than `stream` (torch streams or raw
-    handles)."""
+    handles); ctx: a TpContext for this tp on the current device."""
     if len(shards) != tp:
         raise ValueError(f"{len(shards)} shards for tp={tp}")
     arr = (c_void_p * len(shards))(*[_ptr(t) for t in shards])
@@ -330,7 +402,7 @@ def pblock_ag_in_proj(cfg, tp, rank, shards, h, w_in, b_in, z, c, shards_per_lau
     _check(load_library().pblock_ag_in_proj(
         ctypes.byref(cfg), int(tp), int(rank), arr, _ptr(h), _ptr(w_in), _ptr(b_in), _ptr(z),
         _ptr(c), int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream),
-        len(comm_streams), cs))
+        len(comm_streams), cs, ctx.handle if ctx is not None else None))
 
 
 def pblock_rs_out_proj_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch: int) -> int:
@@ -339,16 +411,17 @@ def pblock_rs_out_proj_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch
 
 
 def pblock_rs_out_proj(cfg, tp, rank, c, w_out, partial, dst, shards_per_launch, ws, stream,
-                       comm_streams):
+                       comm_streams, ctx: TpContext):
     """dst: tp tensors (or addresses), where rank j receives this rank's
-    chunk j; comm_streams as for pblock_ag_in_proj."""
+    chunk j; comm_streams and ctx as for pblock_ag_in_proj."""
     if len(dst) != tp:
         raise ValueError(f"{len(dst)} destinations for tp={tp}")
     arr = (c_void_p * len(dst))(*[_ptr(t) for t in dst])
     cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
     _check(load_library().pblock_rs_out_proj(
         ctypes.byref(cfg), int(tp), int(rank), _ptr(c), _ptr(w_out), _ptr(partial), arr,
-        int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream), len(comm_streams), cs))
+        int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream), len(comm_streams), cs,
+        ctx.handle if ctx is not None else None))
 
 
 def pblock_rs_reduce(cfg, tp, parts, x_shard, b_out, y_shard, stream=None):
@@ -406,18 +479,18 @@ class ParallelBlock:
         )
         self.T = T
 
-    def forward(self, stream=None):
+    def forward(self, stream=None, step_ev=None):
         t = self.t
         pblock_forward(self.cfg, t["x"], t["gamma"], t["beta"], t["w_in"], t["b_in"], t["w_out"],
-                       t["b_out"], self.y, self.saved, self.ws_fwd, stream)
+                       t["b_out"], self.y, self.saved, self.ws_fwd, stream, step_ev)
         return self.y
 
-    def backward(self, dy=None, stream=None):
+    def backward(self, dy=None, stream=None, step_ev=None):
         t, g = self.t, self.grads
         pblock_backward(self.cfg, t["x"], t["gamma"], t["beta"], t["w_in"], t["b_in"], t["w_out"],
                         t["b_out"], self.saved, t["dy"] if dy is None else dy, g["dx"],
                         g["dgamma"], g["dbeta"], g["dw_in"], g["db_in"], g["dw_out"],
-                        g["db_out"], self.ws, stream)
+                        g["db_out"], self.ws, stream, step_ev)
         return g
 
     def saved_view(self, name: str):

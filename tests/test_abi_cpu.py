@@ -86,38 +86,53 @@ def test_saved_layout(name):
 
 
 def tail_split(M, N, K, bf16=True):
-    """The split plan the library uses for an M x N x K GEMM: tiles of
-    256 x 256, 256 CUs; the last partial wave is split along K to fill the
-    chip, and a grid of fewer tiles than CUs is split along K when the
-    estimate (waves x K-steps, plus 3 + 1/16 per partial tile) wins."""
-    tiles = -(-M // 256) * -(-N // 256)
-    n_full = tiles // 256 * 256
-    tail = tiles - n_full
-    if not bf16 or K % 64 or tail == 0:
-        return 0
-    nk = K // 64
-    if n_full:
-        splits = min(256 // tail, nk)
-    else:
-        def cost(s):
-            c = -(-tiles * s // 256) * -(-nk // s)
-            return c if s == 1 else c + 3 + tiles * s / 16
-        splits = 1
-        for s in range(2, min(16, nk) + 1):
-            if cost(s) < cost(splits):
-                splits = s
-    return tail * splits * 65536 if splits >= 2 else 0
+    """Bytes of fp32 partial tiles of an M x N x K GEMM as the library plans
+    it (pblock_gemm_plan): 0 when unsplit."""
+    p = pb.pblock_gemm_plan(pb.PB_BF16 if bf16 else pb.PB_F32, M, N, K)
+    return p.tail * p.splits * 65536 if p.tail else 0
 
 
 def test_split_plan_examples():
-    """A few plans worked out by hand: a partial last wave of 80 tiles splits
-    3 ways; 48 tiles with K = 12288 split 5 ways (240 workgroups, one wave);
-    144 tiles split 3 ways (2 waves of a third of K each)."""
-    assert tail_split(2048, 10752, 12288) == 80 * 3 * 65536
-    assert tail_split(2048, 1536, 12288) == 48 * 5 * 65536
-    assert tail_split(2048, 4608, 12288) == 144 * 3 * 65536
-    assert tail_split(2048, 4608, 12288, bf16=False) == 0
-    assert tail_split(128, 256, 256) == 0  # one tile, four K-steps: not worth a reduction
+    """Plans worked out by hand on 256 x 256 tiles and 256 CUs: a partial
+    last wave is split along K to fill the chip once; a grid of fewer tiles
+    than CUs is split when waves x K-steps per slice, plus a reduction cost of
+    3 + 1/16 K-step per partial tile, is lowest.
+      2048 x 10752 x 12288: 336 tiles = 256 whole + 80, 80 split 256 // 80 = 3
+      2048 x 1536 x 12288: 48 tiles, K-steps 192; cost(s) = ceil(48 s / 256)
+        ceil(192 / s) + 3 + 3 s is lowest at s = 5 (1 x 39 + 18 = 57)
+      2048 x 4608 x 12288: 144 tiles; s = 3: 2 waves x 64 + 30 = 158 beats
+        s = 1 (192) and every other s
+      fp32 and a single 4-K-step tile: unsplit."""
+    plan = lambda *a: pb.pblock_gemm_plan(*a)  # noqa: E731
+    p = plan(pb.PB_BF16, 2048, 10752, 12288)
+    assert (p.tiles, p.n_full, p.tail, p.splits) == (336, 256, 80, 3)
+    assert (p.workgroups, p.threads) == (256 + 80 * 3, 512)
+    p = plan(pb.PB_BF16, 2048, 1536, 12288)
+    assert (p.n_full, p.tail, p.splits, p.workgroups) == (0, 48, 5, 240)
+    p = plan(pb.PB_BF16, 2048, 4608, 12288)
+    assert (p.n_full, p.tail, p.splits) == (0, 144, 3)
+    p = plan(pb.PB_F32, 2048, 4608, 12288)
+    assert (p.tiles, p.tail, p.splits, p.workgroups, p.threads) == (32 * 72, 0, 1, 32 * 72, 256)
+    p = plan(pb.PB_BF16, 128, 256, 256)
+    assert (p.tiles, p.tail, p.splits, p.workgroups) == (1, 0, 1, 1)
+    # K not a multiple of 64 takes the unsplit path
+    p = plan(pb.PB_BF16, 2048, 12288 + 256, 1000)
+    assert (p.tiles, p.tail, p.splits, p.workgroups) == (8 * 49, 0, 1, 8 * 49)
+    for bad in ((pb.PB_BF16, 0, 1, 1), (pb.PB_BF16, 1, -1, 1), (7, 1, 1, 1)):
+        with pytest.raises(pb.PblockError):
+            plan(*bad)
+
+
+def test_backward_pairs_query():
+    """bf16 shapes with every K a multiple of 64 share launches; fp32 never."""
+    assert pb.pblock_backward_pairs(pb.config_from_shape(WORKLOADS["175b_tp8_share"])) == (True, True)
+    assert pb.pblock_backward_pairs(pb.config_from_shape(WORKLOADS["175b_tp8_share"]),
+                                    "serial") == (True, True, True, True)
+    assert pb.pblock_backward_pairs(pb.config_from_shape(WORKLOADS["tiny_f32"])) == (False, False)
+    # 1000 tokens: the weight gradients' K = T is not a multiple of 64
+    ragged = pb.make_config(1, 1000, 1024, 8, 128, 2048, 256)
+    assert pb.pblock_backward_pairs(ragged) == (False, False)
+    assert pb.load_library().pblock_backward_pairs(ctypes.byref(ragged), 2, None) == 1
 
 
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
@@ -325,7 +340,7 @@ def test_ag_in_proj_rejects_bad_arguments_before_launching():
         shards = (ctypes.c_void_p * tp)(*([FAKE] * tp)) if tp > 0 else None
         cs = (ctypes.c_void_p * max(len(comm), 1))(*comm) if comm else None
         return lib.pblock_ag_in_proj(ctypes.byref(cfg), tp, rank, shards, FAKE, FAKE, FAKE, FAKE,
-                                     FAKE, per, ws, nbytes, stream, len(comm), cs)
+                                     FAKE, per, ws, nbytes, stream, len(comm), cs, None)
 
     assert call(tp=3) == 1 and "divisible" in pb.pblock_last_error()
     assert call(tp=65) == 1
@@ -336,6 +351,8 @@ def test_ag_in_proj_rejects_bad_arguments_before_launching():
     assert call(comm=()) == 1
     assert call(ws=FAKE + 16) == 1
     assert call(cfg=good_cfg(head_dim=80)) == 2
+    # every other argument is checked before the context
+    assert call() == 1 and "ctx" in pb.pblock_last_error()
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 8, 1) % 256 == 0
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 8, 9) == 0
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 3, 1) == 0
@@ -350,7 +367,7 @@ def test_rs_out_proj_and_reduce_reject_bad_arguments_before_launching():
         d = (ctypes.c_void_p * tp)(*(dst or [FAKE] * tp)) if tp > 0 else None
         cs = (ctypes.c_void_p * max(len(comm), 1))(*comm) if comm else None
         return lib.pblock_rs_out_proj(ctypes.byref(cfg), tp, rank, FAKE, FAKE, FAKE, d, per, ws,
-                                      nbytes, stream, len(comm), cs)
+                                      nbytes, stream, len(comm), cs, None)
 
     assert call(tp=3) == 1 and "divisible" in pb.pblock_last_error()
     assert call(tp=65) == 1
@@ -363,12 +380,14 @@ def test_rs_out_proj_and_reduce_reject_bad_arguments_before_launching():
     assert call(dst=[FAKE] * 7 + [FAKE + 8]) == 1 and "dst[7]" in pb.pblock_last_error()
     assert call(dst=[FAKE] * 3 + [None] * 5) == 1 and "dst[3]" in pb.pblock_last_error()
     assert call(cfg=good_cfg(head_dim=80)) == 2
+    assert call() == 1 and "ctx" in pb.pblock_last_error()
     assert pb.pblock_rs_out_proj_workspace_bytes(c, 8, 1) % 256 == 0
     assert pb.pblock_rs_out_proj_workspace_bytes(c, 8, 9) == 0
     assert pb.pblock_rs_out_proj_workspace_bytes(c, 3, 1) == 0
     # the python wrappers refuse a list of the wrong length
     with pytest.raises(ValueError):
-        pb.pblock_rs_out_proj(c, 8, 0, FAKE, FAKE, FAKE, [FAKE] * 7, 1, None, FAKE, [FAKE + 256])
+        pb.pblock_rs_out_proj(c, 8, 0, FAKE, FAKE, FAKE, [FAKE] * 7, 1, None, FAKE, [FAKE + 256],
+                              None)
     with pytest.raises(ValueError):
         pb.pblock_rs_reduce(c, 8, [FAKE] * 9, FAKE, FAKE, FAKE)
 
@@ -377,6 +396,12 @@ def test_rs_out_proj_and_reduce_reject_bad_arguments_before_launching():
         return lib.pblock_rs_reduce(ctypes.byref(cfg), tp, arr, x, b, y, FAKE)
 
     assert reduce(tp=3) == 1
+    # a context is made for tp in 1..64 (the events need a device)
+    h = ctypes.c_void_p(FAKE)
+    assert lib.pblock_tp_context_create(0, ctypes.byref(h)) == 1 and h.value is None
+    assert lib.pblock_tp_context_create(65, ctypes.byref(h)) == 1
+    assert lib.pblock_tp_context_create(8, None) == 1
+    lib.pblock_tp_context_destroy(None)
     assert reduce(tp=0) == 1 and reduce(tp=65) == 1
     assert reduce(parts=[FAKE] * 7 + [FAKE + 4]) == 1 and "parts[7]" in pb.pblock_last_error()
     assert reduce(y=None) == 1 and reduce(b=FAKE + 2) == 1

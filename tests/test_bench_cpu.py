@@ -89,7 +89,7 @@ def test_serial_gemm_steps_are_labelled():
             "false, false, (pb::Epi)0, true>()")
     assert bench.gemm_step_of(pair, (192 + 1152) * 512, s, "serial") == "dg+dw_down"
     # 48 tiles of the dO GEMM, K = 12288: 5 slices each
-    assert bench.split_plan(*steps["d_o"]) == (0, 48, 5)
+    assert bench.gemm_grid_threads(*steps["d_o"]) == 48 * 5 * 512
 
 
 def test_paired_gemm_launches_are_labelled_and_counted():

@@ -77,8 +77,9 @@ class Case:
         stream = torch.cuda.Stream()
         comm = [torch.cuda.Stream() for _ in range(n_comm)]
         stream.wait_stream(torch.cuda.current_stream())
-        pb.pblock_ag_in_proj(cfg, tp, rank, shards, h, self.d_w, self.d_b, z, c, per, ws, stream,
-                             comm)
+        with pb.TpContext(tp) as ctx:
+            pb.pblock_ag_in_proj(cfg, tp, rank, shards, h, self.d_w, self.d_b, z, c, per, ws,
+                                 stream, comm, ctx)
         torch.cuda.synchronize()
         assert torch.equal(h, self.d_src), "gathered h differs from the shards"
         A = s.attn_width

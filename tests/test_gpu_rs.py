@@ -80,11 +80,13 @@ class Ranks:
         stream = torch.cuda.Stream()
         comm = [torch.cuda.Stream() for _ in range(n_comm)]
         stream.wait_stream(torch.cuda.current_stream())
+        ctx = pb.TpContext(tp)
         for r in range(tp):
             dst = [partial[r][j * rows:(j + 1) * rows] if (r in in_place and j == r)
                    else recv[j][r] for j in range(tp)]
             pb.pblock_rs_out_proj(cfg, tp, r, self.d_c[r], self.d_w[r], partial[r], dst, per,
-                                  ws, stream, comm)
+                                  ws, stream, comm, ctx)
+        ctx.close()
         y = torch.empty((T, H), dtype=act, device="cuda")
         for j in range(tp):
             parts = [partial[j][j * rows:(j + 1) * rows] if (j in in_place and q == j)
@@ -193,7 +195,8 @@ def test_rs_out_proj_full_size_175b_share():
     stream = torch.cuda.Stream()
     comm = [torch.cuda.Stream() for _ in range(2)]
     stream.wait_stream(torch.cuda.current_stream())
-    pb.pblock_rs_out_proj(cfg, tp, rank, d_c, d_w, partial, dst, 2, ws, stream, comm)
+    with pb.TpContext(tp) as ctx:
+        pb.pblock_rs_out_proj(cfg, tp, rank, d_c, d_w, partial, dst, 2, ws, stream, comm, ctx)
     torch.cuda.synchronize()
     sample = np.array([0, 1, 255, 256, 767, 768, 1000, 2047])
     ref = c[sample].astype(np.float64) @ w.astype(np.float64).T
