@@ -365,7 +365,6 @@ constexpr int kDK = 64;                     // K-tile of the DMA path
 constexpr int kStages = 2;
 constexpr int kDTile = kBM * kDK * 2;       // one operand tile: 32 KB
 constexpr int kPieces = kDTile / kThreads / 16;  // 1 KB DMA pieces per operand per wave: 4
-constexpr int kDmaPerStage = 2 * kPieces;   // DMA instructions per wave per stage
 static_assert(kBM == kBN && kPieces * 1024 * (kThreads / 64) == kDTile, "tile split over waves");
 static_assert(kDK == kBK, "the DMA path's K-tile is the planning unit");
 
@@ -625,31 +624,48 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
 
   // K-tiles [kt0, kt1) of this work item
   const int nt = kt1 - kt0;
-  uint32_t aoff[kPieces], boff[kPieces];
+  // Who moves which part of a K-tile, and when.  All eight waves issuing
+  // their loads together right after the barrier stalls them: the CU's load
+  // path takes the 64 KB of a K-tile in roughly a thousand cycles, and a wave
+  // whose load cannot be queued stops issuing, MFMAs included, while the
+  // second wave of each SIMD, already behind the first, falls further behind
+  // (per-phase clock stamps: ~1000 cycles between the two waves of a SIMD,
+  // ~2800 cycles per K-tile against 2048 of matrix work).  Measured best:
+  //  - both operands K-contiguous: every wave moves its own 4 KB of each
+  //    operand, A of tile t + 2 right after the barrier of tile t and B of
+  //    tile t + 1 at the start of tile t;
+  //  - otherwise (transposing fragment reads): the first wave of each SIMD
+  //    (waves 0-3) moves both 4 KB regions of its SIMD, on the same schedule,
+  //    and the second wave none, which also slows the leading wave down to
+  //    its partner's pace.
+  constexpr int kReg = BK ? 1 : 2;  // 4 KB regions per operand per issuing wave
+  constexpr int kDmaPerTile = 2 * kReg * kPieces;
+  const bool dma_wave = BK || wave < 4;
+  auto region = [&](int r) { return BK ? wave : (wave & 3) + 4 * r; };
+  uint32_t aoff[kReg * kPieces], boff[kReg * kPieces];
 #pragma unroll
-  for (int i = 0; i < kPieces; ++i) {
-    aoff[i] = dma_lane_off<AK>(lda, m0, M, wave, lane, i);
-    boff[i] = dma_lane_off<BK>(ldb, n0, N, wave, lane, i);
-  }
+  for (int r = 0; r < kReg; ++r)
+#pragma unroll
+    for (int i = 0; i < kPieces; ++i) {
+      aoff[r * kPieces + i] = dma_lane_off<AK>(lda, m0, M, region(r), lane, i);
+      boff[r * kPieces + i] = dma_lane_off<BK>(ldb, n0, N, region(r), lane, i);
+    }
   const bf16* abase = (AK ? A + (size_t)m0 * lda : A + m0) + (size_t)kt0 * (AK ? kDK : (size_t)kDK * lda);
   const bf16* bbase = (BK ? B + (size_t)n0 * ldb : B + n0) + (size_t)kt0 * (BK ? kDK : (size_t)kDK * ldb);
   const size_t astep = AK ? kDK : (size_t)kDK * lda;  // elements per K-tile
   const size_t bstep = BK ? kDK : (size_t)kDK * ldb;
-  // this wave's share of tile t: the A pieces (half 0) or the B pieces (half 1)
+  // this wave's pieces of one operand of tile t (half 0: A, half 1: B)
   auto issue_half = [&](int t, int half) {
+    if (!dma_wave) return;
     const int s = t % kStages;
-    const uint32_t piece0 = wave * (kPieces * 1024);
-    if (half == 0) {
-      const bf16* ab = abase + (size_t)t * astep;
+    const bf16* src = half == 0 ? abase + (size_t)t * astep : bbase + (size_t)t * bstep;
+    const uint32_t dst0 = lds0 + (half == 0 ? a_off(s) : b_off(s));
+#pragma unroll
+    for (int r = 0; r < kReg; ++r)
 #pragma unroll
       for (int i = 0; i < kPieces; ++i)
-        dma16s(ab, aoff[i], __builtin_amdgcn_readfirstlane(lds0 + a_off(s) + piece0 + i * 1024));
-    } else {
-      const bf16* bb = bbase + (size_t)t * bstep;
-#pragma unroll
-      for (int i = 0; i < kPieces; ++i)
-        dma16s(bb, boff[i], __builtin_amdgcn_readfirstlane(lds0 + b_off(s) + piece0 + i * 1024));
-    }
+        dma16s(src, half == 0 ? aoff[r * kPieces + i] : boff[r * kPieces + i],
+               __builtin_amdgcn_readfirstlane(dst0 + region(r) * (kPieces * 1024) + i * 1024));
   };
   auto issue = [&](int t) {
     issue_half(t, 0);
@@ -668,10 +684,10 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   // of phase 4 s, each pair of N blocks with its own phase's batch.  The
   // reads of a K-tile's last phase are issued kLook phases before its end;
   // the one workgroup barrier of the K-tile follows them, after which the
-  // tile's stage takes the loads of tile t + 2 (issued over the next two
-  // phases) while the next tile's first fragments are read.  With kLook = 2
-  // at most 14 fragments are live (56 registers beside the 128 of the
-  // accumulators) and a load has a whole K-tile to land.
+  // tile's stage takes A of tile t + 2 (and, from the start of tile t + 1,
+  // B) while the next tile's first fragments are read.  With kLook = 2 at
+  // most 14 fragments are live (56 registers beside the 128 of the
+  // accumulators) and a load has most of a K-tile to land.
   constexpr int kPh = 8, kLook = 2;
   static_assert(kLook >= 2 && kLook < kPh, "DMA halves are issued after the barrier");
   bf16x8 fa[2][kTM16], fb[2][kTN16];
@@ -719,8 +735,9 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
       block_barrier();
       if (t + 2 < nt) issue_half(t + 2, 0);
     }
-    if constexpr (p == kPh - kLook + 1)
-      if (t + 2 < nt) issue_half(t + 2, 1);
+    // B of tile t + 1 (tiles 0 and 1 were issued whole before the loop)
+    if constexpr (p == 0)
+      if (t + 1 >= 2 && t + 1 < nt) issue_half(t + 1, 1);
     // the batch kLook phases ahead (past the last tile: a stale stage, unused)
     if constexpr (p + kLook < kPh) read_frags(t, p + kLook);
     else read_frags(t + 1, p + kLook - kPh);
@@ -741,7 +758,7 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   pin_sgpr(ep.rowpart_ld), pin_sgpr(part);
   if (nt > 0) issue(0);
   if (nt > 1) issue(1);
-  if (nt > 1) wait_dma<kDmaPerStage>();  // tile 0 landed; tile 1 may be in flight
+  if (nt > 1) wait_dma<kDmaPerTile>();  // tile 0 landed; tile 1 may be in flight
   else wait_dma<0>();
   block_barrier();
   // batch by batch, as in the loop, so the wait at the loop's head (merged
