@@ -1281,12 +1281,14 @@ void fwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
 template <int D>
 void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v, int ld,
            const void* o, int ld_o, const void* d_o, int ld_do, const float* lse, float* delta,
-           void* dq, void* dk, void* dv, int ld_d, void* part, size_t part_bytes, hipStream_t s) {
+           bool delta_ready, void* dq, void* dk, void* dv, int ld_d, void* part,
+           size_t part_bytes, hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)D);
   const int nrows = a.batch * a.seq * a.heads;
   if (dt == Dt::BF16) {
-    attn_delta_kernel<bf16><<<(nrows + 255) / 256, 256, 0, s>>>(
-        (const bf16*)o, ld_o, (const bf16*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
+    if (!delta_ready)
+      attn_delta_kernel<bf16><<<(nrows + 255) / 256, 256, 0, s>>>(
+          (const bf16*)o, ld_o, (const bf16*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
     AttnSplit p = attn_bwd_split_plan(dt, a);
     if (!part || part_bytes < attn_bwd_partial_bytes(a, p)) {
       p.fwd_chunk = p.kv_chunk = kUnsplit;
@@ -1311,7 +1313,8 @@ void bwd_d(Dt dt, const AttnShape& a, const void* q, const void* k, const void* 
           pdq, nullptr, p.fwd_chunk, (bf16*)dq, nullptr, ld_d, a.batch, a.seq, a.heads,
           a.window);
   } else {
-    attn_delta_kernel<float><<<(nrows + 255) / 256, 256, 0, s>>>(
+    if (!delta_ready)
+      attn_delta_kernel<float><<<(nrows + 255) / 256, 256, 0, s>>>(
         (const float*)o, ld_o, (const float*)d_o, ld_do, delta, a.batch, a.seq, a.heads, D);
     dim3 g((a.seq + 63) / 64, a.heads, a.batch);
     attn_dq_f32<D><<<g, 64, 0, s>>>((const float*)q, (const float*)k, (const float*)v, ld,
@@ -1384,17 +1387,17 @@ void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k
 
 void launch_attn_backward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
                           int ld_qkv, const void* o, int ld_o, const void* d_o, int ld_do,
-                          const float* lse, float* delta, void* dq, void* dk, void* dv, int ld_d,
-                          void* part, size_t part_bytes, hipStream_t s) {
+                          const float* lse, float* delta, bool delta_ready, void* dq, void* dk,
+                          void* dv, int ld_d, void* part, size_t part_bytes, hipStream_t s) {
   if (a.head_dim == 64)
-    bwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
-              part_bytes, s);
+    bwd_d<64>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, delta_ready, dq, dk, dv,
+              ld_d, part, part_bytes, s);
   else if (a.head_dim == 96)
-    bwd_d<96>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
-              part_bytes, s);
+    bwd_d<96>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, delta_ready, dq, dk, dv,
+              ld_d, part, part_bytes, s);
   else
-    bwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, dq, dk, dv, ld_d, part,
-               part_bytes, s);
+    bwd_d<128>(dt, a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, delta, delta_ready, dq, dk, dv,
+              ld_d, part, part_bytes, s);
 }
 
 }  // namespace pb

@@ -502,7 +502,15 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
         }
       }
       if constexpr (EPI == Epi::DgeluSplit) {
-        if (dg_aux) {
+        if (ep.delta && n < ep.split) {
+          // the attention output O of this lane's four columns, for delta
+#pragma unroll
+          for (int t = 0; t < 16; ++t) {
+            const int mc = min(m0h + 2 * t + hi, M - 1);
+            in2[t] = *reinterpret_cast<const u32x2*>((const bf16*)ep.o_rows +
+                                                     (size_t)mc * ep.ld_o_rows + ncl);
+          }
+        } else if (dg_aux) {
           const int col = max(ncl - ep.split, 0) + ep.col2;
 #pragma unroll
           for (int t = 0; t < 16; ++t) {
@@ -557,6 +565,21 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
 #pragma unroll
           for (int e = 0; e < 4; ++e) o[e] = v[e];
           if (ok) store4((bf16*)ep.out + (size_t)m * ep.ld_out + n, o);
+          if (ep.delta) {
+            // rowsum of dO * O over each head's columns (dO as stored), the
+            // head's lanes (hd / 4 of them) summed across
+            const float ov[4] = {lo_bf(in2[t][0]), hi_bf(in2[t][0]), lo_bf(in2[t][1]),
+                                 hi_bf(in2[t][1])};
+            float sd = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sd += bf2f(f2bf(v[e])) * ov[e];
+            const int gl = ep.delta_hd >> 2;  // lanes per head: 32 or 16
+            for (int off = 1; off < gl; off <<= 1) sd += __shfl_xor(sd, off, 64);
+            if ((c & (gl - 1)) == 0 && ok) {
+              const int b = m / ep.delta_seq, tt = m - b * ep.delta_seq;
+              ep.delta[((size_t)b * ep.delta_heads + n / ep.delta_hd) * ep.delta_seq + tt] = sd;
+            }
+          }
         } else {
           const float u[4] = {lo_bf(in2[t][0]), hi_bf(in2[t][0]), lo_bf(in2[t][1]),
                               hi_bf(in2[t][1])};
@@ -755,7 +778,8 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   pin_sgpr(ep.out), pin_sgpr(ep.ld_out), pin_sgpr(ep.out2), pin_sgpr(ep.ld_out2);
   pin_sgpr(ep.bias), pin_sgpr(ep.resid), pin_sgpr(ep.aux), pin_sgpr(ep.split);
   pin_sgpr(ep.col2), pin_sgpr(ep.mean), pin_sgpr(ep.rstd), pin_sgpr(ep.rowpart);
-  pin_sgpr(ep.rowpart_ld), pin_sgpr(part);
+  pin_sgpr(ep.rowpart_ld), pin_sgpr(part), pin_sgpr(ep.o_rows), pin_sgpr(ep.ld_o_rows);
+  pin_sgpr(ep.delta), pin_sgpr(ep.delta_seq), pin_sgpr(ep.delta_heads), pin_sgpr(ep.delta_hd);
   if (nt > 0) issue(0);
   if (nt > 1) issue(1);
   if (nt > 1) wait_dma<kDmaPerTile>();  // tile 0 landed; tile 1 may be in flight

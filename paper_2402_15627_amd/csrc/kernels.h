@@ -116,6 +116,15 @@ struct EpiArgs {
   const float* rstd = nullptr;
   float2* rowpart = nullptr;
   int rowpart_ld = 0;
+  // DgeluSplit, LDS-staged path only (launch_gemm_pair): when delta is set,
+  // also delta[(b heads + h) seq + t] = sum over head h's columns of
+  // out[m, n] o_rows[m * ld_o_rows + n] for m = b seq + t, n < split, with
+  // out rounded to the activation type first; head_dim 64 or 128, split and
+  // the tile's column blocks aligned to heads.
+  const void* o_rows = nullptr;
+  int ld_o_rows = 0;
+  float* delta = nullptr;
+  int delta_seq = 0, delta_heads = 0, delta_hd = 0;
 };
 // 64-column groups of the LnGrad row terms for a row of n columns.
 inline int ln_row_groups(int n) { return (n + 63) / 64; }
@@ -196,12 +205,13 @@ size_t attn_bwd_partial_bytes(const AttnShape& a, const AttnSplit& p);
 void launch_attn_forward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
                          int ld_qkv, void* o, int ld_o, float* lse, void* part,
                          size_t part_bytes, hipStream_t s);
-// delta[b, head, t] = sum_e do * o (softmax row term of the backward pass).
+// delta[b, head, t] = sum_e do * o (softmax row term of the backward pass),
+// formed here unless delta_ready (the caller has already written it).
 // o uses ld_o, d_o uses ld_do; delta holds batch*heads*seq floats.  part as
 // for the forward, against attn_bwd_partial_bytes.
 void launch_attn_backward(Dt dt, const AttnShape& a, const void* q, const void* k, const void* v,
                           int ld_qkv, const void* o, int ld_o, const void* d_o, int ld_do,
-                          const float* lse, float* delta, void* dq, void* dk, void* dv, int ld_d,
-                          void* part, size_t part_bytes, hipStream_t s);
+                          const float* lse, float* delta, bool delta_ready, void* dq, void* dk,
+                          void* dv, int ld_d, void* part, size_t part_bytes, hipStream_t s);
 
 }  // namespace pb

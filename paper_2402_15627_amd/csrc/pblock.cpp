@@ -644,13 +644,27 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   e4.rstd = rstd;
   e4.rowpart = rowpart;
   e4.rowpart_ld = pb::ln_row_groups(H);
-  const ParallelBwdGemms G = parallel_bwd_gemms(d, dy, w_out, c, dz, w_in, h, e1, e2, e4, e5);
+  ParallelBwdGemms G = parallel_bwd_gemms(d, dy, w_out, c, dz, w_in, h, e1, e2, e4, e5);
   const pb::GemmSpec &g_dc = G.dc, &g_dwo = G.dw_out, &g_dh = G.dh, &g_dwi = G.dw_in;
   auto run = [&](const pb::GemmSpec& g) {
     pb::launch_gemm(dt, g.epi, g.a_kcontig, g.b_kcontig, g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K,
                     g.ep, split_ws, split_f, stream);
   };
   const bool pair_out = pb::gemm_pair_supported(dt, g_dc, g_dwo);
+  // The attention backward's row terms delta = rowsum(dO * O) per head are
+  // formed in dC's epilogue (the shared launch's LDS-staged path), where dO
+  // leaves the accumulators, instead of re-reading dO and O in a launch of
+  // their own: heads of 64 or 128 columns whose blocks align with the
+  // epilogue's 128-column wave blocks.
+  const bool delta_in_dc = pair_out && (d.d == 64 || d.d == 128) && A % 128 == 0;
+  if (delta_in_dc) {
+    G.dc.ep.o_rows = c;  // O = C[:, :A]
+    G.dc.ep.ld_o_rows = K_out;
+    G.dc.ep.delta = delta;
+    G.dc.ep.delta_seq = (int)d.S;
+    G.dc.ep.delta_heads = (int)d.heads;
+    G.dc.ep.delta_hd = (int)d.d;
+  }
   {
     StepScope sc(step_ev, PB_STEP_DC, stream);  // with dW_out when they share a launch
     if (pair_out)
@@ -662,8 +676,8 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   {
     StepScope sc(step_ev, PB_STEP_ATTN_BWD, stream);
     pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c,
-                             K_out, d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e),
-                             N_in, split_ws, split_f * 4, stream);
+                             K_out, d_o, A, lse, delta, delta_in_dc, dz, at(dz, A, e),
+                             at(dz, 2LL * A, e), N_in, split_ws, split_f * 4, stream);
   }
   // B4: dh = dZ W_in, stored in the activation type; its epilogue also forms
   // the LayerNorm backward's row terms (sums of gamma dh and gamma dh xhat per
@@ -851,7 +865,7 @@ pb_status pblock_swattn_backward(const pb_config* cfg, const void* q, const void
   a.head_dim = cfg->head_dim;
   a.window = cfg->window < cfg->seq ? cfg->window : cfg->seq;
   pb::launch_attn_backward(dt_of(cfg), a, q, k, v, ld_qkv, o, ld_o, d_o, ld_do, lse, (float*)ws,
-                           dq, dk, dv, ld_dqkv, (char*)ws + need, ws_bytes - need, stream);
+                           false, dq, dk, dv, ld_dqkv, (char*)ws + need, ws_bytes - need, stream);
   return finish_launches();
 }
 
@@ -1123,7 +1137,7 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   // attention: dO = dx1 W_o, then dQ, dK, dV -> dZ[:, :3A]
   run_with(G.d_o, G.dw_o);
   pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
-                           d_o, A, lse, delta, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in,
+                           d_o, A, lse, delta, false, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in,
                            split_ws, split_f * 4, stream);
   run_with(G.dh1, G.dw_qkv);
   // dx = dx1 + LN1'(dh1); dgamma1, dbeta1, and db_o = sum dx1
