@@ -93,6 +93,9 @@ def step_work(s):
     for a, b in paired_steps(s).items():
         work[a] = ("mfma", work[a][1] + work[b][1])
         work[b] = ("mfma", 0)
+    # db_in is then summed inside dW_in's tiles: its step is empty
+    if "dh" in paired_steps(s):
+        work["db_in"] = ("hbm", 0)
     return work
 
 

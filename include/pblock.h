@@ -142,7 +142,8 @@ typedef enum {
   PB_STEP_ATTN_BWD,   /* dQ, dK, dV                                         */
   PB_STEP_DH,         /* dh = dZ W_in                                       */
   PB_STEP_DW_IN,      /* dW_in = dZ^T h                                     */
-  PB_STEP_DB_IN,      /* db_in = sum over tokens of dZ                      */
+  PB_STEP_DB_IN,      /* db_in = sum over tokens of dZ; empty when formed
+                         in dW_in's launch shared with dh                 */
   PB_STEP_LN_BWD,     /* dx = dy + LN backward; dgamma, dbeta, db_out       */
   PB_STEP_COUNT
 } pb_step;
@@ -152,9 +153,9 @@ typedef enum {
  * launches of step i and end[i] just after them; NULL entries, and a NULL
  * pb_step_events, are skipped.  The events belong to the caller and are
  * only recorded, never waited on.  A step whose work shares a launch with
- * another step records nothing between its events (PB_STEP_DW_OUT and
- * PB_STEP_DW_IN when pblock_backward_pairs reports the pair; PB_STEP_DB_OUT
- * always). */
+ * another step records nothing between its events (PB_STEP_DW_OUT, and
+ * PB_STEP_DW_IN and PB_STEP_DB_IN, when pblock_backward_pairs reports the
+ * pair; PB_STEP_DB_OUT always). */
 typedef struct {
   hipEvent_t begin[PB_STEP_COUNT];
   hipEvent_t end[PB_STEP_COUNT];

@@ -628,7 +628,20 @@ PB_DEV void wave_epilogue_lds(const EpiArgs& ep, float* __restrict__ part_tile,
 // One work item of the DMA GEMM: K-tiles [kt0, kt1) of output tile lid
 // (slice >= 0: one K-slice of tail tile lid, whose fp32 partial tile goes to
 // part for splitk_reduce).
-template <bool AK, bool BK, Epi EPI, bool GT>
+// Sum of a fragment's eight bf16 values, added to acc in fp32.
+PB_DEV float sum_bf16x8(const bf16x8& p, float acc) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 8; i += 2)
+    acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{p[i], p[i + 1]}, one, acc, false);
+  return acc;
+}
+
+// RS (StoreF32 only): also the row sums of A over this work item's K-tiles,
+// rowsum[m] = sum_k A(m, k), from the A fragments the MFMAs consume (the
+// caller sets RS for the tiles of the first tile column only).
+template <bool AK, bool BK, Epi EPI, bool GT, bool RS = false>
 PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb,
                           int M, int N, const EpiArgs& ep, int lid, int slice, int kt0, int kt1,
                           int n_full, int splits, float* __restrict__ part) {
@@ -725,8 +738,15 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
 #pragma unroll
     for (int j = 2 * r; j < 2 * r + 2; ++j) fb[ks][j] = dma_frag16<BK>(pb, wn + 16 * j, ks, lane);
   };
+  float rsum[kTM16];
+#pragma unroll
+  for (int i = 0; i < kTM16; ++i) rsum[i] = 0.f;
   auto mma = [&](auto P) {
     constexpr int p = decltype(P)::value, ks = p >> 2, j0 = 2 * (p & 3);
+    if constexpr (RS && (p & 3) == 0) {
+#pragma unroll
+      for (int i = 0; i < kTM16; ++i) rsum[i] = sum_bf16x8(fa[ks][i], rsum[i]);
+    }
 #pragma unroll
     for (int i = 0; i < kTM16; ++i)
 #pragma unroll
@@ -804,6 +824,18 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   }
 
   block_barrier();  // every wave is done with the main loop's LDS
+  if constexpr (RS) {
+    // lanes l, l + 16, l + 32, l + 48 hold the same row's k groups; the four
+    // waves of the first tile column (wn = 0) cover the tile's 256 rows
+#pragma unroll
+    for (int i = 0; i < kTM16; ++i) {
+      float v = rsum[i];
+      v += __shfl_xor(v, 16, 64);
+      v += __shfl_xor(v, 32, 64);
+      const int m = m0 + wm + 16 * i + (lane & 15);
+      if (wn == 0 && lane < 16 && m < M) ep.rowsum[m] = v;
+    }
+  }
   unsigned char* buf = smem + wave * kEpiWaveLds;
   if (slice >= 0) {
     // partial tile of one K-slice, stored whole (bounds are applied on reduce)
@@ -857,13 +889,24 @@ template <bool AK1, bool BK1, Epi E1, bool AK2, bool BK2, Epi E2, bool GT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_pair(DmaGemm g1, int tiles1,
                                                                   DmaGemm g2, int tiles2) {
   const int b = (int)blockIdx.x;
-  if (b < tiles1)
+  if (b < tiles1) {
     dma_gemm_item<AK1, BK1, E1, GT>(g1.A, g1.lda, g1.B, g1.ldb, g1.M, g1.N, g1.ep,
                                     xcd_remap(b, tiles1), -1, 0, g1.K / kBK, tiles1, 1, nullptr);
-  else
-    dma_gemm_item<AK2, BK2, E2, GT>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep,
-                                    xcd_remap(b - tiles1, tiles2), -1, 0, g2.K / kBK, tiles2, 1,
-                                    nullptr);
+    return;
+  }
+  const int lid = xcd_remap(b - tiles1, tiles2);
+  if constexpr (E2 == Epi::StoreF32) {
+    // the second GEMM's row sums, when asked for, from its first tile column
+    int tm, tn;
+    tile_of(lid, (g2.M + kBM - 1) / kBM, (g2.N + kBN - 1) / kBN, tm, tn);
+    if (g2.ep.rowsum && tn == 0) {
+      dma_gemm_item<AK2, BK2, E2, GT, true>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep, lid, -1,
+                                            0, g2.K / kBK, tiles2, 1, nullptr);
+      return;
+    }
+  }
+  dma_gemm_item<AK2, BK2, E2, GT>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep, lid, -1, 0,
+                                  g2.K / kBK, tiles2, 1, nullptr);
 }
 
 // Sum of the K-slice partials of each tail tile, in slice order (so the

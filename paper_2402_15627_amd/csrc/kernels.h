@@ -125,6 +125,9 @@ struct EpiArgs {
   int ld_o_rows = 0;
   float* delta = nullptr;
   int delta_seq = 0, delta_heads = 0, delta_hd = 0;
+  // StoreF32 as the second GEMM of launch_gemm_pair only: when set, also
+  // rowsum[m] = sum over k of A(m, k) (fp32), for every row m < M.
+  float* rowsum = nullptr;
 };
 // 64-column groups of the LnGrad row terms for a row of n columns.
 inline int ln_row_groups(int n) { return (n + 63) / 64; }

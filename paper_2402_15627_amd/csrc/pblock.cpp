@@ -657,6 +657,10 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   // their own: heads of 64 or 128 columns whose blocks align with the
   // epilogue's 128-column wave blocks.
   const bool delta_in_dc = pair_out && (d.d == 64 || d.d == 128) && A % 128 == 0;
+  // db_in = sum over tokens of dZ: the row sums of dW_in's A operand (dZ^T),
+  // formed by the shared launch's first tile column of dW_in
+  const bool pair_in = pb::gemm_pair_supported(dt, g_dh, g_dwi);
+  if (pair_in) G.dw_in.ep.rowsum = db_in;
   if (delta_in_dc) {
     G.dc.ep.o_rows = c;  // O = C[:, :A]
     G.dc.ep.ld_o_rows = K_out;
@@ -682,7 +686,6 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   // B4: dh = dZ W_in, stored in the activation type; its epilogue also forms
   // the LayerNorm backward's row terms (sums of gamma dh and gamma dh xhat per
   // 64 columns) from the fp32 accumulators
-  const bool pair_in = pb::gemm_pair_supported(dt, g_dh, g_dwi);
   {
     StepScope sc(step_ev, PB_STEP_DH, stream);  // with dW_in when they share a launch
     if (pair_in)
@@ -703,10 +706,11 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   {
     StepScope sc(step_ev, PB_STEP_DB_OUT, stream);  // now inside the LN backward's column sums
   }
-  // db_in = sum over tokens of dZ
+  // db_in = sum over tokens of dZ (already formed in dW_in's launch when
+  // it shared dh's)
   {
     StepScope sc(step_ev, PB_STEP_DB_IN, stream);
-    pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+    if (!pair_in) pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
   }
   {
     StepScope sc(step_ev, PB_STEP_DW_OUT, stream);  // empty when it shared dC's launch
