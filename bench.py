@@ -639,6 +639,69 @@ def time_rs(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
     return {"tp": tp, "n_comm": n_comm, "chunk_bytes": rows * H * partial.element_size(), **out}
 
 
+def time_bwd_overlap(pb, shape, dev, warmup, steps, tp=8, n_comm=2):
+    """The backward pass's mirror of the two overlaps: the dC GEMM pipelined
+    with the all-gather of dy (pblock_ag_dc) and the dh GEMM pipelined with
+    the reduce-scatter of its partial sums (pblock_rs_dh), each against the
+    GEMM alone and the unpipelined order, timed like time_ag / time_rs."""
+    import torch
+    T, H = shape.tokens, shape.hidden
+    cfg = pb.config_from_shape(shape)
+    act = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    rows = T // tp
+    src = torch.randn(T, H, device="cuda").to(act)
+    dy = torch.empty_like(src)
+    z = torch.randn(T, shape.n_in, device="cuda").to(act)
+    d_o = torch.empty(T, shape.attn_width, dtype=act, device="cuda")
+    dz = torch.randn(T, shape.n_in, device="cuda").to(act)
+    w_in_t = dev["w_in"]  # [N_in, H]: dh = dZ W_in
+    partial = torch.empty(T, H, dtype=act, device="cuda")
+    recv = torch.empty(tp, rows, H, dtype=act, device="cuda")
+    stream = torch.cuda.Stream()
+    comm = [torch.cuda.Stream() for _ in range(n_comm)]
+    ctx = pb.TpContext(tp)
+
+    def timed(call):
+        for _ in range(warmup):
+            call()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return round(e0.elapsed_time(e1) / steps, 4)
+
+    def ag(per, in_place):
+        nws = pb.pblock_ag_dc_workspace_bytes(cfg, tp, per)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
+        dy.copy_(src)
+        shards = [dy[j * rows:(j + 1) * rows] if (in_place or j == 0) else
+                  src[j * rows:(j + 1) * rows] for j in range(tp)]
+        torch.cuda.synchronize()
+        return lambda: pb.pblock_ag_dc(cfg, tp, 0, shards, dy, dev["w_out"], z, d_o, dz, per, ws,
+                                       stream, comm, ctx)
+
+    def rs(per, in_place):
+        nws = pb.pblock_rs_dh_workspace_bytes(cfg, tp, per)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
+        dst = [partial[j * rows:(j + 1) * rows] if (in_place or j == 0) else recv[j]
+               for j in range(tp)]
+        return lambda: pb.pblock_rs_dh(cfg, tp, 0, dz, w_in_t, partial, dst, per, ws, stream,
+                                       comm, ctx)
+
+    out = {"tp": tp, "n_comm": n_comm, "shard_bytes": rows * H * src.element_size()}
+    agd = {"gemm_only_ms": timed(ag(tp, True)), "copies_then_gemm_ms": timed(ag(tp, False))}
+    rsd = {"gemm_only_ms": timed(rs(tp, True)), "gemm_then_copies_ms": timed(rs(tp, False))}
+    for per in (1, 2, 4):
+        agd[f"pipelined_{per}_shards_per_launch_ms"] = timed(ag(per, False))
+        rsd[f"pipelined_{per}_shards_per_launch_ms"] = timed(rs(per, False))
+    ctx.close()
+    return {**out, "ag_dc": agd, "rs_dh": rsd}
+
+
 def time_serial(pb, shape, warmup, steps, parallel_ms, flops):
     """The standard block (two LayerNorms, four projections; the same model
     FLOPs) on the same workload and kernels, timed like the parallel block:
@@ -883,6 +946,7 @@ def main():
     if not args.no_ag:
         out["ag_in_proj"] = time_ag(pb, shape, dev, 2, 5)
         out["rs_out_proj"] = time_rs(pb, shape, dev, 2, 5)
+        out["bwd_overlap"] = time_bwd_overlap(pb, shape, dev, 2, 5)
     if not args.no_lamb:
         names = ("w_in", "b_in", "w_out", "b_out", "gamma", "beta")
         gmap = dict(zip(names, (blk.grads[k] for k in ("dw_in", "db_in", "dw_out", "db_out",

@@ -405,6 +405,27 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
                             const hipStream_t* comm_streams,
                             pb_tp_context* ctx);
 
+/* The same overlap in the backward pass (the mirror of the forward's
+ * reduce-scatter): the output gradient dy arrives sharded along the tokens
+ * and is all-gathered before dC = dy W_out, the first GEMM of the backward.
+ * pblock_ag_dc copies dy_shards[j] ([T / tp, H], rank j's rows) into dy
+ * [T, H] exactly as pblock_ag_in_proj copies the LayerNorm shards, and runs
+ * dC over groups of shards_per_launch landed shards, writing d_o [T, A]
+ * (= dC[:, :A]) and the MLP part of dz [T, N_in] (dz[:, 3A:] = dC[:, A:] *
+ * gelu'(U), U read from z [T, N_in], the stash's Z) as pblock_backward
+ * writes them.  w_out [H, K_out] as in pblock_forward.  Requirements, ws
+ * (pblock_ag_dc_workspace_bytes) and ctx as for pblock_ag_in_proj.  The
+ * weight gradient dW_out = dy^T C needs every shard and is left to the
+ * caller (after the call, dy holds them all). */
+size_t pblock_ag_dc_workspace_bytes(const pb_config* cfg, int tp,
+                                    int shards_per_launch);
+pb_status pblock_ag_dc(const pb_config* cfg, int tp, int rank,
+                       const void* const* dy_shards, void* dy,
+                       const void* w_out, const void* z, void* d_o, void* dz,
+                       int shards_per_launch, void* ws, size_t ws_bytes,
+                       hipStream_t stream, int n_comm,
+                       const hipStream_t* comm_streams, pb_tp_context* ctx);
+
 /* --------------------------------------- out-projection + reduce-scatter
  * Section 3.2 ("Overlapping in tensor/sequence parallelism", Fig. 3), the
  * other half of the pattern above: after the row-parallel out-projection
@@ -434,7 +455,8 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank,
  * pblock_rs_reduce (the receiving side of one rank): y_shard = x_shard +
  * b_out + sum over q = 0 .. tp-1 of parts[q], summed in fp32 in the order
  * of q and rounded once; parts[q], x_shard, y_shard: [T / tp, H] in the
- * activation dtype, 16-byte aligned; b_out: [H].  With parts[q] the chunk
+ * activation dtype, 16-byte aligned; b_out: [H].  x_shard and b_out may
+ * each be NULL (left out of the sum).  With parts[q] the chunk
  * rank q sent here, y_shard is this rank's rows of the block output of
  * Eq. 2 (the out-projection of all ranks, the bias and the residual). */
 size_t pblock_rs_out_proj_workspace_bytes(const pb_config* cfg, int tp,
@@ -445,6 +467,24 @@ pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank,
                              size_t ws_bytes, hipStream_t stream, int n_comm,
                              const hipStream_t* comm_streams,
                              pb_tp_context* ctx);
+
+/* The backward's mirror of the forward's all-gather: the column-parallel
+ * in-projection leaves every rank a partial sum of the LayerNorm output's
+ * gradient, dh_r = dZ_r W_in,r (dZ_r, W_in,r: its own columns of dZ and
+ * rows of W_in), and a reduce-scatter leaves rank j the sum of its own rows
+ * (the sequence-parallel dh that the LayerNorm backward of its shard needs).
+ * pblock_rs_dh computes dh_r = dz [T, N_in] w_in [N_in, H] into partial
+ * [T, H] (activation dtype) in row chunks and sends them to dst exactly as
+ * pblock_rs_out_proj does; the receiving side is pblock_rs_reduce with
+ * x_shard = b_out = NULL.  Requirements, ws (pblock_rs_dh_workspace_bytes)
+ * and ctx as for pblock_rs_out_proj. */
+size_t pblock_rs_dh_workspace_bytes(const pb_config* cfg, int tp,
+                                    int shards_per_launch);
+pb_status pblock_rs_dh(const pb_config* cfg, int tp, int rank, const void* dz,
+                       const void* w_in, void* partial, void* const* dst,
+                       int shards_per_launch, void* ws, size_t ws_bytes,
+                       hipStream_t stream, int n_comm,
+                       const hipStream_t* comm_streams, pb_tp_context* ctx);
 pb_status pblock_rs_reduce(const pb_config* cfg, int tp,
                            const void* const* parts, const void* x_shard,
                            const void* b_out, void* y_shard,

@@ -1211,21 +1211,8 @@ void pblock_tp_context_destroy(pb_tp_context* ctx) {
   delete ctx;
 }
 
-// -------------------------------------------- in-projection + all-gather
+// ------------------------- all-gather / reduce-scatter pipelined with GEMMs
 namespace {
-
-// Largest GEMM split region over the launches of one call: row ranges of
-// m whole shards, m = 1 .. per_launch.
-size_t ag_split_bytes(const pb_config* cfg, int tp, int per_launch) {
-  const Dims d = dims_of(cfg);
-  const int rows = (int)(d.T / tp);
-  size_t m = 0;
-  for (int k = 1; k <= per_launch; ++k)
-    m = std::max(m, pb::gemm_split_floats(
-                        pb::gemm_split_plan(dt_of(cfg), rows * k, (int)d.N_in, (int)d.H)) *
-                        4);
-  return align256(m);
-}
 pb_status check_tp_streams(int tp, int rank, long long T, int per_launch, int n_comm,
                            const hipStream_t* comm_streams, hipStream_t stream) {
   if (tp < 1 || tp > kAgMaxTp) return fail(PB_ERR_INVALID_ARG, "tp=%d must be in 1..64", tp);
@@ -1260,83 +1247,54 @@ pb_status check_ctx(const pb_tp_context* ctx, int tp) {
 }
 }  // namespace
 
-size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
-  if (check_config(cfg) != PB_OK || tp < 1 || tp > kAgMaxTp || shards_per_launch < 1 ||
-      shards_per_launch > tp || dims_of(cfg).T % tp)
-    return 0;
-  return ag_split_bytes(cfg, tp, shards_per_launch);
+}  // extern "C"
+
+namespace {
+// Largest GEMM split region over the launches of a pipelined call: row
+// ranges of m whole shards, m = 1 .. per_launch, of an (rows m) x N x K GEMM.
+size_t rows_split_bytes(pb::Dt dt, int rows, int N, int K, int per_launch) {
+  size_t m = 0;
+  for (int k = 1; k <= per_launch; ++k)
+    m = std::max(m, pb::gemm_split_floats(pb::gemm_split_plan(dt, rows * k, N, K)) * 4);
+  return align256(m);
+}
+bool tp_args_ok(const pb_config* cfg, int tp, int per_launch) {
+  return check_config(cfg) == PB_OK && tp >= 1 && tp <= kAgMaxTp && per_launch >= 1 &&
+         per_launch <= tp && dims_of(cfg).T % tp == 0;
 }
 
-pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* const* shards,
-                            void* h, const void* w_in, const void* b_in, void* z, void* c,
-                            int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
-                            int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
-  PB_CHECK(check_config(cfg));
-  const Dims d = dims_of(cfg);
-  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
-  if (!shards) return fail(PB_ERR_INVALID_ARG, "shards is NULL");
-  for (int j = 0; j < tp; ++j) {
-    if (!shards[j] || (uintptr_t)shards[j] % 16)
-      return fail(PB_ERR_INVALID_ARG, "shards[%d] is NULL or not 16-byte aligned", j);
-  }
-  PB_CHECK(check_ptr(h, "h"));
-  PB_CHECK(check_ptr(w_in, "w_in"));
-  PB_CHECK(check_ptr(b_in, "b_in"));
-  PB_CHECK(check_ptr(z, "z"));
-  PB_CHECK(check_ptr(c, "c"));
-  if (ws_bytes && (!ws || (uintptr_t)ws % 256))
-    return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
-  PB_CHECK(check_ctx(ctx, tp));
-  pb_tp_context& ev = *ctx;
+// All-gather pipelined into a row-parallel GEMM: the shards are copied into
+// `gathered` on the comm streams in ring order from `rank` (the k-th on
+// comm_streams[k % n_comm]); gemm_rows(j0, n) computes the GEMM over the
+// rows of shards j0 .. j0 + n - 1 on `stream`, each launch of per_launch
+// shards waiting (by event) only for its own.  Shards already in place at
+// the head of that order are not copied and form a first launch of their
+// own unless the call is unpipelined.
+template <class F>
+pb_status ag_pipeline(int tp, int rank, const void* const* shards, void* gathered,
+                      size_t shard_bytes, int per_launch, hipStream_t stream, int n_comm,
+                      const hipStream_t* comm_streams, pb_tp_context& ev, F gemm_rows) {
   auto ok = [](hipError_t e) { return e == hipSuccess; };
-
-  const pb::Dt dt = dt_of(cfg);
-  const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
-  const int rows = T / tp;
-  const size_t e = d.esz;
-  const size_t shard_bytes = (size_t)rows * H * e;
   // the copies start after the work already on `stream` (which may produce
   // the local shard)
   if (!ok(hipEventRecord(ev.start, stream))) return fail(PB_ERR_HIP, "hipEventRecord failed");
   for (int i = 0; i < n_comm; ++i)
     if (!ok(hipStreamWaitEvent(comm_streams[i], ev.start, 0)))
       return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
-  // shards in ring order from this rank, round-robin over the comm streams
+  auto in_place = [&](int j) {
+    return shards[j] == (const char*)gathered + (size_t)j * shard_bytes;
+  };
   for (int k = 0; k < tp; ++k) {
     const int j = (rank + k) % tp;
     hipStream_t cs = comm_streams[k % n_comm];
-    char* dst = (char*)h + (size_t)j * shard_bytes;
-    if (shards[j] != dst &&
+    char* dst = (char*)gathered + (size_t)j * shard_bytes;
+    if (!in_place(j) &&
         !ok(hipMemcpyAsync(dst, shards[j], shard_bytes, hipMemcpyDeviceToDeviceNoCU, cs)))
       return fail(PB_ERR_HIP, "hipMemcpyAsync of shard %d failed", j);
     if (!ok(hipEventRecord(ev.landed[k], cs))) return fail(PB_ERR_HIP, "hipEventRecord failed");
   }
-  // the in-projection over groups of shards_per_launch shards in arrival
-  // order, each launch on `stream` once its shards have landed (a group that
-  // wraps past the last rank is two row ranges)
-  float* split_ws = (float*)ws;
-  const size_t split_f = ws_bytes / 4;
-  auto gemm_rows = [&](int j0, int nsh) {
-    const int r0 = j0 * rows, m = nsh * rows;
-    pb::EpiArgs e1;
-    e1.out = at(z, (long long)r0 * N_in, e);
-    e1.ld_out = N_in;
-    e1.out2 = at(c, (long long)r0 * K_out, e);
-    e1.ld_out2 = K_out;
-    e1.bias = b_in;
-    e1.split = 3 * A;
-    e1.col2 = A;
-    e1.gelu_tanh = cfg->gelu_tanh;
-    pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, at(h, (long long)r0 * H, e), H, w_in, H,
-                    m, N_in, H, e1, split_ws, split_f, stream);
-  };
-  // Shards already in place at the head of the ring order (this rank's own
-  // LayerNorm output, typically) need no copy: unless the call is unpipelined
-  // they form a first launch of their own, which runs while the first copies
-  // land; the rest go in groups of shards_per_launch.
   int ready = 0;
-  while (ready < tp && shards[(rank + ready) % tp] == (char*)h + (size_t)((rank + ready) % tp) * shard_bytes)
-    ++ready;
+  while (ready < tp && in_place((rank + ready) % tp)) ++ready;
   auto launch_group = [&](int k0, int k1, bool wait) -> bool {
     if (wait)
       for (int k = k0; k < k1; ++k)
@@ -1351,83 +1309,30 @@ pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* 
     return true;
   };
   int k0 = 0;
-  if (ready > 0 && ready < tp && shards_per_launch < tp) {
+  if (ready > 0 && ready < tp && per_launch < tp) {
     if (!launch_group(0, ready, false)) return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
     k0 = ready;
   }
-  for (; k0 < tp; k0 += shards_per_launch)
-    if (!launch_group(k0, std::min(tp, k0 + shards_per_launch), true))
+  for (; k0 < tp; k0 += per_launch)
+    if (!launch_group(k0, std::min(tp, k0 + per_launch), true))
       return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
-  return finish_launches();
+  return PB_OK;
 }
 
-// --------------------------------------- out-projection + reduce-scatter
-namespace {
-size_t rs_split_bytes(const pb_config* cfg, int tp, int per_launch) {
-  const Dims d = dims_of(cfg);
-  const int rows = (int)(d.T / tp);
-  size_t m = 0;
-  for (int k = 1; k <= per_launch; ++k)
-    m = std::max(m, pb::gemm_split_floats(
-                        pb::gemm_split_plan(dt_of(cfg), rows * k, (int)d.H, (int)d.K_out)) *
-                        4);
-  return align256(m);
-}
-
-}  // namespace
-
-size_t pblock_rs_out_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
-  if (check_config(cfg) != PB_OK || tp < 1 || tp > kAgMaxTp || shards_per_launch < 1 ||
-      shards_per_launch > tp || dims_of(cfg).T % tp)
-    return 0;
-  return rs_split_bytes(cfg, tp, shards_per_launch);
-}
-
-pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank, const void* c,
-                             const void* w_out, void* partial, void* const* dst,
-                             int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
-                             int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
-  PB_CHECK(check_config(cfg));
-  const Dims d = dims_of(cfg);
-  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
-  if (!dst) return fail(PB_ERR_INVALID_ARG, "dst is NULL");
-  for (int j = 0; j < tp; ++j) {
-    if (!dst[j] || (uintptr_t)dst[j] % 16)
-      return fail(PB_ERR_INVALID_ARG, "dst[%d] is NULL or not 16-byte aligned", j);
-  }
-  PB_CHECK(check_ptr(c, "c"));
-  PB_CHECK(check_ptr(w_out, "w_out"));
-  PB_CHECK(check_ptr(partial, "partial"));
-  if (ws_bytes && (!ws || (uintptr_t)ws % 256))
-    return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
-  PB_CHECK(check_ctx(ctx, tp));
-  pb_tp_context& ev = *ctx;
+// A row-parallel GEMM pipelined into a reduce-scatter: gemm_rows(j0, n)
+// writes the rows of chunks j0 .. j0 + n - 1 of `partial` on `stream`, in
+// ring order from rank + 1 (this rank's own chunk last), per_launch chunks
+// per launch; chunk j goes to dst[j] on comm_streams[k % n_comm] (k its
+// position) as soon as its launch has finished.  Later work on `stream`
+// follows every send.
+template <class F>
+pb_status rs_pipeline(int tp, int rank, const void* partial, void* const* dst, size_t chunk_bytes,
+                      int per_launch, hipStream_t stream, int n_comm,
+                      const hipStream_t* comm_streams, pb_tp_context& ev, F gemm_rows) {
   auto ok = [](hipError_t e) { return e == hipSuccess; };
-
-  const pb::Dt dt = dt_of(cfg);
-  const int H = (int)d.H, K_out = (int)d.K_out;
-  const int rows = (int)(d.T / tp);
-  const size_t e = d.esz;
-  const size_t chunk_bytes = (size_t)rows * H * e;
-  float* split_ws = (float*)ws;
-  const size_t split_f = ws_bytes / 4;
-  // P = C W_out^T over a row range, stored in the activation type
-  auto gemm_rows = [&](int j0, int nsh) {
-    const int r0 = j0 * rows, m = nsh * rows;
-    pb::EpiArgs ep;
-    ep.out = at(partial, (long long)r0 * H, e);
-    ep.ld_out = H;
-    ep.split = H;  // every column is a plain store
-    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, true, at(c, (long long)r0 * K_out, e), K_out,
-                    w_out, K_out, m, H, K_out, ep, split_ws, split_f, stream);
-  };
-  // chunks in ring order from rank + 1, so this rank's own rows come last;
-  // each group of shards_per_launch chunks is one launch (two row ranges
-  // when it wraps past the last rank), and each chunk is sent on its comm
-  // stream as soon as its launch has finished
   int group = 0;
-  for (int k0 = 0; k0 < tp; k0 += shards_per_launch, ++group) {
-    const int k1 = std::min(tp, k0 + shards_per_launch);
+  for (int k0 = 0; k0 < tp; k0 += per_launch, ++group) {
+    const int k1 = std::min(tp, k0 + per_launch);
     const int j0 = (rank + 1 + k0) % tp, n = k1 - k0;
     if (j0 + n <= tp) {
       gemm_rows(j0, n);
@@ -1449,10 +1354,201 @@ pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank, const void*
       if (!ok(hipEventRecord(ev.sent[k], cs))) return fail(PB_ERR_HIP, "hipEventRecord failed");
     }
   }
-  // later work on `stream` follows every send
   for (int k = 0; k < tp; ++k)
     if (!ok(hipStreamWaitEvent(stream, ev.sent[k], 0)))
       return fail(PB_ERR_HIP, "hipStreamWaitEvent failed");
+  return PB_OK;
+}
+
+pb_status check_list(const void* const* p, int n, const char* name) {
+  if (!p) return fail(PB_ERR_INVALID_ARG, "%s is NULL", name);
+  for (int j = 0; j < n; ++j)
+    if (!p[j] || (uintptr_t)p[j] % 16)
+      return fail(PB_ERR_INVALID_ARG, "%s[%d] is NULL or not 16-byte aligned", name, j);
+  return PB_OK;
+}
+pb_status check_ws(const void* ws, size_t ws_bytes) {
+  if (ws_bytes && (!ws || (uintptr_t)ws % 256))
+    return fail(PB_ERR_INVALID_ARG, "ws is NULL or not 256-byte aligned");
+  return PB_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t pblock_ag_in_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
+  if (!tp_args_ok(cfg, tp, shards_per_launch)) return 0;
+  const Dims d = dims_of(cfg);
+  return rows_split_bytes(dt_of(cfg), (int)(d.T / tp), (int)d.N_in, (int)d.H, shards_per_launch);
+}
+
+pb_status pblock_ag_in_proj(const pb_config* cfg, int tp, int rank, const void* const* shards,
+                            void* h, const void* w_in, const void* b_in, void* z, void* c,
+                            int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
+                            int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
+  PB_CHECK(check_list(shards, tp, "shards"));
+  PB_CHECK(check_ptr(h, "h"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(b_in, "b_in"));
+  PB_CHECK(check_ptr(z, "z"));
+  PB_CHECK(check_ptr(c, "c"));
+  PB_CHECK(check_ws(ws, ws_bytes));
+  PB_CHECK(check_ctx(ctx, tp));
+  const pb::Dt dt = dt_of(cfg);
+  const int H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  const int rows = (int)(d.T / tp);
+  const size_t e = d.esz;
+  float* split_ws = (float*)ws;
+  const size_t split_f = ws_bytes / 4;
+  // the in-projection of rows of h: Z (bias) and G = gelu(U) as the forward
+  auto gemm_rows = [&](int j0, int nsh) {
+    const int r0 = j0 * rows, m = nsh * rows;
+    pb::EpiArgs e1;
+    e1.out = at(z, (long long)r0 * N_in, e);
+    e1.ld_out = N_in;
+    e1.out2 = at(c, (long long)r0 * K_out, e);
+    e1.ld_out2 = K_out;
+    e1.bias = b_in;
+    e1.split = 3 * A;
+    e1.col2 = A;
+    e1.gelu_tanh = cfg->gelu_tanh;
+    pb::launch_gemm(dt, pb::Epi::BiasGelu, true, true, at(h, (long long)r0 * H, e), H, w_in, H,
+                    m, N_in, H, e1, split_ws, split_f, stream);
+  };
+  PB_CHECK(ag_pipeline(tp, rank, shards, h, (size_t)rows * H * e, shards_per_launch, stream,
+                       n_comm, comm_streams, *ctx, gemm_rows));
+  return finish_launches();
+}
+
+size_t pblock_ag_dc_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
+  if (!tp_args_ok(cfg, tp, shards_per_launch)) return 0;
+  const Dims d = dims_of(cfg);
+  return rows_split_bytes(dt_of(cfg), (int)(d.T / tp), (int)d.K_out, (int)d.H, shards_per_launch);
+}
+
+pb_status pblock_ag_dc(const pb_config* cfg, int tp, int rank, const void* const* dy_shards,
+                       void* dy, const void* w_out, const void* z, void* d_o, void* dz,
+                       int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
+                       int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
+  PB_CHECK(check_list(dy_shards, tp, "dy_shards"));
+  PB_CHECK(check_ptr(dy, "dy"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(z, "z"));
+  PB_CHECK(check_ptr(d_o, "d_o"));
+  PB_CHECK(check_ptr(dz, "dz"));
+  PB_CHECK(check_ws(ws, ws_bytes));
+  PB_CHECK(check_ctx(ctx, tp));
+  const pb::Dt dt = dt_of(cfg);
+  const int H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
+  const int rows = (int)(d.T / tp);
+  const size_t e = d.esz;
+  float* split_ws = (float*)ws;
+  const size_t split_f = ws_bytes / 4;
+  // dC = dy W_out over rows of dy: dO = dC[:, :A], dU = dC[:, A:] * gelu'(U)
+  // -> dZ[:, 3A:], as the backward pass writes them
+  auto gemm_rows = [&](int j0, int nsh) {
+    const int r0 = j0 * rows, m = nsh * rows;
+    pb::EpiArgs e1;
+    e1.out = at(d_o, (long long)r0 * A, e);
+    e1.ld_out = A;
+    e1.out2 = at(dz, (long long)r0 * N_in, e);
+    e1.ld_out2 = N_in;
+    e1.aux = at(z, (long long)r0 * N_in, e);
+    e1.split = A;
+    e1.col2 = 3 * A;
+    e1.gelu_tanh = cfg->gelu_tanh;
+    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, at(dy, (long long)r0 * H, e), H, w_out,
+                    K_out, m, K_out, H, e1, split_ws, split_f, stream);
+  };
+  PB_CHECK(ag_pipeline(tp, rank, dy_shards, dy, (size_t)rows * H * e, shards_per_launch, stream,
+                       n_comm, comm_streams, *ctx, gemm_rows));
+  return finish_launches();
+}
+
+size_t pblock_rs_out_proj_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
+  if (!tp_args_ok(cfg, tp, shards_per_launch)) return 0;
+  const Dims d = dims_of(cfg);
+  return rows_split_bytes(dt_of(cfg), (int)(d.T / tp), (int)d.H, (int)d.K_out, shards_per_launch);
+}
+
+pb_status pblock_rs_out_proj(const pb_config* cfg, int tp, int rank, const void* c,
+                             const void* w_out, void* partial, void* const* dst,
+                             int shards_per_launch, void* ws, size_t ws_bytes, hipStream_t stream,
+                             int n_comm, const hipStream_t* comm_streams, pb_tp_context* ctx) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
+  PB_CHECK(check_list(dst, tp, "dst"));
+  PB_CHECK(check_ptr(c, "c"));
+  PB_CHECK(check_ptr(w_out, "w_out"));
+  PB_CHECK(check_ptr(partial, "partial"));
+  PB_CHECK(check_ws(ws, ws_bytes));
+  PB_CHECK(check_ctx(ctx, tp));
+  const pb::Dt dt = dt_of(cfg);
+  const int H = (int)d.H, K_out = (int)d.K_out;
+  const int rows = (int)(d.T / tp);
+  const size_t e = d.esz;
+  float* split_ws = (float*)ws;
+  const size_t split_f = ws_bytes / 4;
+  // P = C W_out^T over a row range, stored in the activation type
+  auto gemm_rows = [&](int j0, int nsh) {
+    const int r0 = j0 * rows, m = nsh * rows;
+    pb::EpiArgs ep;
+    ep.out = at(partial, (long long)r0 * H, e);
+    ep.ld_out = H;
+    ep.split = H;  // every column is a plain store
+    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, true, at(c, (long long)r0 * K_out, e), K_out,
+                    w_out, K_out, m, H, K_out, ep, split_ws, split_f, stream);
+  };
+  PB_CHECK(rs_pipeline(tp, rank, partial, dst, (size_t)rows * H * e, shards_per_launch, stream,
+                       n_comm, comm_streams, *ctx, gemm_rows));
+  return finish_launches();
+}
+
+size_t pblock_rs_dh_workspace_bytes(const pb_config* cfg, int tp, int shards_per_launch) {
+  if (!tp_args_ok(cfg, tp, shards_per_launch)) return 0;
+  const Dims d = dims_of(cfg);
+  return rows_split_bytes(dt_of(cfg), (int)(d.T / tp), (int)d.H, (int)d.N_in, shards_per_launch);
+}
+
+pb_status pblock_rs_dh(const pb_config* cfg, int tp, int rank, const void* dz, const void* w_in,
+                       void* partial, void* const* dst, int shards_per_launch, void* ws,
+                       size_t ws_bytes, hipStream_t stream, int n_comm,
+                       const hipStream_t* comm_streams, pb_tp_context* ctx) {
+  PB_CHECK(check_config(cfg));
+  const Dims d = dims_of(cfg);
+  PB_CHECK(check_tp_streams(tp, rank, d.T, shards_per_launch, n_comm, comm_streams, stream));
+  PB_CHECK(check_list(dst, tp, "dst"));
+  PB_CHECK(check_ptr(dz, "dz"));
+  PB_CHECK(check_ptr(w_in, "w_in"));
+  PB_CHECK(check_ptr(partial, "partial"));
+  PB_CHECK(check_ws(ws, ws_bytes));
+  PB_CHECK(check_ctx(ctx, tp));
+  const pb::Dt dt = dt_of(cfg);
+  const int H = (int)d.H, N_in = (int)d.N_in;
+  const int rows = (int)(d.T / tp);
+  const size_t e = d.esz;
+  float* split_ws = (float*)ws;
+  const size_t split_f = ws_bytes / 4;
+  // this rank's partial dh = dZ W_in over a row range (W_in's rows are
+  // MN-contiguous here), stored in the activation type
+  auto gemm_rows = [&](int j0, int nsh) {
+    const int r0 = j0 * rows, m = nsh * rows;
+    pb::EpiArgs ep;
+    ep.out = at(partial, (long long)r0 * H, e);
+    ep.ld_out = H;
+    ep.split = H;  // every column is a plain store
+    pb::launch_gemm(dt, pb::Epi::DgeluSplit, true, false, at(dz, (long long)r0 * N_in, e), N_in,
+                    w_in, H, m, H, N_in, ep, split_ws, split_f, stream);
+  };
+  PB_CHECK(rs_pipeline(tp, rank, partial, dst, (size_t)rows * H * e, shards_per_launch, stream,
+                       n_comm, comm_streams, *ctx, gemm_rows));
   return finish_launches();
 }
 
@@ -1472,8 +1568,9 @@ pb_status pblock_rs_reduce(const pb_config* cfg, int tp, const void* const* part
       return fail(PB_ERR_INVALID_ARG, "parts[%d] is NULL or not 16-byte aligned", q);
     rp.p[q] = parts[q];
   }
-  PB_CHECK(check_ptr(x_shard, "x_shard"));
-  PB_CHECK(check_ptr(b_out, "b_out"));
+  // x_shard and b_out may be NULL (the sum alone: the backward's dh)
+  if (x_shard) PB_CHECK(check_ptr(x_shard, "x_shard"));
+  if (b_out) PB_CHECK(check_ptr(b_out, "b_out"));
   PB_CHECK(check_ptr(y_shard, "y_shard"));
   pb::launch_rs_reduce(dt_of(cfg), rp, x_shard, b_out, y_shard, (int)(d.T / tp), (int)d.H,
                        stream);

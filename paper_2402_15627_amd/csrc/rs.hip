@@ -2,7 +2,9 @@
 // (Section 3.2, tensor/sequence-parallel overlap; Megatron sequence
 // parallelism): each of tp ranks holds a partial sum C_r W_out,r^T of every
 // token row, and rank j keeps the sum over ranks of its own rows plus the
-// residual and the output bias, y = x + b_out + sum_r P_r.
+// residual and the output bias, y = x + b_out + sum_r P_r.  The same pass,
+// without x and b_out, sums the backward's partial LayerNorm-output
+// gradients dh_r.
 //
 // HBM-bound elementwise pass: every thread owns eight consecutive columns of
 // one row and adds the partials in rank order in fp32 (deterministic), then
@@ -26,10 +28,14 @@ __global__ __launch_bounds__(kRsThreads) void rs_reduce_kernel(RsParts parts, co
   const int r = (int)(g / groups), c = (int)(g % groups) * 8;
   const size_t off = (size_t)r * H + c;
   float acc[8], v[8];
-  load8<T>(x + off, acc);
-  load8<T>(bias + c, v);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] += v[e];
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  if (x) load8<T>(x + off, acc);
+  if (bias) {
+    load8<T>(bias + c, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += v[e];
+  }
   for (int q = 0; q < parts.n; ++q) {
     load8<T>((const T*)parts.p[q] + off, v);
 #pragma unroll

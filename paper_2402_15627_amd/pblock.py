@@ -40,6 +40,7 @@ EXPORTS = (
     "pblock_serial_backward", "pblock_lamb_workspace_bytes", "pblock_lamb_step",
     "pblock_ag_in_proj_workspace_bytes", "pblock_ag_in_proj",
     "pblock_rs_out_proj_workspace_bytes", "pblock_rs_out_proj", "pblock_rs_reduce",
+    "pblock_ag_dc_workspace_bytes", "pblock_ag_dc", "pblock_rs_dh_workspace_bytes", "pblock_rs_dh",
     "pblock_swattn_forward_noalloc",
 )
 NOALLOC_SCRATCH_BYTES = 32 << 20  # PB_NOALLOC_SCRATCH_BYTES
@@ -137,6 +138,12 @@ def load_library(path: str = LIB_PATH):
         "pblock_rs_out_proj": (c_int, [cfgp, c_int, c_int, P, P, P, POINTER(c_void_p), c_int, P,
                                        c_size_t, P, c_int, POINTER(c_void_p), P]),
         "pblock_rs_reduce": (c_int, [cfgp, c_int, POINTER(c_void_p), P, P, P, P]),
+        "pblock_ag_dc_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
+        "pblock_ag_dc": (c_int, [cfgp, c_int, c_int, POINTER(c_void_p), P, P, P, P, P, c_int, P,
+                                 c_size_t, P, c_int, POINTER(c_void_p), P]),
+        "pblock_rs_dh_workspace_bytes": (c_size_t, [cfgp, c_int, c_int]),
+        "pblock_rs_dh": (c_int, [cfgp, c_int, c_int, P, P, P, POINTER(c_void_p), c_int, P,
+                                 c_size_t, P, c_int, POINTER(c_void_p), P]),
         "pblock_lamb_step": (c_int, [POINTER(LambConfig), c_int, POINTER(LambTensor), c_int, P, P,
                                      c_size_t, P]),
     }
@@ -420,6 +427,44 @@ def pblock_rs_out_proj(cfg, tp, rank, c, w_out, partial, dst, shards_per_launch,
     cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
     _check(load_library().pblock_rs_out_proj(
         ctypes.byref(cfg), int(tp), int(rank), _ptr(c), _ptr(w_out), _ptr(partial), arr,
+        int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream), len(comm_streams), cs,
+        ctx.handle if ctx is not None else None))
+
+
+def pblock_ag_dc_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch: int) -> int:
+    return load_library().pblock_ag_dc_workspace_bytes(ctypes.byref(cfg), int(tp),
+                                                       int(shards_per_launch))
+
+
+def pblock_ag_dc(cfg, tp, rank, dy_shards, dy, w_out, z, d_o, dz, shards_per_launch, ws, stream,
+                 comm_streams, ctx):
+    """dy_shards: tp tensors (or addresses), rank j's rows of dy; dy is the
+    gathered [T, H]; comm_streams and ctx as for pblock_ag_in_proj."""
+    if len(dy_shards) != tp:
+        raise ValueError(f"{len(dy_shards)} shards for tp={tp}")
+    arr = (c_void_p * tp)(*[_ptr(t) for t in dy_shards])
+    cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
+    _check(load_library().pblock_ag_dc(
+        ctypes.byref(cfg), int(tp), int(rank), arr, _ptr(dy), _ptr(w_out), _ptr(z), _ptr(d_o),
+        _ptr(dz), int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream),
+        len(comm_streams), cs, ctx.handle if ctx is not None else None))
+
+
+def pblock_rs_dh_workspace_bytes(cfg: PbConfig, tp: int, shards_per_launch: int) -> int:
+    return load_library().pblock_rs_dh_workspace_bytes(ctypes.byref(cfg), int(tp),
+                                                       int(shards_per_launch))
+
+
+def pblock_rs_dh(cfg, tp, rank, dz, w_in, partial, dst, shards_per_launch, ws, stream,
+                 comm_streams, ctx):
+    """dst: tp tensors (or addresses), where rank j receives this rank's
+    chunk j of the partial dh; comm_streams and ctx as for pblock_ag_in_proj."""
+    if len(dst) != tp:
+        raise ValueError(f"{len(dst)} destinations for tp={tp}")
+    arr = (c_void_p * tp)(*[_ptr(t) for t in dst])
+    cs = (c_void_p * len(comm_streams))(*[_stream(x) for x in comm_streams])
+    _check(load_library().pblock_rs_dh(
+        ctypes.byref(cfg), int(tp), int(rank), _ptr(dz), _ptr(w_in), _ptr(partial), arr,
         int(shards_per_launch), _ptr(ws), _nbytes(ws), _stream(stream), len(comm_streams), cs,
         ctx.handle if ctx is not None else None))
 

@@ -358,6 +358,54 @@ def test_ag_in_proj_rejects_bad_arguments_before_launching():
     assert pb.pblock_ag_in_proj_workspace_bytes(c, 3, 1) == 0
 
 
+def test_backward_ag_and_rs_reject_bad_arguments_before_launching():
+    """pblock_ag_dc and pblock_rs_dh check what their forward counterparts
+    check, every other argument before the context."""
+    lib = pb.load_library()
+    c = good_cfg()  # 13B shape: T = 2048, H = 5120
+
+    def ag(cfg=c, tp=8, rank=0, per=1, stream=FAKE, comm=(FAKE + 256,), ws=FAKE, nbytes=1 << 20,
+           shards=None, dy=FAKE):
+        sh = (ctypes.c_void_p * tp)(*(shards or [FAKE] * tp)) if tp > 0 else None
+        cs = (ctypes.c_void_p * max(len(comm), 1))(*comm) if comm else None
+        return lib.pblock_ag_dc(ctypes.byref(cfg), tp, rank, sh, dy, FAKE, FAKE, FAKE, FAKE, per,
+                                ws, nbytes, stream, len(comm), cs, None)
+
+    def rs(cfg=c, tp=8, rank=0, per=1, stream=FAKE, comm=(FAKE + 256,), ws=FAKE, nbytes=1 << 20,
+           dst=None, dz=FAKE):
+        d = (ctypes.c_void_p * tp)(*(dst or [FAKE] * tp)) if tp > 0 else None
+        cs = (ctypes.c_void_p * max(len(comm), 1))(*comm) if comm else None
+        return lib.pblock_rs_dh(ctypes.byref(cfg), tp, rank, dz, FAKE, FAKE, d, per, ws, nbytes,
+                                stream, len(comm), cs, None)
+
+    for call, lst in ((ag, "shards"), (rs, "dst")):
+        assert call(tp=3) == 1 and "divisible" in pb.pblock_last_error()
+        assert call(tp=65) == 1
+        assert call(rank=8) == 1 and call(rank=-1) == 1
+        assert call(per=0) == 1 and call(per=9) == 1
+        assert call(comm=(FAKE,)) == 1
+        assert call(comm=(FAKE + 256, FAKE + 256)) == 1
+        assert call(comm=()) == 1
+        assert call(ws=FAKE + 16) == 1
+        assert call(cfg=good_cfg(head_dim=80)) == 2
+        assert call(**{lst: [FAKE] * 7 + [FAKE + 8]}) == 1
+        assert "[7]" in pb.pblock_last_error()
+        assert call() == 1 and "ctx" in pb.pblock_last_error()
+    assert ag(dy=None) == 1 and "dy" in pb.pblock_last_error()
+    assert rs(dz=None) == 1 and "dz" in pb.pblock_last_error()
+    for f in (pb.pblock_ag_dc_workspace_bytes, pb.pblock_rs_dh_workspace_bytes):
+        assert f(c, 8, 1) % 256 == 0 and f(c, 8, 9) == 0 and f(c, 3, 1) == 0
+    # dC over 2 shards of 256 rows: 2 x 100 = 200 tiles of K = 5120, fewer
+    # than the CUs: split along K (the small-grid plan)
+    assert pb.pblock_ag_dc_workspace_bytes(c, 8, 2) > 0
+    with pytest.raises(ValueError):
+        pb.pblock_ag_dc(c, 8, 0, [FAKE] * 7, FAKE, FAKE, FAKE, FAKE, FAKE, 1, None, FAKE,
+                        [FAKE + 256], None)
+    with pytest.raises(ValueError):
+        pb.pblock_rs_dh(c, 8, 0, FAKE, FAKE, FAKE, [FAKE] * 9, 1, None, FAKE, [FAKE + 256],
+                        None)
+
+
 def test_rs_out_proj_and_reduce_reject_bad_arguments_before_launching():
     lib = pb.load_library()
     c = good_cfg()  # 13B shape: T = 2048, H = 5120
