@@ -134,7 +134,7 @@ KERNEL_SOURCES = {
 }
 STEP_SOURCE = {"in_proj": "gemm", "out_proj": "gemm", "dc": "gemm", "dw_out": "gemm", "dh": "gemm",
                "dw_in": "gemm", "attn_fwd": "attn", "attn_bwd": "attn", "ln_fwd": "ln",
-               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln", "lamb": "lamb",
+               "ln_bwd": "ln", "db_out": "ln", "db_in": "ln", "lamb": "lamb", "ln": "ln",
                "dc+dw_out": "gemm", "dh+dw_in": "gemm"}
 COPY_BYTES = 1 << 30  # read and written once by the calibration copy
 
@@ -304,6 +304,49 @@ def lamb_traffic_summary(dirs, workload):
     rec["traffic_bytes"] = total
     rec["algorithmic_bytes"] = LAMB_BYTES_PER_ELEMENT * elements
     rec["source_fingerprint"] = source_fingerprint("lamb")
+    return rec
+
+
+def ln_traffic_summary(dirs, workload):
+    """FETCH_SIZE / WRITE_SIZE per dispatch of the LayerNorm kernels (forward,
+    backward apply, and the column sums of its partial rows), scaled by the
+    calibration copy, next to each kernel's algorithmic bytes: what it must
+    read and write once, its own partial rows included."""
+    from paper_2402_15627_amd.inputs import WORKLOADS
+    s = WORKLOADS[workload]
+    T, H = s.tokens, s.hidden
+    e = 2 if s.dtype == "bf16" else 4
+    chunks, ng = -(-T // 16), -(-H // 64)
+    copy_pick = lambda r: "neg_kernel" in r["Kernel_Name"]  # noqa: E731
+    cfetch, _ = _per_dispatch(_counter_rows(dirs[2]), "FETCH_SIZE", copy_pick)
+    cwrite, _ = _per_dispatch(_counter_rows(dirs[3]), "WRITE_SIZE", copy_pick)
+    ff, wf = COPY_BYTES / 1024 / cfetch, COPY_BYTES / 1024 / cwrite
+    kernels = {
+        # x read, h written, gamma and beta, the row statistics
+        "ln_fwd_wave_bf16": 2 * T * H * e + 2 * H * e + 8 * T,
+        # x, dh, dy read, dx written; statistics, the dh GEMM's row terms,
+        # gamma, and three fp32 partial rows per 16-row chunk
+        "ln_bwd_apply": 4 * T * H * e + 8 * T + 8 * T * ng + H * e + 3 * chunks * H * 4,
+        # the partial rows read, dgamma, dbeta, db_out written
+        "colsum_rows_f32": 3 * chunks * H * 4 + 3 * H * 4,
+    }
+    rec = {"step": "ln", "workload": workload, "copy_bytes": COPY_BYTES,
+           "copy_fetch_kib": round(cfetch, 1), "copy_write_kib": round(cwrite, 1),
+           "fetch_scale": round(ff, 4), "write_scale": round(wf, 4), "kernels": {}}
+    total = alg = 0
+    for kern, ab in kernels.items():
+        pick = lambda r, k=kern: k in r["Kernel_Name"]  # noqa: E731
+        fetch, n1 = _per_dispatch(_counter_rows(dirs[0]), "FETCH_SIZE", pick)
+        write, n2 = _per_dispatch(_counter_rows(dirs[1]), "WRITE_SIZE", pick)
+        tb = int(fetch * 1024 * ff + write * 1024 * wf)
+        total += tb
+        alg += ab
+        rec["kernels"][kern] = {"dispatches": [n1, n2], "fetch_kib": round(fetch, 1),
+                                "write_kib": round(write, 1), "traffic_bytes": tb,
+                                "algorithmic_bytes": ab, "ratio": round(tb / ab, 3)}
+    rec["traffic_bytes"] = total
+    rec["algorithmic_bytes"] = alg
+    rec["source_fingerprint"] = source_fingerprint("ln")
     return rec
 
 
@@ -770,6 +813,9 @@ def main():
         if args.traffic_step == "lamb":
             rec = lamb_traffic_summary(args.traffic_summary, args.workload)
             what = "the LAMB step's moments and update kernels"
+        elif args.traffic_step == "ln":
+            rec = ln_traffic_summary(args.traffic_summary, args.workload)
+            what = "the LayerNorm forward, backward and column-sum kernels"
         else:
             rec = traffic_summary(args.traffic_summary, args.workload, args.traffic_step)
             what = f"the {args.traffic_step} GEMM"

@@ -217,33 +217,12 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
   const int cb = (int)blockIdx.x % ncb, chunk = (int)blockIdx.x / ncb;
   const int r0 = chunk * kApplyRows;
   const int nr = min(kApplyRows, rows - r0);
-  {
-    // 16 threads per row, each summing every 16th group, then a butterfly
-    const int rr = threadIdx.x >> 4, l = threadIdx.x & 15;
-    float s1 = 0.f, s2 = 0.f;
-    if (rr < nr)
-      for (int g = l; g < ngroups; g += 16) {
-        const float2 p = rowpart[(size_t)(r0 + rr) * ngroups + g];
-        s1 += p.x;
-        s2 += p.y;
-      }
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) {
-      s1 += __shfl_xor(s1, off, 16);
-      s2 += __shfl_xor(s2, off, 16);
-    }
-    if (l == 0) {
-      stat[rr][0] = s1 / (float)H;
-      stat[rr][1] = s2 / (float)H;
-      stat[rr][2] = rr < nr ? mean[r0 + rr] : 0.f;
-      stat[rr][3] = rr < nr ? rstd[r0 + rr] : 0.f;
-    }
-  }
-  __syncthreads();
   const int c = (cb * kApplyThreads + threadIdx.x) * 8;
-  if (c >= H) return;
+  const bool col_ok = c < H;
   float gm[8], adg[8], adb[8], ady[8];
-  load8(gamma + c, gm);
+  // the first rows' loads go out before the row terms are folded (they do
+  // not depend on them), so their latency overlaps the fold and its barrier
+  if (col_ok) load8(gamma + c, gm);
 #pragma unroll
   for (int e = 0; e < 8; ++e) adg[e] = adb[e] = ady[e] = 0.f;
   // Rows in batches of kBatch, double-buffered: the next batch's loads are
@@ -263,7 +242,32 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
       yv[buf][i].load(dy + off);
     }
   };
-  load_batch(0, 0);
+  if (col_ok) load_batch(0, 0);
+  {
+    // 16 threads per row, each summing every 16th group, then a butterfly
+    const int rr = threadIdx.x >> 4, l = threadIdx.x & 15;
+    float s1 = 0.f, s2 = 0.f;
+    if (rr < nr)
+      for (int g = l; g < ngroups; g += 16) {
+        const float2 p = rowpart[(size_t)(r0 + rr) * ngroups + g];
+        s1 += p.x;
+        s2 += p.y;
+      }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) {
+      s1 += __shfl_xor(s1, off, 16);
+      s2 += __shfl_xor(s2, off, 16);
+    }
+    if (l == 0 && rr < kApplyRows) {
+      stat[rr][0] = s1 / (float)H;
+      stat[rr][1] = s2 / (float)H;
+      stat[rr][2] = rr < nr ? mean[r0 + rr] : 0.f;
+      stat[rr][3] = rr < nr ? rstd[r0 + rr] : 0.f;
+    }
+  }
+  __syncthreads();
+  if (!col_ok) return;
+
 #pragma unroll
   for (int bt = 0; bt < kBatches; ++bt) {
     const int cur = bt & 1;
@@ -284,7 +288,16 @@ __global__ __launch_bounds__(kApplyThreads) void ln_bwd_apply(
           ady[e] += yv[cur][i][e];
           o[e] = yv[cur][i][e] + rs * (gm[e] * d - m1 - xh * m2);
         }
-        store8(dx + off, o);
+        {
+          u32x4 wv;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) wv[q] = pack_bf2(o[2 * q], o[2 * q + 1]);
+          // dx is not read again here: streamed past the caches
+          if constexpr (sizeof(T) == 2)
+            __builtin_nontemporal_store(wv, reinterpret_cast<u32x4*>(dx + off));
+          else
+            store8(dx + off, o);
+        }
       }
     }
   }
