@@ -188,8 +188,10 @@ pb_status pblock_forward_timed(const pb_config* cfg, const void* x,
  *   dz  [T, N_in]  act  dQ | dK | dV | dU, the in-projection's output
  *                       gradient (dQ, dK, dV from the attention backward)
  *   dh  [T, H]     act  the LayerNorm output's gradient
+ *   delta [batch, heads, seq] fp32  the attention backward's row terms
+ *                       rowsum(dO O) per head
  * They hold these values once the backward call has passed on its stream,
- * until the workspace is used again.  offsets must hold 3 entries.  Host
+ * until the workspace is used again.  offsets must hold 4 entries.  Host
  * only; for inspection and tests. */
 pb_status pblock_workspace_offsets(const pb_config* cfg, size_t* offsets);
 

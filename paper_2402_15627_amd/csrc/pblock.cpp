@@ -351,6 +351,7 @@ pb_status pblock_workspace_offsets(const pb_config* cfg, size_t* offsets) {
   offsets[0] = W.d_o;
   offsets[1] = W.dz;
   offsets[2] = W.dh;
+  offsets[3] = W.delta;
   return PB_OK;
 }
 

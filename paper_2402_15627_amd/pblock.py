@@ -24,7 +24,7 @@ ATTN_WS_FORWARD, ATTN_WS_BACKWARD_MIN, ATTN_WS_BACKWARD = 0, 1, 2
 STATUS = {0: "PB_OK", 1: "PB_ERR_INVALID_ARG", 2: "PB_ERR_UNSUPPORTED", 3: "PB_ERR_WORKSPACE",
           4: "PB_ERR_HIP"}
 SAVED_REGIONS = ("h", "z", "c", "mean", "rstd", "lse")
-WORKSPACE_REGIONS = ("d_o", "dz", "dh")
+WORKSPACE_REGIONS = ("d_o", "dz", "dh", "delta")
 SERIAL_SAVED_REGIONS = ("h1", "z", "c", "mean1", "rstd1", "lse", "x1", "h2", "mean2", "rstd2")
 
 # Every function the header declares (checked by the CPU tests).
@@ -216,7 +216,7 @@ def pblock_workspace_bytes(cfg: PbConfig, mode: int) -> int:
 
 
 def pblock_workspace_offsets(cfg: PbConfig) -> dict:
-    """Offsets of d_o, dz and dh in the backward workspace."""
+    """Offsets of d_o, dz, dh and delta in the backward workspace."""
     arr = (c_size_t * len(WORKSPACE_REGIONS))()
     _check(load_library().pblock_workspace_offsets(ctypes.byref(cfg), arr))
     return dict(zip(WORKSPACE_REGIONS, list(arr)))
@@ -543,12 +543,17 @@ class ParallelBlock:
         return _stash_view(self.cfg, self.saved, pblock_saved_offsets(self.cfg), name)
 
     def workspace_view(self, name: str):
-        """A typed view of one backward intermediate (d_o, dz, dh) in the
-        workspace, valid after backward() until the next call."""
+        """A typed view of one backward intermediate (d_o, dz, dh, delta) in
+        the workspace, valid after backward() until the next call."""
         import torch
         cfg = self.cfg
         T, H, A = cfg.batch * cfg.seq, cfg.hidden, cfg.heads * cfg.head_dim
         act = torch.bfloat16 if cfg.dtype == PB_BF16 else torch.float32
+        if name == "delta":
+            off = pblock_workspace_offsets(cfg)["delta"]
+            n = cfg.batch * cfg.heads * cfg.seq
+            return self.ws[off:off + 4 * n].view(torch.float32).view(cfg.batch, cfg.heads,
+                                                                     cfg.seq)
         cols = {"d_o": A, "dz": 3 * A + cfg.ffn, "dh": H}[name]
         off = pblock_workspace_offsets(cfg)[name]
         nbytes = T * cols * torch.empty((), dtype=act).element_size()

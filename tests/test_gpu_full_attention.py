@@ -11,7 +11,10 @@ intermediates is compared with the fp64 oracle computed for that head alone
   forward   O (the stash's C[:, head]) and lse (the stash), plus the head's
             Q, K, V in the stash's Z;
   backward  dO (the workspace's d_o[:, head], from the dC GEMM) and dQ, dK,
-            dV (the workspace's dZ[:, head], from the attention backward).
+            dV (the workspace's dZ[:, head], from the attention backward);
+            the row terms delta = rowsum(dO O) that the dC GEMM's epilogue
+            forms, against the same sum over the stored dO and O (1e-5 of
+            max |delta|: fp32 summation order only).
 
 Normwise per tensor <= 2e-2 (bf16 storage, fp32 accumulation); lse, a log,
 within 2e-2 absolute.
@@ -84,3 +87,11 @@ def test_full_size_attention_per_head(name, heads):
         assert not bad, (hd, bad)
         for k, v in got.items():
             assert torch.isfinite(v).all(), (hd, k)
+        # the backward's row terms delta = rowsum(dO O) of this head (formed in
+        # the dC GEMM's epilogue), against the same sum over the block's own
+        # stored dO and O in fp64
+        dref = (d_o[:, cols].double() * c[:, cols].double()).sum(dim=1).cpu().numpy()
+        dgot = blk.workspace_view("delta")[0, hd].double().cpu().numpy()
+        ed = float(np.abs(dgot - dref).max() / max(np.abs(dref).max(), 1e-30))
+        _say(f"      head {hd} delta vs rowsum(dO O): {ed:.2e}")
+        assert ed <= 1e-5, (hd, ed)
