@@ -1117,8 +1117,27 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   e4.rstd = rstd1;
   e4.rowpart = rowpart;
   e4.rowpart_ld = pb::ln_row_groups(H);
-  const SerialBwdGemms G = serial_bwd_gemms(
+  SerialBwdGemms G = serial_bwd_gemms(
       d, SerialBwdOperands{dy, dx1, c, dz, h1, h2, w_in, w_out}, e1, wd, e2, wu, e3, wo, e4, wq);
+  // As in the parallel block: db_in from the row sums of the weight
+  // gradients' A operands (dU^T in dW_up, dQKV^T in dW_qkv) when both share
+  // launches, and the attention backward's delta from the dO GEMM's epilogue
+  const bool db_in_fused = pb::gemm_pair_supported(dt, G.dh2, G.dw_up) &&
+                           pb::gemm_pair_supported(dt, G.dh1, G.dw_qkv);
+  if (db_in_fused) {
+    G.dw_up.ep.rowsum = db_in + 3LL * A;
+    G.dw_qkv.ep.rowsum = db_in;
+  }
+  const bool delta_in_do = pb::gemm_pair_supported(dt, G.d_o, G.dw_o) &&
+                           (d.d == 64 || d.d == 128) && A % 128 == 0;
+  if (delta_in_do) {
+    G.d_o.ep.o_rows = c;  // O = C[:, :A]
+    G.d_o.ep.ld_o_rows = K_out;
+    G.d_o.ep.delta = delta;
+    G.d_o.ep.delta_seq = (int)d.S;
+    G.d_o.ep.delta_heads = (int)d.heads;
+    G.d_o.ep.delta_hd = (int)d.d;
+  }
   auto run = [&](const pb::GemmSpec& g) {
     pb::launch_gemm(dt, g.epi, g.a_kcontig, g.b_kcontig, g.A, g.lda, g.B, g.ldb, g.M, g.N, g.K,
                     g.ep, split_ws, split_f, stream);
@@ -1142,15 +1161,15 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   // attention: dO = dx1 W_o, then dQ, dK, dV -> dZ[:, :3A]
   run_with(G.d_o, G.dw_o);
   pb::launch_attn_backward(dt, attn_shape(d), z, at(z, A, e), at(z, 2LL * A, e), N_in, c, K_out,
-                           d_o, A, lse, delta, false, dz, at(dz, A, e), at(dz, 2LL * A, e), N_in,
-                           split_ws, split_f * 4, stream);
+                           d_o, A, lse, delta, delta_in_do, dz, at(dz, A, e), at(dz, 2LL * A, e),
+                           N_in, split_ws, split_f * 4, stream);
   run_with(G.dh1, G.dw_qkv);
   // dx = dx1 + LN1'(dh1); dgamma1, dbeta1, and db_o = sum dx1
   pb::launch_ln_backward(dt, x, mean1, rstd1, ln1_gamma, dh, rowpart, dx1, dx, pdg, pdb, pdy, T,
                          H, stream);
   pb::launch_colsum3_f32(pdg, pdb, pdy, H, nblk, H, dln1_gamma, dln1_beta, db_o, stream);
   // bias gradients of the input projections: db_in = sum over tokens of dZ
-  pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
+  if (!db_in_fused) pb::launch_colsum(dt, dz, N_in, T, N_in, part, db_in, stream);
   // weight gradients that did not share a launch, last
   for (int i = 0; i < n_deferred; ++i) run(*deferred[i]);
   return finish_launches();
