@@ -104,15 +104,19 @@ constexpr int kTileBytes = kBM * kBK * 2;  // one operand tile (32 KB)
 PB_DEV int swz(int row, int c) { return c ^ ((row ^ (row >> 3)) & 7); }
 
 // Tile order.  Workgroup b runs on XCD b % 8; xcd_remap gives each XCD a
-// contiguous run of logical ids, and tile_of walks logical ids in groups of 8
+// contiguous run of logical ids, and tile_of walks logical ids in groups of G
 // tile-rows, so concurrently running workgroups on one XCD share operand
-// strips in its L2.
+// strips in its L2.  The LDS-DMA GEMMs take G = tile_group(epilogue): groups
+// of 4 rows (a 32-workgroup XCD share spans 4 x 8 tiles) measured faster for
+// the backward's GEMMs and the in-projection, groups of 8 for the
+// out-projection (BiasResid); groups of 2 or 16 were slower for all.
 PB_DEV int xcd_remap(int bid, int n) {
   const int q = n / 8, r = n % 8, x = bid % 8;
   return x * q + min(x, r) + bid / 8;
 }
+constexpr int tile_group(Epi e) { return e == Epi::BiasResid ? 8 : 4; }
+template <int G = 8>
 PB_DEV void tile_of(int lid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  constexpr int G = 8;
   const int per_group = G * tiles_n;
   const int group = lid / per_group;
   const int first_m = group * G;
@@ -652,7 +656,7 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
 
   const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
   int tm, tn;
-  tile_of(lid, tiles_m, tiles_n, tm, tn);
+  tile_of<tile_group(EPI)>(lid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
@@ -898,7 +902,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_pair(DmaGemm g1, in
   if constexpr (E2 == Epi::StoreF32) {
     // the second GEMM's row sums, when asked for, from its first tile column
     int tm, tn;
-    tile_of(lid, (g2.M + kBM - 1) / kBM, (g2.N + kBN - 1) / kBN, tm, tn);
+    tile_of<tile_group(E2)>(lid, (g2.M + kBM - 1) / kBM, (g2.N + kBN - 1) / kBN, tm, tn);
     if (g2.ep.rowsum && tn == 0) {
       dma_gemm_item<AK2, BK2, E2, GT, true>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep, lid, -1,
                                             0, g2.K / kBK, tiles2, 1, nullptr);
@@ -920,7 +924,7 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ p
   const int g = (blockIdx.x % 64) * 256 + threadIdx.x;  // 0 .. 16383
   const int row = g / (kBN / 4), col = (g % (kBN / 4)) * 4;
   int tm, tn;
-  tile_of(n_full + t_local, tiles_m, tiles_n, tm, tn);
+  tile_of<tile_group(EPI)>(n_full + t_local, tiles_m, tiles_n, tm, tn);
   const int m = tm * kBM + row, n = tn * kBN + col;
   const bool ok = m < M && n < N;
   float v[4] = {0.f, 0.f, 0.f, 0.f};
