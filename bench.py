@@ -67,6 +67,8 @@ METRIC = "parallel-block fwd+bwd TFLOP/s and % of MI355X bf16 MFMA peak"
 # launch_gemm_pair): dC with dW_out, dh with dW_in; in the serial block each
 # weight gradient with the GEMM before it.
 GEMM_PAIRS = {"dc": "dw_out", "dh": "dw_in"}
+# Workgroups of a persistent shared launch: one per CU.
+PERSISTENT_WORKGROUPS = 256
 SERIAL_GEMM_PAIRS = {"dg": "dw_down", "dh2": "dw_up", "d_o": "dw_o", "dh1": "dw_qkv"}
 
 
@@ -190,8 +192,11 @@ def gemm_step_of(name, grid, s, block="parallel"):
     steps = gemm_steps(s, block)
     if "gemm_bf16_dma_pair" in name:
         tiles = lambda st: gemm_tiles(*steps[st])  # noqa: E731
+        # one workgroup per tile of either GEMM, or (persistent) one per CU
+        wgs = lambda a, b: (min(PERSISTENT_WORKGROUPS, tiles(a) + tiles(b))  # noqa: E731
+                            if "persistent" in name else tiles(a) + tiles(b))
         hits = [f"{a}+{b}" for a, b in paired_steps(s, block).items()
-                if GEMM_SIGNATURE[a] in name and (tiles(a) + tiles(b)) * 512 == grid]
+                if GEMM_SIGNATURE[a] in name and wgs(a, b) * 512 == grid]
         return "/".join(hits)
     hits = [st for st, mnk in steps.items()
             if "gemm_bf16" in name and GEMM_SIGNATURE[st] in name

@@ -199,7 +199,12 @@ pb_status pblock_workspace_offsets(const pb_config* cfg, size_t* offsets);
  * parameter, given the stash of the matching forward call.  dx is in the
  * activation dtype; the six parameter gradients are fp32 and overwritten.
  * ws should hold pblock_workspace_bytes(cfg, PB_WS_BACKWARD) bytes (fewer,
- * down to the size without the GEMM partial-tile region, also works). */
+ * down to the size without the GEMM partial-tile region, also works).
+ * Where dC and dW_out (dh and dW_in) share a launch, that launch is
+ * persistent: one workgroup per CU takes tiles from per-XCD queues whose
+ * heads live in ws and are zeroed by the call itself, so ws needs no
+ * initialisation and two calls in flight at once need separate workspaces
+ * (as for every other region of ws). */
 pb_status pblock_backward(const pb_config* cfg, const void* x,
                           const void* ln_gamma, const void* ln_beta,
                           const void* w_in, const void* b_in,

@@ -99,6 +99,8 @@ constexpr int kThreads = 64 * kWavesM * kWavesN;
 constexpr int kWTM = kBM / kWavesM, kWTN = kBN / kWavesN;
 constexpr int kTM = kWTM / 32, kTN = kWTN / 32;
 constexpr int kTileBytes = kBM * kBK * 2;  // one operand tile (32 KB)
+// CUs of MI355X; the DMA kernels' 128 KB of LDS allows one workgroup per CU.
+constexpr int kCUs = 256;
 
 // 16-byte chunk c (0..7) of LDS row `row` lives at physical chunk swz(row, c).
 PB_DEV int swz(int row, int c) { return c ^ ((row ^ (row >> 3)) & 7); }
@@ -645,10 +647,16 @@ PB_DEV float sum_bf16x8(const bf16x8& p, float acc) {
 // RS (StoreF32 only): also the row sums of A over this work item's K-tiles,
 // rowsum[m] = sum_k A(m, k), from the A fragments the MFMAs consume (the
 // caller sets RS for the tiles of the first tile column only).
+// Persistent launches pass qctr: thread 0 then takes the next ticket of that
+// queue (*qticket) right after the main loop, so the atomic's latency is
+// spent under the epilogue; and tid_in, the thread index the caller keeps
+// out of the compiler's sight (see gemm_bf16_dma_pair_persistent).
 template <bool AK, bool BK, Epi EPI, bool GT, bool RS = false>
 PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb,
                           int M, int N, const EpiArgs& ep, int lid, int slice, int kt0, int kt1,
-                          int n_full, int splits, float* __restrict__ part) {
+                          int n_full, int splits, float* __restrict__ part,
+                          int* __restrict__ qctr = nullptr, int* qticket = nullptr,
+                          int tid_in = -1) {
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(PB_LDS unsigned char*)smem;
   auto a_off = [&](int s) { return (2 * s) * kDTile; };
@@ -658,8 +666,9 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   int tm, tn;
   tile_of<tile_group(EPI)>(lid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int tid = tid_in >= 0 ? tid_in : (int)threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int wm = (wave % kWavesM) * kWTM, wn = (wave / kWavesM) * kWTN;
 
   // K-tiles [kt0, kt1) of this work item
@@ -828,6 +837,7 @@ PB_DEV void dma_gemm_item(const bf16* __restrict__ A, int lda, const bf16* __res
   }
 
   block_barrier();  // every wave is done with the main loop's LDS
+  if (qctr && tid == 0) *qticket = atomicAdd(qctr, 1);
   if constexpr (RS) {
     // lanes l, l + 16, l + 32, l + 48 hold the same row's k groups; the four
     // waves of the first tile column (wn = 0) cover the tile's 256 rows
@@ -911,6 +921,120 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_pair(DmaGemm g1, in
   }
   dma_gemm_item<AK2, BK2, E2, GT>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep, lid, -1, 0,
                                   g2.K / kBK, tiles2, 1, nullptr);
+}
+
+// Persistent form of the pair launch: one workgroup per CU takes work items
+// until none is left.  The items (the first GEMM's tiles, then the
+// second's) are dealt to eight queues, one per XCD, each holding the tiles
+// the launch above gives that XCD (xcd_remap); a workgroup reads its XCD
+// from the hardware, takes items from that queue and, once it is empty,
+// from the others.  So a slower XCD hands its last items to faster ones
+// (workgroup clock stamps showed XCDs 5-9% apart in K-tile time, and the
+// launch waiting on the slowest), and no workgroup pays a launch and
+// prologue between items.  The queue heads are kQueueInts ints that must be
+// zero when the launch starts (launch_queue_reset); the launch leaves them
+// non-zero.  Results do not depend on which workgroup takes an item.
+struct PairArgs {
+  DmaGemm g1;
+  int tiles1;
+  DmaGemm g2;
+  int tiles2;
+  int* queue;
+};
+typedef const PairArgs __attribute__((address_space(4)))* PairArgsPtr;
+// Items [queue_start, queue_start + queue_count) of n go to XCD q's queue.
+PB_DEV int queue_start(int n, int q) { return q * (n / 8) + min(q, n % 8); }
+PB_DEV int queue_count(int n, int q) { return n / 8 + (q < n % 8 ? 1 : 0); }
+template <bool AK1, bool BK1, Epi E1, bool AK2, bool BK2, Epi E2, bool GT>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_pair_persistent(PairArgs args) {
+  __shared__ int s_item;
+  const int tiles1 = args.tiles1, tiles2 = args.tiles2;
+  int* const queue = args.queue;
+  // XCC_ID hardware register (bits 3:0: the XCD this wave runs on)
+  const int x = __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 7;
+  auto item_of = [&](int q, int i) {  // i-th item of queue q, or -1 past its end
+    const int c1 = queue_count(tiles1, q);
+    if (i < c1) return queue_start(tiles1, q) + i;
+    if (i < c1 + queue_count(tiles2, q)) return tiles1 + queue_start(tiles2, q) + (i - c1);
+    return -1;
+  };
+  // Wave 0: the item of a ticket of the own queue or, past its end, one taken
+  // from the first other queue (in XCD order after x) whose head has not
+  // passed its end; every failed take moves a head past its end, so the loop
+  // ends.
+  auto resolve = [&](int ticket) {
+    const int lane = threadIdx.x & 63;
+    int item = item_of(x, ticket);
+    while (item < 0) {
+      int left = 0;
+      if (lane < 8)
+        left = queue_count(tiles1, lane) + queue_count(tiles2, lane) -
+               __hip_atomic_load(queue + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned long long m = __ballot(left > 0) & 0xffull;
+      if (!m) break;
+      m = ((m >> x) | (m << (8 - x))) & 0xffull;  // bit v: queue x + v
+      const int q = (x + __builtin_ctzll(m)) & 7;
+      int i = 0;
+      if (lane == 0) i = atomicAdd(queue + q, 1);
+      item = item_of(q, __shfl(i, 0, 64));
+    }
+    return item;
+  };
+  if (threadIdx.x < 64) {
+    int t = 0;
+    if (threadIdx.x == 0) t = atomicAdd(queue + x, 1);
+    const int it = resolve(__shfl(t, 0, 64));
+    if (threadIdx.x == 0) s_item = it;
+  }
+  __syncthreads();
+  int item = __builtin_amdgcn_readfirstlane(s_item);
+  while (item >= 0) {
+    // Thread 0's s_item write for the next item comes after this item's
+    // barriers, which every thread reaches only after reading s_item above.
+    int ticket = 0;
+    // The thread index and the GEMM descriptions are taken afresh for every
+    // item (the descriptions by scalar loads of the kernel arguments), hidden
+    // from the compiler by empty asm: otherwise it keeps what it derives from
+    // them live across items, runs out of registers and spills, and a reload
+    // before the main loop put a full memory wait into every K-tile.
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    PairArgsPtr pa = (PairArgsPtr)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(pa));
+    const PairArgs* ap = (const PairArgs*)pa;
+    if (item < tiles1) {
+      const DmaGemm g1 = ap->g1;
+      dma_gemm_item<AK1, BK1, E1, GT>(g1.A, g1.lda, g1.B, g1.ldb, g1.M, g1.N, g1.ep, item, -1, 0,
+                                      g1.K / kBK, tiles1, 1, nullptr, queue + x, &ticket, tid);
+    } else {
+      const DmaGemm g2 = ap->g2;
+      const int lid = item - tiles1;
+      bool done = false;
+      if constexpr (E2 == Epi::StoreF32) {
+        int tm, tn;
+        tile_of<tile_group(E2)>(lid, (g2.M + kBM - 1) / kBM, (g2.N + kBN - 1) / kBN, tm, tn);
+        if (g2.ep.rowsum && tn == 0) {
+          dma_gemm_item<AK2, BK2, E2, GT, true>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep,
+                                                lid, -1, 0, g2.K / kBK, tiles2, 1, nullptr,
+                                                queue + x, &ticket, tid);
+          done = true;
+        }
+      }
+      if (!done)
+        dma_gemm_item<AK2, BK2, E2, GT>(g2.A, g2.lda, g2.B, g2.ldb, g2.M, g2.N, g2.ep, lid, -1, 0,
+                                        g2.K / kBK, tiles2, 1, nullptr, queue + x, &ticket, tid);
+    }
+    if (threadIdx.x < 64) {
+      const int it = resolve(__shfl(ticket, 0, 64));
+      if (threadIdx.x == 0) s_item = it;
+    }
+    __syncthreads();
+    item = __builtin_amdgcn_readfirstlane(s_item);
+  }
+}
+
+__global__ void queue_reset_kernel(int* __restrict__ q, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) q[i] = 0;
 }
 
 // Sum of the K-slice partials of each tail tile, in slice order (so the
@@ -1058,7 +1182,6 @@ SplitPlan gemm_split_plan(Dt dt, int M, int N, int K) {
   const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   SplitPlan none{tiles, 0, 1};
   if (dt != Dt::BF16 || K % kBK != 0) return none;
-  constexpr int kCUs = 256;  // MI355X; one workgroup per CU
   const int nk = K / kBK;
   const int n_full = tiles / kCUs * kCUs;
   const int tail = tiles - n_full;
@@ -1117,7 +1240,11 @@ bool gemm_pair_supported(Dt dt, const GemmSpec& g1, const GemmSpec& g2) {
          !g2.a_kcontig && !g2.b_kcontig && g2.epi == Epi::StoreF32;
 }
 
-bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, hipStream_t s) {
+void launch_queue_reset(int* queue, int n, hipStream_t s) {
+  if (n > 0) queue_reset_kernel<<<1, 64, 0, s>>>(queue, n);
+}
+
+bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, int* queue, hipStream_t s) {
   if (!gemm_pair_supported(dt, g1, g2)) return false;
   auto desc = [](const GemmSpec& g) {
     return DmaGemm{(const bf16*)g.A, g.lda, (const bf16*)g.B, g.ldb, g.M, g.N, g.K, g.ep};
@@ -1128,6 +1255,18 @@ bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, hipStream_t
   const DmaGemm d1 = desc(g1), d2 = desc(g2);
   const int t1 = tiles(g1), t2 = tiles(g2);
   const size_t lds = 4 * (size_t)kTileBytes;
+  // (the erf GeLU' form keeps the plain launch: its persistent build spills)
+  if (queue && (g1.epi == Epi::LnGrad || g1.ep.gelu_tanh)) {
+    const PairArgs pa{d1, t1, d2, t2, queue};
+    const int grid = std::min(kCUs, t1 + t2);
+    if (g1.epi == Epi::LnGrad)
+      gemm_bf16_dma_pair_persistent<true, false, Epi::LnGrad, false, false, Epi::StoreF32, true>
+          <<<grid, kThreads, lds, s>>>(pa);
+    else
+      gemm_bf16_dma_pair_persistent<true, false, Epi::DgeluSplit, false, false, Epi::StoreF32,
+                                    true><<<grid, kThreads, lds, s>>>(pa);
+    return true;
+  }
   if (g1.epi == Epi::LnGrad)
     gemm_bf16_dma_pair<true, false, Epi::LnGrad, false, false, Epi::StoreF32, true>
         <<<t1 + t2, kThreads, lds, s>>>(d1, t1, d2, t2);

@@ -173,8 +173,18 @@ struct GemmSpec {
   int M, N, K;
   EpiArgs ep;
 };
+//
+// With queue non-NULL the launch is persistent: one workgroup per CU takes
+// tiles from per-XCD queues until none is left, so XCDs that run slower hand
+// their last tiles to the others.  queue points to kQueueInts ints (device
+// memory) that must be zero when the launch runs, e.g. from
+// launch_queue_reset earlier on the same stream; the launch leaves them
+// non-zero, and two launches in flight at once need separate queues.  The
+// results are the same bits either way.
+constexpr int kQueueInts = 8;
+void launch_queue_reset(int* queue, int n, hipStream_t s);  // n ints = 0 (a kernel)
 bool gemm_pair_supported(Dt dt, const GemmSpec& g1, const GemmSpec& g2);
-bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, hipStream_t s);
+bool launch_gemm_pair(Dt dt, const GemmSpec& g1, const GemmSpec& g2, int* queue, hipStream_t s);
 
 // -------------------------------------------------------------- attention
 // Causal sliding-window attention over [batch, seq] rows; q/k/v/o/do/dq/dk/dv

@@ -148,8 +148,13 @@ size_t split_bytes_bwd(const Dims& d, pb::Dt dt) {
   return std::max(m * 4, pb::attn_bwd_partial_bytes(a, pb::attn_bwd_split_plan(dt, a)));
 }
 
+// Queue heads of the backward's persistent GEMM launches: kQueueInts ints per
+// launch, zeroed at the start of each call.
+constexpr int kBwdQueueSets = 4;
+constexpr size_t kBwdQueueBytes = kBwdQueueSets * pb::kQueueInts * sizeof(int);
+
 struct BwdLayout {
-  size_t d_o, dz, dh, delta, rowpart, pdg, pdb, pdy, part, split, base, total;
+  size_t d_o, dz, dh, delta, rowpart, pdg, pdb, pdy, part, queue, split, base, total;
 };
 BwdLayout bwd_layout(const Dims& d) {
   BwdLayout L;
@@ -174,6 +179,7 @@ BwdLayout bwd_layout(const Dims& d) {
   if (p2 > part) part = p2;
   if (p3 > part) part = p3;
   L.part = take(part * 4);
+  L.queue = take(kBwdQueueBytes);
   L.base = o;  // required; the tail-split region after it is optional
   L.split = take(split_bytes_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32));
   L.total = o;
@@ -227,7 +233,7 @@ size_t serial_split_bwd(const Dims& d, pb::Dt dt) {
 // LayerNorms), dx1, softmax row terms, LN row terms, LN partial column sums,
 // column-sum scratch, then the optional split region.
 struct SerialBwdLayout {
-  size_t d_o, dz, dh, dx1, delta, rowpart, pdg, pdb, pdy, part, split, base, total;
+  size_t d_o, dz, dh, dx1, delta, rowpart, pdg, pdb, pdy, part, queue, split, base, total;
 };
 SerialBwdLayout serial_bwd_layout(const Dims& d) {
   SerialBwdLayout L;
@@ -250,6 +256,7 @@ SerialBwdLayout serial_bwd_layout(const Dims& d) {
   size_t part = pb::colsum_partial_floats((int)d.T, (int)d.N_in);
   part = std::max(part, pb::colsum_partial_floats(nblk, (int)d.H));
   L.part = take(part * 4);
+  L.queue = take(kBwdQueueBytes);
   L.base = o;
   L.split = take(serial_split_bwd(d, d.esz == 2 ? pb::Dt::BF16 : pb::Dt::F32));
   L.total = o;
@@ -606,6 +613,7 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   float* pdb = (float*)(wb + W.pdb);
   float* pdy = (float*)(wb + W.pdy);
   float* part = (float*)(wb + W.part);
+  int* queue = (int*)(wb + W.queue);
   float* split_ws = (float*)(wb + W.split);
   const size_t split_f = ws_bytes >= W.total ? (W.total - W.split) / 4 : 0;
   const int T = (int)d.T, H = (int)d.H, A = (int)d.A, N_in = (int)d.N_in, K_out = (int)d.K_out;
@@ -672,8 +680,10 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   }
   {
     StepScope sc(step_ev, PB_STEP_DC, stream);  // with dW_out when they share a launch
+    // the shared launches are persistent: their queue heads start at zero
+    if (pair_out || pair_in) pb::launch_queue_reset(queue, 2 * pb::kQueueInts, stream);
     if (pair_out)
-      pb::launch_gemm_pair(dt, g_dc, g_dwo, stream);
+      pb::launch_gemm_pair(dt, g_dc, g_dwo, queue, stream);
     else
       run(g_dc);
   }
@@ -690,7 +700,7 @@ pb_status pblock_backward_timed(const pb_config* cfg, const void* x, const void*
   {
     StepScope sc(step_ev, PB_STEP_DH, stream);  // with dW_in when they share a launch
     if (pair_in)
-      pb::launch_gemm_pair(dt, g_dh, g_dwi, stream);
+      pb::launch_gemm_pair(dt, g_dh, g_dwi, queue + pb::kQueueInts, stream);
     else
       run(g_dh);
   }
@@ -1058,6 +1068,7 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   float* pdb = (float*)(wb + W.pdb);
   float* pdy = (float*)(wb + W.pdy);
   float* part = (float*)(wb + W.part);
+  int* queue = (int*)(wb + W.queue);
   float* split_ws = (float*)(wb + W.split);
   const size_t split_f = ws_bytes >= W.total ? (W.total - W.split) / 4 : 0;
   const int T = (int)d.T, H = (int)d.H, A = (int)d.A, F = (int)d.F, N_in = (int)d.N_in,
@@ -1144,8 +1155,15 @@ pb_status pblock_serial_backward(const pb_config* cfg, const void* x, const void
   };
   const pb::GemmSpec* deferred[4];
   int n_deferred = 0;
+  // the shared launches are persistent, each with its own queue heads,
+  // zeroed here
+  static_assert(kBwdQueueSets >= 4, "one queue per shared launch");
+  if (pb::gemm_pair_supported(dt, G.dg, G.dw_down) || pb::gemm_pair_supported(dt, G.dh2, G.dw_up) ||
+      pb::gemm_pair_supported(dt, G.d_o, G.dw_o) || pb::gemm_pair_supported(dt, G.dh1, G.dw_qkv))
+    pb::launch_queue_reset(queue, 4 * pb::kQueueInts, stream);
+  int n_pairs = 0;
   auto run_with = [&](const pb::GemmSpec& g, const pb::GemmSpec& wg) {
-    if (!pb::launch_gemm_pair(dt, g, wg, stream)) {
+    if (!pb::launch_gemm_pair(dt, g, wg, queue + pb::kQueueInts * n_pairs++, stream)) {
       run(g);
       deferred[n_deferred++] = &wg;
     }

@@ -98,6 +98,14 @@ def load_library(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run __graft_entry__.build() "
                           f"(or python -m paper_2402_15627_amd.build)")
+    # torch first, when it is installed: the library then binds to the HIP
+    # runtime torch has loaded, and both see the same devices and streams (a
+    # library loaded before torch brought in a second runtime that reported
+    # no device)
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     P = c_void_p
     cfgp = POINTER(PbConfig)

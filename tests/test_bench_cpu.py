@@ -108,6 +108,13 @@ def test_paired_gemm_launches_are_labelled_and_counted():
     dc = name.replace("(pb::Epi)4", "(pb::Epi)3")
     # dC: 8 x 30 tiles, dW_out: 48 x 30 tiles
     assert bench.gemm_step_of(dc, (240 + 1440) * 512, s) == "dc+dw_out"
+    # the persistent form: one workgroup per CU
+    pers = name.replace("gemm_bf16_dma_pair<", "gemm_bf16_dma_pair_persistent<")
+    assert bench.gemm_step_of(pers, 256 * 512, s) == "dh+dw_in"
+    assert bench.gemm_step_of(pers, (384 + 2016) * 512, s) == ""
+    # serial block: dG + dW_down and dO + dW_o share the template and the grid
+    pers_dc = pers.replace("(pb::Epi)4", "(pb::Epi)3")
+    assert bench.gemm_step_of(pers_dc, 256 * 512, s, "serial") == "dg+dw_down/d_o+dw_o"
     work, plain = bench.step_work(s), bench._step_work(s)
     assert work["dh"][1] == plain["dh"][1] + plain["dw_in"][1] and work["dw_in"][1] == 0
     assert work["dc"][1] == plain["dc"][1] + plain["dw_out"][1] and work["dw_out"][1] == 0
