@@ -251,14 +251,12 @@ def traffic_summary(dirs, workload, step):
     parts = step.split("+")
     if any(p not in gemm_steps(s) for p in parts):
         raise SystemExit(f"traffic summary supports the GEMM steps and pairs, not {step}")
-    if len(parts) == 2:
-        tiles = lambda st: gemm_tiles(*gemm_steps(s)[st])  # noqa: E731
-        grid = (tiles(parts[0]) + tiles(parts[1])) * 512
-    else:
-        grid = gemm_grid_threads(*gemm_steps(s)[step])
     pick = lambda r: gemm_step_of(r["Kernel_Name"], int(r["Grid_Size"]), s) == step  # noqa: E731
     copy_pick = lambda r: "neg_kernel" in r["Kernel_Name"]  # noqa: E731
-    fetch, n1 = _per_dispatch(_counter_rows(dirs[0]), "FETCH_SIZE", pick)
+    fetch_rows = _counter_rows(dirs[0])
+    grid = max(int(r["Grid_Size"]) for r in fetch_rows if pick(r)) if any(
+        pick(r) for r in fetch_rows) else 0
+    fetch, n1 = _per_dispatch(fetch_rows, "FETCH_SIZE", pick)
     write, n2 = _per_dispatch(_counter_rows(dirs[1]), "WRITE_SIZE", pick)
     cfetch, _ = _per_dispatch(_counter_rows(dirs[2]), "FETCH_SIZE", copy_pick)
     cwrite, _ = _per_dispatch(_counter_rows(dirs[3]), "WRITE_SIZE", copy_pick)
