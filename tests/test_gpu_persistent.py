@@ -11,7 +11,10 @@ order in which workgroups take tiles changes from run to run, bitwise
 equality across these runs also shows that no result depends on the
 schedule.  Shapes have several hundred tiles per launch (every XCD queue
 non-empty, so workgroups take tiles from other XCDs' queues at the end) and
-a ragged one with tiles at the matrix edges.
+a ragged one with tiles at the matrix edges.  Two blocks whose backward
+calls run at the same time on two streams (separate workspaces, so separate
+queue heads; the two persistent launches share the CUs) must give the bits
+each gives alone.
 """
 import sys
 
@@ -82,3 +85,28 @@ def test_serial_backward_is_independent_of_queue_state(s):
     b1, b2 = _run(pb.SerialBlock, s, inp, 255)
     bad = _same(a1, a2) + _same(a1, b1) + _same(a1, b2)
     assert not bad, f"gradients differ between runs: {bad}"
+
+
+def test_backward_calls_on_two_streams_at_once():
+    import torch
+    from paper_2402_15627_amd import pblock as pb
+    s = SHAPES[0]
+    _say(f"[gpu] two concurrent backward calls {s.name}")
+    cfg = pb.config_from_shape(s)
+    blocks = [pb.ParallelBlock(cfg, to_device(s, make_inputs(s, seed=seed))) for seed in (7, 8)]
+    alone = []
+    for blk in blocks:
+        blk.forward()
+        blk.backward()
+        torch.cuda.synchronize()
+        alone.append(_grads(blk))
+    streams = [torch.cuda.Stream() for _ in blocks]
+    for st in streams:
+        st.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        for blk, st in zip(blocks, streams):
+            blk.backward(stream=st)
+    torch.cuda.synchronize()
+    for i, blk in enumerate(blocks):
+        bad = _same(alone[i], _grads(blk))
+        assert not bad, f"block {i}: gradients differ when run beside another call: {bad}"
