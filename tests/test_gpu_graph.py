@@ -4,7 +4,8 @@ the caller's stream (no allocation, synchronisation or memset; the
 backward's queue heads are zeroed by a kernel), so a graph of one step,
 replayed, must give the bits of the same step run eagerly.  Each replay
 follows eager work on the outputs (they are overwritten with garbage) and a
-synchronisation, and every replay is checked.
+synchronisation, and every replay is checked; the parallel block and the
+serial (standard pre-LN) block alike.
 """
 import sys
 
@@ -26,12 +27,15 @@ def _say(msg):
     sys.stdout.flush()
 
 
+@pytest.mark.parametrize("block", ["parallel", "serial"])
 @pytest.mark.parametrize("s", SHAPES, ids=[s.name for s in SHAPES])
-def test_block_step_replays_in_a_graph(s):
+def test_block_step_replays_in_a_graph(s, block):
     import torch
     from paper_2402_15627_amd import pblock as pb
-    _say(f"[gpu] graph capture of forward + backward {s.name}")
-    blk = pb.ParallelBlock(pb.config_from_shape(s), to_device(s, make_inputs(s, seed=11)))
+    _say(f"[gpu] graph capture of forward + backward {s.name} {block}")
+    cls = pb.ParallelBlock if block == "parallel" else pb.SerialBlock
+    inp = make_inputs(s, seed=11, serial=block == "serial")
+    blk = cls(pb.config_from_shape(s), to_device(s, inp))
     outs = [blk.y] + list(blk.grads.values())
 
     def snapshot():
