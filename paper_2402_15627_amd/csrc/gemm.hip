@@ -999,6 +999,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_dma_pair_persistent(Pai
     // before the main loop put a full memory wait into every K-tile.
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
+    // (PairArgs is the kernel's only argument, so it starts the segment)
     PairArgsPtr pa = (PairArgsPtr)__builtin_amdgcn_kernarg_segment_ptr();
     asm volatile("" : "+s"(pa));
     const PairArgs* ap = (const PairArgs*)pa;
