@@ -63,6 +63,10 @@
  * asynchronous on the given HIP stream; buffers must stay valid until the
  * stream has passed the call.  Other calls on disjoint buffers may run
  * concurrently.  Parameter gradients are overwritten, not accumulated.
+ * The block's forward and backward calls (parallel and serial) only launch
+ * kernels on the given stream (no allocation, memset, copy or
+ * synchronisation), so a caller may capture them into a HIP graph and
+ * replay it.
  *
  * ---------------------------------------------------------------- errors
  * Functions return a pb_status.  Arguments are checked on the host before any
